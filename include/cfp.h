@@ -1,0 +1,156 @@
+/*
+ * cfp.h -- C ABI of the min-plus chain search library (libcfp.so, gfx950).
+ *
+ * The library computes the plan search of CFP (arXiv 2504.00598, Sec. 4.4,
+ * "Plan Cost Estimation and Optimization"): a model is a chain of N blocks
+ * (ParallelBlocks or segments); block i picks one of K strategies; a plan
+ * x = (x_0 .. x_{N-1}) costs, by Eq. T,
+ *
+ *     T(x) = sum_i c[i][x_i] + sum_{i=1}^{N-1} R_{e(i)}[x_{i-1}][x_i]
+ *
+ * where c[i][s] is the profiled time of block i under strategy s (the
+ * paper's p_n + c_n, computation plus communication) and R_e[t][s] is the
+ * profiled resharding time from strategy t of a block to strategy s of the
+ * next one (the paper's r_n).  Resharding tables are shared by all edges
+ * with the same e(i) = redge[i], as profiles of matched segments are reused
+ * (Sec. 4.1).  Optionally each block/strategy has a quantised peak memory
+ * mem[i][s] and the plan must satisfy Eq. M, sum_i mem[i][x_i] <= budget
+ * (Sec. 4.4: least cost under the memory limit, memory quantised).
+ *
+ * Every call answers B independent searches that share rtab/redge but have
+ * their own cost (and mem, budget) tables.  Results are exact: the optimum
+ * is the int64 minimum of Eq. T, and the plan is, among all optimal plans,
+ * the one chosen by taking the lowest index at every tie (equivalently the
+ * least optimal plan in reversed lexicographic order (x_{N-1}, ..., x_0)).
+ *
+ * Conventions for every call:
+ *  - Arrays are C-contiguous, row-major.  "device" pointers are HIP device
+ *    memory of the current device; "host" pointers are ordinary host memory.
+ *  - The caller owns all memory.  The library allocates nothing, frees
+ *    nothing and keeps no pointer after a call returns.
+ *  - Work is enqueued on `stream` (a hipStream_t passed as void*; NULL is
+ *    the default stream) and ordered like any other stream work; inputs must
+ *    stay valid until that work has run.
+ *  - Argument errors (descriptor fields, NULL pointers, host redge out of
+ *    range, workspace too small, unsupported K) are returned synchronously,
+ *    as a negative CFP_ERR_* code, before any HIP call is made.
+ *  - Outcomes found on the device are written per search to status[b]:
+ *    CFP_ST_BADINPUT when a device array holds a value outside its
+ *    documented range, CFP_ST_INFEASIBLE when no plan exists (a block with
+ *    every strategy unavailable, or no plan within the memory budget).  When
+ *    status[b] != CFP_ST_OK, opt[b] = INT64_MAX and the traced plan is all -1.
+ *  - No global mutable state: calls on different streams with different
+ *    workspaces may run concurrently.
+ */
+#ifndef CFP_H
+#define CFP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* A cost entry equal to CFP_COST_INF marks a strategy that is unavailable at
+ * that block (used to pad blocks with fewer than K strategies). */
+#define CFP_COST_INF 0x7FFFFFFF
+
+/* Synchronous return codes. */
+enum {
+  CFP_OK = 0,
+  CFP_ERR_ARG = -1,         /* NULL pointer or a descriptor field out of range */
+  CFP_ERR_RANGE = -2,       /* host array (redge) holds an out-of-range value */
+  CFP_ERR_WORKSPACE = -3,   /* ws is NULL or ws_bytes < cfp_workspace_bytes() */
+  CFP_ERR_UNSUPPORTED = -4, /* K or n_mem beyond what the library supports */
+  CFP_ERR_HIP = -5          /* a HIP runtime call or kernel launch failed */
+};
+
+/* Per-search status written on the device. */
+enum {
+  CFP_ST_OK = 0,
+  CFP_ST_INFEASIBLE = 1, /* no plan (all strategies unavailable at a block, or budget too small) */
+  CFP_ST_OVERFLOW = 2,   /* reserved: device arithmetic left its exact range (not reachable with valid inputs) */
+  CFP_ST_TIMEOUT = 3,    /* reserved: a bounded device wait expired */
+  CFP_ST_BADINPUT = 4    /* a device array value is outside its documented range */
+};
+
+/* Forward variants (the argument `variant` of cfp_workspace_bytes / cfp_traceback). */
+enum { CFP_V_CHAIN = 0, CFP_V_MEM = 1, CFP_V_SCAN = 2 };
+
+/* Largest supported number of strategies per block. */
+#define CFP_MAX_K 512
+
+typedef struct {
+  int32_t n_blocks;     /* N >= 1 */
+  int32_t k;            /* strategies per block, 1 <= K <= CFP_MAX_K */
+  int32_t batch;        /* independent searches B >= 1 */
+  int32_t n_tables;     /* distinct resharding tables E >= 1 */
+  const int32_t *cost;  /* device [B][N][K]; each entry in [0, CFP_COST_INF] (CFP_COST_INF = unavailable) */
+  const int32_t *rtab;  /* device [E][K][K]; rtab[e][t][s]: strategy t of block i-1 -> strategy s of block i;
+                           each entry in [0, cfp_r_limit(variant, K)) */
+  const int32_t *redge; /* HOST [N]; redge[i] in [0, E) names the table of edge (i-1 -> i); redge[0] is ignored */
+} cfp_chain_desc;
+
+/* Exclusive upper bound on resharding-table entries for which `variant` with
+ * K strategies is exact.  The kernels carry (cost, argmin) packed in one
+ * 32-bit word with ceil(log2 K) index bits (at least 4), so the bound depends
+ * on K: 2^(31-b) for K <= 128, 2^(32-b) - 1 for K > 128 (chain and scan), and
+ * 2^(31-b) for the memory variant, with b = max(4, ceil(log2 K)).  Returns 0
+ * for an unsupported K or variant. */
+int32_t cfp_r_limit(int32_t variant, int32_t k);
+
+/* Bytes of device workspace a forward call of `variant` needs (n_mem is the
+ * memory axis size M for CFP_V_MEM, ignored otherwise).  Returns 0 for an
+ * invalid descriptor. */
+size_t cfp_workspace_bytes(const cfp_chain_desc *d, int32_t variant, int32_t n_mem);
+
+/* Unconstrained search by the forward chain recurrence
+ *     D[0][s] = c[0][s],   D[i][s] = c[i][s] + min_t (D[i-1][t] + R_{e(i)}[t][s])
+ * (Sec. 4.4; the dynamic program that starts at the first block).
+ *   ws     device workspace of at least cfp_workspace_bytes(d, CFP_V_CHAIN, 0)
+ *          bytes; on return (in stream order) it holds the argmin tables that
+ *          cfp_traceback reads.
+ *   opt    device [B] int64: min_x T(x), or INT64_MAX when status != OK.
+ *   status device [B] int32: CFP_ST_*.  */
+int cfp_dp_chain(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t *opt, int32_t *status,
+                 void *stream);
+
+/* Search under a memory budget (Sec. 4.4 with Eq. M as the constraint):
+ *     D[i][s][m] = c[i][s] + min_t D[i-1][t][m - mem[i][s]] + R_{e(i)}[t][s]
+ * with D[0][s][m] = c[0][s] if mem[0][s] <= m; the answer is
+ * min_s D[N-1][s][budget[b]] (total memory <= budget, inclusive).
+ *   mem    device [B][N][K] uint8, each entry in [0, n_mem)
+ *   n_mem  M, the number of memory buckets, 1 <= M <= 4096
+ *   budget device [B] int32, each in [0, M)
+ * ws must hold cfp_workspace_bytes(d, CFP_V_MEM, n_mem) bytes. */
+int cfp_dp_chain_mem(const cfp_chain_desc *d, const uint8_t *mem, int32_t n_mem, const int32_t *budget,
+                     void *ws, size_t ws_bytes, int64_t *opt, int32_t *status, void *stream);
+
+/* The same optimum as cfp_dp_chain computed as a min-plus parallel scan:
+ * block i becomes the transfer matrix T_i[t][s] = R_{e(i)}[t][s] + c[i][s]
+ * (T_0[t][s] = c[0][s]), the matrices are composed by a tree of min-plus
+ * matrix products (min-plus matrix product is associative), and a down-sweep
+ * recovers every prefix vector D[i].  For long chains.  ws must hold
+ * cfp_workspace_bytes(d, CFP_V_SCAN, 0) bytes. */
+int cfp_minplus_scan(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t *opt, int32_t *status,
+                     void *stream);
+
+/* Recover the plan x (Sec. 4.4: the plan tuple i = (i_1 .. i_N)) of every
+ * search from a workspace filled by the forward call of `variant` with the
+ * same descriptor (and n_mem for CFP_V_MEM): plan[b][N-1] is the lowest
+ * optimal final strategy and plan[b][i-1] the lowest predecessor attaining
+ * D[i][plan[b][i]].  The traceback reads the forward tables in ws and uses a
+ * small scratch region of ws (chunk maps), so it writes to ws as well.
+ *   plan   device [B][N] int32; all -1 for a search whose status is not OK. */
+int cfp_traceback(const cfp_chain_desc *d, int32_t variant, int32_t n_mem, void *ws, size_t ws_bytes,
+                  int32_t *plan, void *stream);
+
+/* Static string for a CFP_ERR_* or CFP_ST_* code (status codes are >= 0). */
+const char *cfp_status_string(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CFP_H */

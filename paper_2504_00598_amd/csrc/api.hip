@@ -1,0 +1,211 @@
+// Exported C ABI of libcfp: argument validation, workspace layout and launch
+// sequencing.  Every check that can be made on the host is made before the
+// first HIP call, so argument errors never touch the device.
+#include <string.h>
+
+#include <vector>
+
+#include "cfp_internal.h"
+
+namespace cfp {
+
+WsLayout layout(int variant, int n, int k, int batch, int n_mem) {
+  WsLayout L;
+  L.elem = k > 256 ? 2 : 1;
+  size_t off = sizeof(WsHeader);
+  L.redge = off;
+  off = align_up(off + (size_t)n * 4);
+  L.result = off;
+  off = align_up(off + (size_t)batch * sizeof(SearchResult));
+  L.nchunks = n > 1 ? (n - 1 + kChunk - 1) / kChunk : 0;
+  L.table = off;
+  size_t cells = (size_t)batch * n * k;
+  if (variant == CFP_V_MEM) {
+    off = align_up(off + cells * (size_t)n_mem * L.elem);
+    L.mem = off;
+    off = align_up(off + cells);
+  } else {
+    off = align_up(off + cells * L.elem);
+  }
+  L.maps = off;
+  off = align_up(off + (size_t)batch * L.nchunks * k * 2);
+  L.bounds = off;
+  off = align_up(off + (size_t)batch * L.nchunks * 4);
+  if (variant == CFP_V_SCAN) {
+    L.scan = off;
+    L.scan_bytes = scan_region_bytes(n, k, batch);
+    off = align_up(off + L.scan_bytes);
+  }
+  L.total = off;
+  return L;
+}
+
+}  // namespace cfp
+
+using namespace cfp;
+
+namespace {
+
+bool desc_ok(const cfp_chain_desc *d) {
+  if (!d) return false;
+  if (d->n_blocks < 1 || d->k < 1 || d->k > CFP_MAX_K || d->batch < 1 || d->n_tables < 1) return false;
+  if (!d->cost || !d->rtab || !d->redge) return false;
+  return true;
+}
+
+int check_desc(const cfp_chain_desc *d) {
+  if (!d) return CFP_ERR_ARG;
+  if (d->k > CFP_MAX_K) return CFP_ERR_UNSUPPORTED;
+  if (!desc_ok(d)) return CFP_ERR_ARG;
+  for (int i = 1; i < d->n_blocks; ++i)
+    if (d->redge[i] < 0 || d->redge[i] >= d->n_tables) return CFP_ERR_RANGE;
+  return CFP_OK;
+}
+
+// Header + device copy of redge, enqueued as one host-to-device copy.
+int upload_header(const cfp_chain_desc *d, int variant, int n_mem, const WsLayout &L, void *ws, hipStream_t st) {
+  std::vector<uint8_t> buf(L.redge + (size_t)d->n_blocks * 4, 0);
+  WsHeader h;
+  memset(&h, 0, sizeof h);
+  h.magic = kMagic;
+  h.variant = variant;
+  h.n = d->n_blocks;
+  h.k = d->k;
+  h.batch = d->batch;
+  h.n_mem = n_mem;
+  h.elem = L.elem;
+  h.rflag = 0;
+  memcpy(buf.data(), &h, sizeof h);
+  memcpy(buf.data() + L.redge, d->redge, (size_t)d->n_blocks * 4);
+  memset(buf.data() + L.redge, 0, 4);  // redge[0] is ignored; keep it a valid table index
+  if (hipMemcpyAsync(ws, buf.data(), buf.size(), hipMemcpyHostToDevice, st) != hipSuccess) return CFP_ERR_HIP;
+  return CFP_OK;
+}
+
+}  // namespace
+
+#pragma GCC visibility push(default)
+extern "C" {
+
+int32_t cfp_r_limit(int32_t variant, int32_t k) {
+  if (k < 1 || k > CFP_MAX_K) return 0;
+  int b = index_bits(k);
+  switch (variant) {
+    case CFP_V_CHAIN:
+    case CFP_V_SCAN:
+      return k <= 128 ? (int32_t)(1u << (31 - b)) : (int32_t)((1u << (32 - b)) - 1u);
+    case CFP_V_MEM:
+      return k <= 256 ? (int32_t)(1u << (31 - b)) : 0;
+    default:
+      return 0;
+  }
+}
+
+size_t cfp_workspace_bytes(const cfp_chain_desc *d, int32_t variant, int32_t n_mem) {
+  if (!desc_ok(d)) return 0;
+  if (variant == CFP_V_MEM) {
+    if (n_mem < 1 || n_mem > 4096 || d->k > 256) return 0;
+  } else if (variant != CFP_V_CHAIN && variant != CFP_V_SCAN) {
+    return 0;
+  }
+  return layout(variant, d->n_blocks, d->k, d->batch, variant == CFP_V_MEM ? n_mem : 0).total;
+}
+
+int cfp_dp_chain(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t *opt, int32_t *status,
+                 void *stream) {
+  int rc = check_desc(d);
+  if (rc != CFP_OK) return rc;
+  if (!opt || !status) return CFP_ERR_ARG;
+  WsLayout L = layout(CFP_V_CHAIN, d->n_blocks, d->k, d->batch, 0);
+  if (!ws || ws_bytes < L.total) return CFP_ERR_WORKSPACE;
+  hipStream_t st = (hipStream_t)stream;
+  uint8_t *w = (uint8_t *)ws;
+  if ((rc = upload_header(d, CFP_V_CHAIN, 0, L, ws, st)) != CFP_OK) return rc;
+  WsHeader *hdr = (WsHeader *)w;
+  if (launch_validate_rtab(d->rtab, d->n_tables, d->k, cfp_r_limit(CFP_V_CHAIN, d->k), hdr, st) != hipSuccess)
+    return CFP_ERR_HIP;
+  if (launch_chain_fwd(*d, (const int32_t *)(w + L.redge), w + L.table, L.elem, (SearchResult *)(w + L.result),
+                       hdr, opt, status, st) != hipSuccess)
+    return CFP_ERR_HIP;
+  return CFP_OK;
+}
+
+int cfp_dp_chain_mem(const cfp_chain_desc *d, const uint8_t *mem, int32_t n_mem, const int32_t *budget,
+                     void *ws, size_t ws_bytes, int64_t *opt, int32_t *status, void *stream) {
+  int rc = check_desc(d);
+  if (rc != CFP_OK) return rc;
+  if (!mem || !budget || !opt || !status) return CFP_ERR_ARG;
+  if (n_mem < 1) return CFP_ERR_ARG;
+  if (n_mem > 4096 || d->k > 256) return CFP_ERR_UNSUPPORTED;
+  WsLayout L = layout(CFP_V_MEM, d->n_blocks, d->k, d->batch, n_mem);
+  if (!ws || ws_bytes < L.total) return CFP_ERR_WORKSPACE;
+  hipStream_t st = (hipStream_t)stream;
+  uint8_t *w = (uint8_t *)ws;
+  if ((rc = upload_header(d, CFP_V_MEM, n_mem, L, ws, st)) != CFP_OK) return rc;
+  WsHeader *hdr = (WsHeader *)w;
+  if (launch_validate_rtab(d->rtab, d->n_tables, d->k, cfp_r_limit(CFP_V_MEM, d->k), hdr, st) != hipSuccess)
+    return CFP_ERR_HIP;
+  if (launch_chain_mem_fwd(*d, mem, n_mem, budget, (const int32_t *)(w + L.redge), w + L.table, w + L.mem,
+                           (SearchResult *)(w + L.result), hdr, opt, status, st) != hipSuccess)
+    return CFP_ERR_HIP;
+  return CFP_OK;
+}
+
+int cfp_minplus_scan(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t *opt, int32_t *status,
+                     void *stream) {
+  int rc = check_desc(d);
+  if (rc != CFP_OK) return rc;
+  if (!opt || !status) return CFP_ERR_ARG;
+  WsLayout L = layout(CFP_V_SCAN, d->n_blocks, d->k, d->batch, 0);
+  if (!ws || ws_bytes < L.total) return CFP_ERR_WORKSPACE;
+  hipStream_t st = (hipStream_t)stream;
+  uint8_t *w = (uint8_t *)ws;
+  if ((rc = upload_header(d, CFP_V_SCAN, 0, L, ws, st)) != CFP_OK) return rc;
+  WsHeader *hdr = (WsHeader *)w;
+  if (launch_validate_rtab(d->rtab, d->n_tables, d->k, cfp_r_limit(CFP_V_SCAN, d->k), hdr, st) != hipSuccess)
+    return CFP_ERR_HIP;
+  if (launch_scan(*d, (const int32_t *)(w + L.redge), w + L.scan, L.scan_bytes, w + L.table, L.elem,
+                  (SearchResult *)(w + L.result), hdr, opt, status, st) != hipSuccess)
+    return CFP_ERR_HIP;
+  return CFP_OK;
+}
+
+int cfp_traceback(const cfp_chain_desc *d, int32_t variant, int32_t n_mem, void *ws, size_t ws_bytes,
+                  int32_t *plan, void *stream) {
+  if (!desc_ok(d)) return d && d->k > CFP_MAX_K ? CFP_ERR_UNSUPPORTED : CFP_ERR_ARG;
+  if (!plan) return CFP_ERR_ARG;
+  if (variant != CFP_V_CHAIN && variant != CFP_V_MEM && variant != CFP_V_SCAN) return CFP_ERR_ARG;
+  if (variant == CFP_V_MEM && (n_mem < 1 || n_mem > 4096 || d->k > 256)) return CFP_ERR_ARG;
+  WsLayout L = layout(variant, d->n_blocks, d->k, d->batch, variant == CFP_V_MEM ? n_mem : 0);
+  if (!ws || ws_bytes < L.total) return CFP_ERR_WORKSPACE;
+  hipStream_t st = (hipStream_t)stream;
+  uint8_t *w = (uint8_t *)ws;
+  hipError_t e;
+  if (variant == CFP_V_MEM)
+    e = launch_traceback_mem(d->n_blocks, d->k, d->batch, n_mem, w + L.table, w + L.mem,
+                             (const SearchResult *)(w + L.result), plan, st);
+  else
+    e = launch_traceback_chain(d->n_blocks, d->k, d->batch, L.elem, w + L.table,
+                               (const SearchResult *)(w + L.result), (uint16_t *)(w + L.maps),
+                               (int32_t *)(w + L.bounds), L.nchunks, plan, st);
+  return e == hipSuccess ? CFP_OK : CFP_ERR_HIP;
+}
+
+const char *cfp_status_string(int code) {
+  switch (code) {
+    case CFP_OK: return "ok";
+    case CFP_ST_INFEASIBLE: return "infeasible: no plan satisfies the constraints";
+    case CFP_ST_OVERFLOW: return "overflow: device arithmetic left its exact range";
+    case CFP_ST_TIMEOUT: return "timeout: a bounded device wait expired";
+    case CFP_ST_BADINPUT: return "bad input: a device array value is outside its documented range";
+    case CFP_ERR_ARG: return "invalid argument";
+    case CFP_ERR_RANGE: return "host array value out of range";
+    case CFP_ERR_WORKSPACE: return "workspace missing or too small";
+    case CFP_ERR_UNSUPPORTED: return "unsupported size";
+    case CFP_ERR_HIP: return "HIP runtime error";
+    default: return "unknown code";
+  }
+}
+
+}  // extern "C"
+#pragma GCC visibility pop

@@ -1,0 +1,78 @@
+// Internal layout and launcher declarations of libcfp (not installed).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "cfp.h"
+
+namespace cfp {
+
+constexpr uint32_t kMagic = 0xCF900598u;
+constexpr int kThreads = 256;   // threads of every search workgroup (4 waves of 64)
+constexpr int kChunk = 64;      // traceback chunk length (steps)
+
+// Number of index bits of the packed (value, index) word for K strategies.
+inline int index_bits(int k) {
+  int b = 4;
+  while ((1 << b) < k) ++b;
+  return b;
+}
+
+// Workspace header, written by the host at the start of every forward call.
+struct WsHeader {
+  uint32_t magic;
+  int32_t variant, n, k, batch, n_mem, elem;  // elem: bytes per argmin entry
+  int32_t rflag;                               // set to 1 by the device if rtab breaks its range
+  int32_t pad[56];
+};
+static_assert(sizeof(WsHeader) == 256, "header is 256 bytes");
+
+// Per-search record written by the forward kernels and read by the traceback.
+struct SearchResult {
+  int32_t final_state;  // lowest optimal final strategy, -1 if status != OK
+  int32_t status;
+  int32_t final_m;      // memory variant: budget of the search
+  int32_t pad;
+};
+
+inline size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
+
+struct WsLayout {
+  size_t redge = 0;    // int32 [N]
+  size_t result = 0;   // SearchResult [B]
+  size_t table = 0;    // argmin entries [B][N][K] (chain, scan) or [B][N][K][M] (mem)
+  size_t mem = 0;      // memory variant: copy of mem [B][N][K]
+  size_t maps = 0;     // traceback chunk maps uint16 [B][nchunks][K]
+  size_t bounds = 0;   // traceback chunk boundary states int32 [B][nchunks]
+  size_t scan = 0;     // scan variant: start of its private region
+  size_t scan_bytes = 0;
+  size_t total = 0;
+  int elem = 1;
+  int nchunks = 0;
+};
+
+WsLayout layout(int variant, int n, int k, int batch, int n_mem);
+
+// Launchers (return hipSuccess or the launch error).
+hipError_t launch_validate_rtab(const int32_t *rtab, int e, int k, int32_t limit, WsHeader *hdr,
+                                hipStream_t st);
+hipError_t launch_chain_fwd(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *table, int elem,
+                            SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
+                            hipStream_t st);
+hipError_t launch_chain_mem_fwd(const cfp_chain_desc &d, const uint8_t *mem, int n_mem, const int32_t *budget,
+                                const int32_t *redge_dev, uint8_t *table, uint8_t *mem_copy,
+                                SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
+                                hipStream_t st);
+hipError_t launch_traceback_chain(int n, int k, int batch, int elem, const uint8_t *table,
+                                  const SearchResult *res, uint16_t *maps, int32_t *bounds, int nchunks,
+                                  int32_t *plan, hipStream_t st);
+hipError_t launch_traceback_mem(int n, int k, int batch, int n_mem, const uint8_t *table, const uint8_t *mem,
+                                const SearchResult *res, int32_t *plan, hipStream_t st);
+hipError_t launch_scan(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *region, size_t region_bytes,
+                       uint8_t *table, int elem, SearchResult *res, const WsHeader *hdr, int64_t *opt,
+                       int32_t *status, hipStream_t st);
+size_t scan_region_bytes(int n, int k, int batch);
+
+}  // namespace cfp

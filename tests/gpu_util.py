@@ -1,0 +1,54 @@
+"""Helpers of the GPU parity tests: move seeded inputs to the device, run the
+library through its C ABI binding, and compare with the oracle."""
+from __future__ import annotations
+
+import os
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+
+
+def need_gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU in this container")
+
+
+def oracle_threads() -> int:
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+def dev(a, dtype=None):
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    if dtype is not None:
+        t = t.to(dtype)
+    return t.cuda()
+
+
+def say(*args):
+    print(*args, flush=True)
+    sys.stdout.flush()
+
+
+def run_chain(cost, rtab, redge):
+    import torch
+    from paper_2504_00598_amd import search
+    res = search.dp_chain(dev(cost), dev(rtab), redge)
+    torch.cuda.synchronize()
+    return res.opt.cpu().numpy(), res.status.cpu().numpy(), res.plan.cpu().numpy()
+
+
+def assert_chain_parity(cost, rtab, redge, label=""):
+    cost = np.asarray(cost, np.int32)
+    if cost.ndim == 2:
+        cost = cost[None]
+    g_opt, g_st, g_plan = run_chain(cost, rtab, redge)
+    o_opt, o_plan, o_st = O.chain(cost, rtab, redge, nthreads=oracle_threads())
+    np.testing.assert_array_equal(g_st, o_st, err_msg=f"status {label}")
+    np.testing.assert_array_equal(g_opt, o_opt, err_msg=f"opt {label}")
+    np.testing.assert_array_equal(g_plan, o_plan, err_msg=f"plan {label}")
+    return g_opt, g_plan

@@ -1,0 +1,107 @@
+"""GPU parity of cfp_dp_chain + cfp_traceback against the CPU oracle:
+optimum, status and plan must match bit for bit."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from tests.gpu_util import assert_chain_parity, dev, need_gpu, run_chain, say
+from workloads import configs, gen
+
+pytestmark = pytest.mark.gpu
+
+INF = gen.COST_INF
+
+
+def rand_case(seed, B, N, K, E, lo, hi, rlo=None, rhi=None, inf_frac=0.0):
+    rs = np.random.default_rng(seed)
+    cost = rs.integers(lo, hi, size=(B, N, K)).astype(np.int32)
+    if inf_frac:
+        cost[rs.random((B, N, K)) < inf_frac] = INF
+    rtab = rs.integers(lo if rlo is None else rlo, hi if rhi is None else rhi, size=(E, K, K)).astype(np.int32)
+    redge = rs.integers(0, E, size=N).astype(np.int32)
+    return cost, rtab, redge
+
+
+@pytest.mark.parametrize("cfg", ["chain_gpt_n24_k16", "chain_gpt_n1152_k64", "chain_wide_n512_k256"])
+def test_configs_full(cfg):
+    need_gpu()
+    say("config", cfg)
+    d = configs.make(cfg)
+    assert_chain_parity(d["cost"], d["rtab"], d["redge"], cfg)
+
+
+SHAPES = [(1, 1), (1, 5), (2, 1), (3, 2), (7, 3), (65, 16), (130, 17), (129, 31), (64, 32), (70, 33),
+          (200, 64), (66, 65), (131, 100), (90, 128), (40, 129), (67, 200), (33, 256), (20, 257), (9, 300),
+          (12, 512)]
+
+
+@pytest.mark.parametrize("N,K", SHAPES)
+def test_shapes_realistic_values(N, K):
+    need_gpu()
+    say("shape", N, K)
+    from paper_2504_00598_amd import cfp_r_limit
+    rhi = min(10_000_000, cfp_r_limit(0, K))  # resharding values within the documented exact range
+    cost, rtab, redge = rand_case([1, N, K], 3, N, K, 5, 10_000, 10_000_000, rlo=10_000, rhi=rhi)
+    assert_chain_parity(cost, rtab, redge, f"N={N} K={K}")
+
+
+@pytest.mark.parametrize("N,K", SHAPES)
+def test_shapes_heavy_ties(N, K):
+    need_gpu()
+    say("ties", N, K)
+    cost, rtab, redge = rand_case([2, N, K], 2, N, K, 3, 0, 3)
+    assert_chain_parity(cost, rtab, redge, f"ties N={N} K={K}")
+
+
+@pytest.mark.parametrize("K", [16, 64, 200, 512])
+def test_largest_allowed_resharding(K):
+    """R entries at cfp_r_limit - 1 and costs near 2^31: still exact."""
+    need_gpu()
+    from paper_2504_00598_amd import cfp_r_limit
+    lim = cfp_r_limit(0, K)
+    rs = np.random.default_rng(K)
+    N = 50
+    cost = rs.integers(2**31 - 10**6, 2**31 - 1, size=(2, N, K)).astype(np.int32)
+    rtab = rs.integers(lim - 1000, lim, size=(4, K, K)).astype(np.int32)
+    rtab[:, np.arange(K), np.arange(K)] = rs.integers(0, 3, size=(4, K))
+    redge = rs.integers(0, 4, size=N).astype(np.int32)
+    assert_chain_parity(cost, rtab, redge, f"max R K={K}")
+
+
+@pytest.mark.parametrize("K", [3, 64, 256])
+def test_unavailable_strategies(K):
+    need_gpu()
+    cost, rtab, redge = rand_case([3, K], 4, 40, K, 3, 0, 100, inf_frac=0.3)
+    cost[1, 7, :] = INF        # search 1: every strategy of block 7 unavailable -> infeasible
+    cost[2, 0, :] = INF        # search 2: block 0 unavailable -> infeasible
+    cost[3, :, 1:] = INF       # search 3: only strategy 0 is left anywhere
+    cost[3, :, 0] = 5
+    g_opt, g_plan = assert_chain_parity(cost, rtab, redge, f"inf K={K}")
+    assert (g_plan[1] == -1).all() and (g_plan[2] == -1).all()
+    assert (g_plan[3] == 0).all()
+
+
+def test_badinput_statuses():
+    need_gpu()
+    from paper_2504_00598_amd import CFP_ST_BADINPUT, cfp_r_limit
+    cost, rtab, redge = rand_case(4, 3, 20, 16, 2, 0, 100)
+    cost[1, 3, 4] = -5
+    opt, st, plan = run_chain(cost, rtab, redge)
+    assert st.tolist() == [0, CFP_ST_BADINPUT, 0]
+    assert opt[1] == np.iinfo(np.int64).max and (plan[1] == -1).all()
+    rtab2 = rtab.copy()
+    rtab2[1, 2, 3] = cfp_r_limit(0, 16)
+    opt, st, plan = run_chain(cost, rtab2, redge)
+    assert (st == CFP_ST_BADINPUT).all() and (plan == -1).all()
+
+
+def test_repeat_is_bit_identical():
+    need_gpu()
+    d = configs.make("chain_gpt_n1152_k64", batch=32)
+    first = run_chain(d["cost"], d["rtab"], d["redge"])
+    for _ in range(3):
+        again = run_chain(d["cost"], d["rtab"], d["redge"])
+        for a, b in zip(first, again):
+            np.testing.assert_array_equal(a, b)
