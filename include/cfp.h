@@ -95,7 +95,7 @@ typedef struct {
 /* Exclusive upper bound on resharding-table entries for which `variant` with
  * K strategies is exact.  The kernels carry (cost, argmin) packed in one
  * 32-bit word with ceil(log2 K) index bits (at least 4), so the bound depends
- * on K: 2^(31-b) for K <= 128, 2^(32-b) - 1 for K > 128 (chain and scan), and
+ * on K: 2^(30-b) for K <= 64, 2^(32-b) - 1 for K > 64 (chain and scan), and
  * 2^(31-b) for the memory variant, with b = max(4, ceil(log2 K)).  Returns 0
  * for an unsupported K or variant. */
 int32_t cfp_r_limit(int32_t variant, int32_t k);

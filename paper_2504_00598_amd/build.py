@@ -20,6 +20,11 @@ FLAGS = [
     "-shared",
     "-Wall",
     "-fvisibility=hidden",
+    # keep the per-table switch cases of the register-resident kernel separate
+    # (otherwise the cases are merged behind register copies)
+    "-mllvm", "-simplifycfg-sink-common=false",
+    # LDS atomics stay single instructions (no per-lane scalar loop)
+    "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
     # no packed fp32 instructions anywhere in device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I", os.path.join(ROOT, "include"),

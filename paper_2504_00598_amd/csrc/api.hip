@@ -93,7 +93,7 @@ int32_t cfp_r_limit(int32_t variant, int32_t k) {
   switch (variant) {
     case CFP_V_CHAIN:
     case CFP_V_SCAN:
-      return k <= 128 ? (int32_t)(1u << (31 - b)) : (int32_t)((1u << (32 - b)) - 1u);
+      return k <= 64 ? (int32_t)(1u << (30 - b)) : (int32_t)((1u << (32 - b)) - 1u);
     case CFP_V_MEM:
       return k <= 256 ? (int32_t)(1u << (31 - b)) : 0;
     default:

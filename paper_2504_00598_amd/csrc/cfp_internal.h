@@ -61,6 +61,12 @@ hipError_t launch_validate_rtab(const int32_t *rtab, int e, int k, int32_t limit
 hipError_t launch_chain_fwd(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *table, int elem,
                             SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
                             hipStream_t st);
+bool chain_fwd_res_supported(int k, int n_tables);
+hipError_t launch_chain_fwd_res(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *table, SearchResult *res,
+                                const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st);
+hipError_t launch_chain_fwd_generic(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *table,
+                                    SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
+                                    hipStream_t st);
 hipError_t launch_chain_mem_fwd(const cfp_chain_desc &d, const uint8_t *mem, int n_mem, const int32_t *budget,
                                 const int32_t *redge_dev, uint8_t *table, uint8_t *mem_copy,
                                 SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,

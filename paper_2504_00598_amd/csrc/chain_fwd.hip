@@ -181,6 +181,8 @@ hipError_t launch_chain_fwd(const cfp_chain_desc &d, const int32_t *redge_dev, u
                             SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
                             hipStream_t st) {
   (void)elem;
+  if (chain_fwd_res_supported(d.k, d.n_tables))
+    return launch_chain_fwd_res(d, redge_dev, table, res, hdr, opt, status, st);
   const int k = d.k;
   if (k <= 16) launch_kp<16>(d, redge_dev, table, res, hdr, opt, status, st);
   else if (k <= 32) launch_kp<32>(d, redge_dev, table, res, hdr, opt, status, st);

@@ -15,6 +15,13 @@
 
 namespace cfp {
 
+// Index bits of the packed words (the stored argmin may carry value bits above them).
+__device__ __forceinline__ int index_bits_dev(int k) {
+  int b = 4;
+  while ((1 << b) < k) ++b;
+  return b;
+}
+
 struct ChunkSpan {
   int lo, hi;  // the chunk covers steps hi, hi-1, ..., lo+1 (block indices)
 };
@@ -45,10 +52,11 @@ __global__ __launch_bounds__(kThreads) void tb_maps_kernel(int n, int k, const T
   if (res[b].status != CFP_ST_OK) return;
   const ChunkSpan sp = chunk_span(c, n);
   load_chunk(tab, b, n, k, sp, rows);
+  const int mask = (1 << index_bits_dev(k)) - 1;
   for (int s = threadIdx.x; s < k; s += blockDim.x) {
     int t = s;
     for (int i = sp.hi; i > sp.lo; --i) {
-      int p = rows[(i - sp.lo - 1) * k + t];
+      int p = rows[(i - sp.lo - 1) * k + t] & mask;
       t = p < k ? p : k - 1;  // unreachable end states may carry any index; stay in bounds
     }
     maps[((size_t)b * nchunks + c) * k + s] = (uint16_t)t;
@@ -89,9 +97,10 @@ __global__ __launch_bounds__(kThreads) void tb_fill_kernel(int n, int k, const T
   load_chunk(tab, b, n, k, sp, rows);
   __shared__ int32_t out[kChunk];
   if (threadIdx.x == 0) {
+    const int mask = (1 << index_bits_dev(k)) - 1;
     int t = bounds[(size_t)b * nchunks + c];
     for (int i = sp.hi; i > sp.lo; --i) {
-      int p = rows[(i - sp.lo - 1) * k + t];
+      int p = rows[(i - sp.lo - 1) * k + t] & mask;
       t = p < k ? p : k - 1;
       out[i - 1 - sp.lo] = t;
     }

@@ -38,9 +38,9 @@ def test_only_the_abi_is_exported():
 
 def test_r_limit_values():
     # packed (value, index) words: b = max(4, ceil(log2 K)) index bits
-    assert L.cfp_r_limit(L.CFP_V_CHAIN, 16) == 2 ** 27
-    assert L.cfp_r_limit(L.CFP_V_CHAIN, 64) == 2 ** 25
-    assert L.cfp_r_limit(L.CFP_V_CHAIN, 65) == 2 ** 24
+    assert L.cfp_r_limit(L.CFP_V_CHAIN, 16) == 2 ** 26
+    assert L.cfp_r_limit(L.CFP_V_CHAIN, 64) == 2 ** 24
+    assert L.cfp_r_limit(L.CFP_V_CHAIN, 65) == 2 ** 25 - 1
     assert L.cfp_r_limit(L.CFP_V_CHAIN, 256) == 2 ** 24 - 1
     assert L.cfp_r_limit(L.CFP_V_CHAIN, 512) == 2 ** 23 - 1
     assert L.cfp_r_limit(L.CFP_V_CHAIN, 513) == 0
