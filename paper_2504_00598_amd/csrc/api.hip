@@ -24,6 +24,9 @@ WsLayout layout(int variant, int n, int k, int batch, int n_mem) {
     off = align_up(off + cells * (size_t)n_mem * L.elem);
     L.mem = off;
     off = align_up(off + cells);
+    L.memreg = off;
+    L.memreg_bytes = mem_region_bytes(n, k, batch, n_mem);
+    off = align_up(off + L.memreg_bytes);
   } else {
     off = align_up(off + cells * L.elem);
   }
@@ -95,7 +98,7 @@ int32_t cfp_r_limit(int32_t variant, int32_t k) {
     case CFP_V_SCAN:
       return k <= 64 ? (int32_t)(1u << (30 - b)) : (int32_t)((1u << (32 - b)) - 1u);
     case CFP_V_MEM:
-      return k <= 256 ? (int32_t)(1u << (31 - b)) : 0;
+      return k <= 32 ? (int32_t)(1u << (31 - b)) : 0;
     default:
       return 0;
   }
@@ -104,7 +107,7 @@ int32_t cfp_r_limit(int32_t variant, int32_t k) {
 size_t cfp_workspace_bytes(const cfp_chain_desc *d, int32_t variant, int32_t n_mem) {
   if (!desc_ok(d)) return 0;
   if (variant == CFP_V_MEM) {
-    if (n_mem < 1 || n_mem > 4096 || d->k > 256) return 0;
+    if (n_mem < 1 || n_mem > 4096 || !chain_mem_supported(d->k, d->n_tables)) return 0;
   } else if (variant != CFP_V_CHAIN && variant != CFP_V_SCAN) {
     return 0;
   }
@@ -136,7 +139,7 @@ int cfp_dp_chain_mem(const cfp_chain_desc *d, const uint8_t *mem, int32_t n_mem,
   if (rc != CFP_OK) return rc;
   if (!mem || !budget || !opt || !status) return CFP_ERR_ARG;
   if (n_mem < 1) return CFP_ERR_ARG;
-  if (n_mem > 4096 || d->k > 256) return CFP_ERR_UNSUPPORTED;
+  if (n_mem > 4096 || !chain_mem_supported(d->k, d->n_tables)) return CFP_ERR_UNSUPPORTED;
   WsLayout L = layout(CFP_V_MEM, d->n_blocks, d->k, d->batch, n_mem);
   if (!ws || ws_bytes < L.total) return CFP_ERR_WORKSPACE;
   hipStream_t st = (hipStream_t)stream;
@@ -146,7 +149,7 @@ int cfp_dp_chain_mem(const cfp_chain_desc *d, const uint8_t *mem, int32_t n_mem,
   if (launch_validate_rtab(d->rtab, d->n_tables, d->k, cfp_r_limit(CFP_V_MEM, d->k), hdr, st) != hipSuccess)
     return CFP_ERR_HIP;
   if (launch_chain_mem_fwd(*d, mem, n_mem, budget, (const int32_t *)(w + L.redge), w + L.table, w + L.mem,
-                           (SearchResult *)(w + L.result), hdr, opt, status, st) != hipSuccess)
+                           w + L.memreg, (SearchResult *)(w + L.result), hdr, opt, status, st) != hipSuccess)
     return CFP_ERR_HIP;
   return CFP_OK;
 }
@@ -175,7 +178,8 @@ int cfp_traceback(const cfp_chain_desc *d, int32_t variant, int32_t n_mem, void 
   if (!desc_ok(d)) return d && d->k > CFP_MAX_K ? CFP_ERR_UNSUPPORTED : CFP_ERR_ARG;
   if (!plan) return CFP_ERR_ARG;
   if (variant != CFP_V_CHAIN && variant != CFP_V_MEM && variant != CFP_V_SCAN) return CFP_ERR_ARG;
-  if (variant == CFP_V_MEM && (n_mem < 1 || n_mem > 4096 || d->k > 256)) return CFP_ERR_ARG;
+  if (variant == CFP_V_MEM && (n_mem < 1 || n_mem > 4096 || !chain_mem_supported(d->k, d->n_tables)))
+    return CFP_ERR_ARG;
   WsLayout L = layout(variant, d->n_blocks, d->k, d->batch, variant == CFP_V_MEM ? n_mem : 0);
   if (!ws || ws_bytes < L.total) return CFP_ERR_WORKSPACE;
   hipStream_t st = (hipStream_t)stream;

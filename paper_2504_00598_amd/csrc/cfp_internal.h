@@ -44,6 +44,8 @@ struct WsLayout {
   size_t result = 0;   // SearchResult [B]
   size_t table = 0;    // argmin entries [B][N][K] (chain, scan) or [B][N][K][M] (mem)
   size_t mem = 0;      // memory variant: copy of mem [B][N][K]
+  size_t memreg = 0;   // memory variant: state order, packed tables, chunk flags and halo ring
+  size_t memreg_bytes = 0;
   size_t maps = 0;     // traceback chunk maps uint16 [B][nchunks][K]
   size_t bounds = 0;   // traceback chunk boundary states int32 [B][nchunks]
   size_t scan = 0;     // scan variant: start of its private region
@@ -67,8 +69,10 @@ hipError_t launch_chain_fwd_res(const cfp_chain_desc &d, const int32_t *redge_de
 hipError_t launch_chain_fwd_generic(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *table,
                                     SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
                                     hipStream_t st);
+bool chain_mem_supported(int k, int n_tables);
+size_t mem_region_bytes(int n, int k, int batch, int n_mem);
 hipError_t launch_chain_mem_fwd(const cfp_chain_desc &d, const uint8_t *mem, int n_mem, const int32_t *budget,
-                                const int32_t *redge_dev, uint8_t *table, uint8_t *mem_copy,
+                                const int32_t *redge_dev, uint8_t *table, uint8_t *mem_copy, uint8_t *region,
                                 SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
                                 hipStream_t st);
 hipError_t launch_traceback_chain(int n, int k, int batch, int elem, const uint8_t *table,

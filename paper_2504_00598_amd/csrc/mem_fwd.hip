@@ -1,0 +1,426 @@
+// Search under a memory budget (Sec. 4.4: least Eq. T cost with Eq. M within
+// the memory limit, memory quantised into buckets):
+//     D[0][s][m] = c[0][s]                                   if mem[0][s] <= m
+//     D[i][s][m] = c[i][s] + min_t D[i-1][t][m - mem[i][s]] + R_{e(i)}[t][s]
+// with D = +inf where m < mem[i][s]; the answer is min_s D[N-1][s][budget].
+// D[i][s][m] is the least cost of a prefix whose memory total is at most m,
+// so it does not increase with m.
+//
+// Layout.  Each search is cut into chunks of 64 memory buckets; one workgroup
+// (4 waves) computes one chunk for all K <= 32 states, lanes running over the
+// buckets m of the chunk, wave w over a quarter of the states.  Step i of a
+// chunk only reads buckets m - mem[i][s] >= m - kMemShift of step i-1, so a
+// chunk needs the top kMemShift buckets of the chunk below it: each chunk
+// publishes them in a device ring (one slot per step) and raises a flag;
+// the chunk above waits for the flag (release/acquire at agent scope, bounded
+// spin).  Chunks of one search have workgroup ids j*B + b, so a producer
+// always has a lower id than its consumer and, for B a multiple of 8, all
+// chunks of a search share one XCD and its L2.
+//
+// Arithmetic.  Column m carries an exact int64 offset o[m] = min_s D[s][m];
+// LDS holds Q[s][m] = min(D[s][m] - o[m], cap) with cap = 2^(32-b) - 1.  A
+// candidate is the saturating sum (Q[t][m-d] << b) + ((R[t][s] << b) | t)
+// with the resharding column of state s taken from SGPRs; its value is
+// relative to o[m-d], and o[m-d] - o[m] >= 0 (fewer buckets never cost
+// less) converts it.  The best candidate of any state is at most R_max
+// (through the minimum of column m-d), so it is exact for R < cap; a state
+// whose relative value reaches the cap is beaten, at the same memory, by the
+// minimum state of its column and can never lie on an optimal plan.  States
+// are visited in order of their memory shift so each wave loads every
+// shifted row once.
+#include "cfp_internal.h"
+#include "common.h"
+
+namespace cfp {
+
+constexpr int kMemChunk = 64;  // buckets per workgroup
+constexpr int kMemShift = 16;  // largest supported mem entry (halo width)
+constexpr int64_t kOffInf = (int64_t)1 << 62;
+constexpr int kSpinLimit = 1 << 22;
+
+enum { MEMF_BAD = 1, MEMF_TIMEOUT = 2, MEMF_OVERFLOW = 4 };
+
+// Per-search, per-block order of the states by memory shift (stable), with
+// their shifts and costs; copies mem for the traceback; validates mem and the
+// budget.  One wave per (b, i) row.
+template <int KP>
+__global__ __launch_bounds__(256) void mem_prep_kernel(const int32_t *__restrict__ cost, const uint8_t *__restrict__ mem,
+                                                       const int32_t *__restrict__ budget, int N, int K, int M, int B,
+                                                       uint8_t *__restrict__ sidx, uint8_t *__restrict__ sdel,
+                                                       int32_t *__restrict__ scost, uint8_t *__restrict__ mem_copy,
+                                                       int32_t *__restrict__ mflags) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= B * N) return;
+  const int b = row / N;
+  const size_t base = (size_t)row * K;
+  int d = 0, c = CFP_COST_INF;
+  bool bad = false;
+  if (lane < K) {
+    d = mem[base + lane];
+    c = cost[base + lane];
+    mem_copy[base + lane] = (uint8_t)d;
+    bad = d >= M || d > kMemShift || c < 0;
+  }
+  if (lane == 0 && (row % N) == 0 && (budget[b] < 0 || budget[b] >= M)) bad = true;
+  if (__any(bad) && lane == 0) atomicOr(&mflags[b], MEMF_BAD);
+  if (d > kMemShift) d = kMemShift;
+  // stable rank by shift; states K..KP-1 (unavailable padding) sort last
+  const int key = lane < K ? d : kMemShift + 1;
+  int rank = 0;
+  for (int o = 0; o < KP; ++o) {
+    const int ko = __shfl(key, o, 64);
+    rank += (ko < key) || (ko == key && o < lane);
+  }
+  if (lane < KP) {
+    const size_t obase = (size_t)row * KP;
+    sidx[obase + rank] = (uint8_t)lane;
+    sdel[obase + rank] = (uint8_t)(lane < K ? d : 0);
+    scost[obase + rank] = lane < K ? c : CFP_COST_INF;
+  }
+}
+
+// Resharding tables transposed and packed: rpT[e][s][t] = (R[e][t][s] << b) | t.
+template <int KP>
+__global__ void mem_pack_rtab_kernel(const int32_t *__restrict__ rtab, int E, int K, uint32_t *__restrict__ rpT) {
+  constexpr int BITS = Pow2Bits<KP>::value;
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= E * KP * KP) return;
+  const int e = idx / (KP * KP), s = (idx / KP) % KP, t = idx % KP;
+  rpT[idx] = (s < K && t < K) ? (((uint32_t)rtab[((size_t)e * K + t) * K + s] << BITS) | (uint32_t)t) : kSat;
+}
+
+struct MemWs {
+  uint8_t *sidx, *sdel;
+  int32_t *scost;
+  uint32_t *rpT;
+  int32_t *mflags;   // [B]
+  int32_t *pub;      // [B][nchunk]: last step published by each chunk
+  uint32_t *ring;    // [B][nchunk][N][KP][kMemShift]
+  int64_t *ring_off; // [B][nchunk][N][kMemShift]
+  int nchunk;
+};
+
+template <int KP>
+__global__ __launch_bounds__(kThreads) void mem_fwd_kernel(const int32_t *__restrict__ redge, const int32_t *__restrict__ budget,
+                                                           int N, int K, int M, int B, MemWs w, uint8_t *__restrict__ table,
+                                                           SearchResult *__restrict__ res, const WsHeader *__restrict__ hdr,
+                                                           int64_t *__restrict__ opt, int32_t *__restrict__ status) {
+  constexpr int BITS = Pow2Bits<KP>::value;
+  constexpr uint32_t CAP = (1u << (32 - BITS)) - 1u;
+  constexpr int SW = KP / 4;                 // states per wave
+  constexpr int H = kMemShift, C = kMemChunk;
+  constexpr int COLS = H + C;
+
+  __shared__ uint32_t Q[KP][COLS];
+  __shared__ int64_t off[COLS];
+  __shared__ uint32_t part[4][C];
+  __shared__ uint32_t reach[4][C];
+  __shared__ int abort_flag;
+
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int b = blockIdx.x % B, j = blockIdx.x / B;
+  const int m0 = j * C;
+  const int Bb = budget[b];
+  const int mf = w.mflags[b];  // written by the prep kernel earlier in the stream
+  if (mf & MEMF_BAD) {
+    if (j == 0 && tid == 0) {
+      status[b] = CFP_ST_BADINPUT;
+      opt[b] = INT64_MAX;
+      res[b].final_state = -1;
+      res[b].status = CFP_ST_BADINPUT;
+      res[b].final_m = -1;
+    }
+    return;
+  }
+  if (m0 > Bb) return;  // no bucket of this chunk is within the budget
+  const int m = m0 + lane;
+  const bool active = m <= Bb;
+  const size_t rowbase = (size_t)b * N;
+  int flags = 0;
+
+  // Halo of chunk 0: buckets below 0 are infeasible.
+  for (int x = tid; x < KP * H; x += kThreads) Q[x / H][x % H] = CAP;
+  if (tid < H) off[tid] = kOffInf;
+  __syncthreads();
+
+  const size_t chunk_id = (size_t)b * w.nchunk + j;
+  uint32_t *my_ring = w.ring + chunk_id * N * KP * H;
+  int64_t *my_roff = w.ring_off + chunk_id * N * H;
+  const uint32_t *lo_ring = w.ring + (chunk_id - 1) * N * KP * H;
+  const int64_t *lo_roff = w.ring_off + (chunk_id - 1) * N * H;
+
+  // y[k]: value of the wave's k-th state at bucket m relative to the previous
+  // offset of column m; rk: the state is reachable.
+  uint32_t y[SW];
+  bool rk[SW];
+
+  auto finish_step = [&](int i) __attribute__((always_inline)) {
+    // column minimum over all states
+    uint32_t pm = kSat, pr = 0;
+#pragma unroll
+    for (int k = 0; k < SW; ++k) {
+      pm = umin(pm, y[k]);
+      pr |= rk[k] ? 1u : 0u;
+    }
+    part[wid][lane] = pm;
+    reach[wid][lane] = pr;
+    __syncthreads();
+    const uint32_t cm = umin(umin(part[0][lane], part[1][lane]), umin(part[2][lane], part[3][lane]));
+    const bool feas = (reach[0][lane] | reach[1][lane] | reach[2][lane] | reach[3][lane]) != 0;
+    if (feas && cm >= 0x80000000u) flags |= MEMF_OVERFLOW;
+    const int64_t onew = (feas && cm < kSat) ? off[H + lane] + (int64_t)cm : kOffInf;
+    const size_t sbase = (rowbase + i) * KP;
+#pragma unroll
+    for (int k = 0; k < SW; ++k) {
+      const int s = w.sidx[sbase + wid * SW + k];
+      const uint32_t q = (onew < kOffInf && y[k] < kSat) ? umin(y[k] - cm, CAP) : CAP;
+      Q[s][H + lane] = q;
+      if (lane >= C - H) my_ring[((size_t)i * KP + s) * H + (lane - (C - H))] = q;
+    }
+    __syncthreads();  // every wave has read the old offsets
+    if (wid == 0) {
+      off[H + lane] = onew;
+      if (lane >= C - H) my_roff[(size_t)i * H + (lane - (C - H))] = onew;
+    }
+    __threadfence();
+    __syncthreads();
+    if (tid == 0) __hip_atomic_store(&w.pub[chunk_id], i, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    // Halo for step i+1: the top buckets of the chunk below, at step i.
+    if (j > 0 && i + 1 < N) {
+      if (tid == 0) {
+        int spins = 0;
+        while (__hip_atomic_load(&w.pub[chunk_id - 1], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < i) {
+          if (++spins > kSpinLimit) {
+            abort_flag = 1;
+            atomicOr(&w.mflags[b], MEMF_TIMEOUT);
+            break;
+          }
+          __builtin_amdgcn_s_sleep(2);
+        }
+      }
+      __syncthreads();
+      for (int x = tid; x < KP * H; x += kThreads)
+        Q[x / H][x % H] = __hip_atomic_load(&lo_ring[(size_t)i * KP * H + x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (tid < H) off[tid] = __hip_atomic_load(&lo_roff[(size_t)i * H + tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __syncthreads();
+    }
+  };
+
+  if (tid == 0) abort_flag = 0;
+  // Block 0.
+  {
+    const size_t sbase = rowbase * KP;
+#pragma unroll
+    for (int k = 0; k < SW; ++k) {
+      const int pos = wid * SW + k;
+      const int d = w.sdel[sbase + pos];
+      const int32_t c = w.scost[sbase + pos];
+      rk[k] = active && m >= d && c != CFP_COST_INF;
+      y[k] = rk[k] ? (uint32_t)c : kSat;
+    }
+    if (wid == 0) off[H + lane] = 0;  // block 0 values are absolute
+    __syncthreads();
+    finish_step(0);
+  }
+
+  for (int i = 1; i < N; ++i) {
+    const int e = redge[i];
+    const size_t sbase = (rowbase + i) * KP;
+    uint32_t A[KP];
+    int dprev = -1;
+    uint32_t goff = 0;
+    bool srcok = false;
+#pragma unroll
+    for (int k = 0; k < SW; ++k) {
+      const int pos = wid * SW + k;
+      const int s = w.sidx[sbase + pos];
+      const int d = w.sdel[sbase + pos];
+      const int32_t c = w.scost[sbase + pos];
+      if (d != dprev) {
+        dprev = d;
+#pragma unroll
+        for (int t = 0; t < KP; ++t) A[t] = Q[t][H + lane - d] << BITS;
+        const int64_t os = off[H + lane - d], od = off[H + lane];
+        srcok = os < kOffInf;
+        const int64_t g = srcok ? os - od : 0;
+        goff = g > 0x7FFFFFFF ? 0x80000000u : (uint32_t)g;
+      }
+      const uint32_t *col = w.rpT + ((size_t)e * KP + s) * KP;
+      uint32_t acc = sat_add(A[0], col[0]);
+#pragma unroll
+      for (int t = 1; t < KP; ++t) acc = umin(acc, sat_add(A[t], col[t]));
+      if (active && s < K) table[((rowbase + i) * K + s) * (size_t)M + m] = (uint8_t)acc;
+      const uint32_t v = acc >> BITS;
+      rk[k] = active && srcok && v < CAP && c != CFP_COST_INF;
+      y[k] = rk[k] ? sat_add(sat_add(v, (uint32_t)c), goff) : kSat;
+    }
+    finish_step(i);
+  }
+
+  // The chunk holding the budget bucket reports the search.
+  if (abort_flag) flags |= MEMF_TIMEOUT;
+  if (Bb >= m0 && Bb < m0 + C) {
+    __shared__ uint32_t fin[4];
+    const int col = H + (Bb - m0);
+    uint32_t pk = kSat;
+    if (tid < KP && tid < K) pk = (Q[tid][col] << BITS) | (uint32_t)tid;
+    pk = wave_min(pk);
+    if (lane == 0) fin[wid] = pk;
+    __syncthreads();
+    if (tid == 0) {
+      const uint32_t f = umin(umin(fin[0], fin[1]), umin(fin[2], fin[3]));
+      const int64_t o = off[col];
+      const int sf = __hip_atomic_load(&w.mflags[b], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) | flags;
+      int st = CFP_ST_OK;
+      if (abort_flag || (sf & MEMF_TIMEOUT)) st = CFP_ST_TIMEOUT;
+      else if (sf & MEMF_OVERFLOW) st = CFP_ST_OVERFLOW;
+      else if (hdr->rflag) st = CFP_ST_BADINPUT;
+      else if (o >= kOffInf) st = CFP_ST_INFEASIBLE;
+      else if ((f >> BITS) != 0) st = CFP_ST_OVERFLOW;
+      status[b] = st;
+      opt[b] = st == CFP_ST_OK ? o : INT64_MAX;
+      res[b].final_state = st == CFP_ST_OK ? (int32_t)(f & ((1u << BITS) - 1u)) : -1;
+      res[b].status = st;
+      res[b].final_m = Bb;
+    }
+  }
+  if (flags & MEMF_OVERFLOW) atomicOr(&w.mflags[b], MEMF_OVERFLOW);
+}
+
+// Plan recovery for the memory variant.  The state is (s, m): the table gives
+// the predecessor strategy t = arg[i][s][m] and the budget shrinks by
+// mem[i][s].  The chase runs in windows of kMemWin steps: the argmin rows of
+// the window are loaded into LDS for the only buckets it can reach,
+// [m - kMemShift*(kMemWin-1), m], then one thread follows them.
+constexpr int kMemWin = 12;
+
+__device__ __forceinline__ int mem_index_bits(int k) {
+  int b = 4;
+  while ((1 << b) < k) ++b;
+  return b;
+}
+
+__global__ __launch_bounds__(kThreads) void mem_tb_kernel(int N, int K, int M, const uint8_t *__restrict__ table,
+                                                          const uint8_t *__restrict__ mem_copy,
+                                                          const SearchResult *__restrict__ res,
+                                                          int32_t *__restrict__ plan) {
+  extern __shared__ __align__(16) uint8_t win[];  // [kMemWin][K][width] then mem rows [kMemWin][K]
+  __shared__ int cur_s, cur_m;
+  const int b = blockIdx.x, tid = threadIdx.x;
+  int32_t *pb = plan + (size_t)b * N;
+  if (res[b].status != CFP_ST_OK) {
+    for (int i = tid; i < N; i += blockDim.x) pb[i] = -1;
+    return;
+  }
+  const int mask = (1 << mem_index_bits(K)) - 1;
+  const int width = kMemShift * (kMemWin - 1) + 1;
+  uint8_t *mrow = win + (size_t)kMemWin * K * width;
+  if (tid == 0) {
+    cur_s = res[b].final_state;
+    cur_m = res[b].final_m;
+    pb[N - 1] = cur_s;
+  }
+  __syncthreads();
+  for (int i = N - 1; i >= 1;) {
+    const int steps = i < kMemWin ? i : kMemWin;
+    const int mtop = cur_m;
+    const int lo = mtop - kMemShift * (steps - 1) > 0 ? mtop - kMemShift * (steps - 1) : 0;
+    const int wd = mtop - lo + 1;
+    for (int x = tid; x < steps * K * wd; x += blockDim.x) {
+      const int k = x / (K * wd), t = (x / wd) % K, c = x % wd;
+      win[((size_t)k * K + t) * width + c] = table[(((size_t)b * N + (i - k)) * K + t) * M + lo + c];
+    }
+    for (int x = tid; x < steps * K; x += blockDim.x)
+      mrow[x] = mem_copy[((size_t)b * N + (i - x / K)) * K + x % K];
+    __syncthreads();
+    if (tid == 0) {
+      int s = cur_s, m = mtop;
+      for (int k = 0; k < steps; ++k) {
+        int t = win[((size_t)k * K + s) * width + (m - lo)] & mask;
+        if (t >= K) t = K - 1;
+        m -= mrow[k * K + s];
+        if (m < lo) m = lo;  // cannot happen on a consistent table; stay inside the window
+        pb[i - k - 1] = t;
+        s = t;
+      }
+      cur_s = s;
+      cur_m = m;
+    }
+    __syncthreads();
+    i -= steps;
+  }
+}
+
+hipError_t launch_traceback_mem(int n, int k, int batch, int n_mem, const uint8_t *table, const uint8_t *mem,
+                                const SearchResult *res, int32_t *plan, hipStream_t st) {
+  const size_t lds = (size_t)kMemWin * k * (kMemShift * (kMemWin - 1) + 1) + (size_t)kMemWin * k;
+  hipLaunchKernelGGL(mem_tb_kernel, dim3(batch), dim3(kThreads), lds, st, n, k, n_mem, table, mem, res, plan);
+  return hipGetLastError();
+}
+
+size_t mem_region_bytes(int n, int k, int batch, int n_mem) {
+  const int KP = k <= 16 ? 16 : 32;
+  const int nchunk = (n_mem + kMemChunk - 1) / kMemChunk;
+  size_t off = 0;
+  off = align_up(off + (size_t)batch * n * KP);      // sidx
+  off = align_up(off + (size_t)batch * n * KP);      // sdel
+  off = align_up(off + (size_t)batch * n * KP * 4);  // scost
+  off = align_up(off + (size_t)12 * KP * KP * 4);    // rpT (tables beyond 12 are rejected)
+  off = align_up(off + (size_t)batch * 4);           // mflags
+  off = align_up(off + (size_t)batch * nchunk * 4);  // pub
+  off = align_up(off + (size_t)batch * nchunk * n * KP * kMemShift * 4);
+  off = align_up(off + (size_t)batch * nchunk * n * kMemShift * 8);
+  return off;
+}
+
+static MemWs carve(uint8_t *region, int n, int k, int batch, int n_mem) {
+  const int KP = k <= 16 ? 16 : 32;
+  MemWs w;
+  w.nchunk = (n_mem + kMemChunk - 1) / kMemChunk;
+  size_t off = 0;
+  w.sidx = region + off; off = align_up(off + (size_t)batch * n * KP);
+  w.sdel = region + off; off = align_up(off + (size_t)batch * n * KP);
+  w.scost = (int32_t *)(region + off); off = align_up(off + (size_t)batch * n * KP * 4);
+  w.rpT = (uint32_t *)(region + off); off = align_up(off + (size_t)12 * KP * KP * 4);
+  w.mflags = (int32_t *)(region + off); off = align_up(off + (size_t)batch * 4);
+  w.pub = (int32_t *)(region + off); off = align_up(off + (size_t)batch * w.nchunk * 4);
+  w.ring = (uint32_t *)(region + off); off = align_up(off + (size_t)batch * w.nchunk * n * KP * kMemShift * 4);
+  w.ring_off = (int64_t *)(region + off);
+  return w;
+}
+
+__global__ void mem_init_kernel(int32_t *mflags, int nb, int32_t *pub, int np) {
+  for (int x = blockIdx.x * blockDim.x + threadIdx.x; x < nb + np; x += gridDim.x * blockDim.x) {
+    if (x < nb) mflags[x] = 0;
+    else pub[x - nb] = -1;
+  }
+}
+
+template <int KP>
+static void launch_mem(const cfp_chain_desc &d, const uint8_t *mem, int n_mem, const int32_t *budget,
+                       const int32_t *redge_dev, uint8_t *table, uint8_t *mem_copy, uint8_t *region,
+                       SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st) {
+  const int N = d.n_blocks, K = d.k, B = d.batch, E = d.n_tables;
+  MemWs w = carve(region, N, K, B, n_mem);
+  hipLaunchKernelGGL(mem_init_kernel, dim3(64), dim3(256), 0, st, w.mflags, B, w.pub, B * w.nchunk);
+  hipLaunchKernelGGL(mem_pack_rtab_kernel<KP>, dim3((E * KP * KP + 255) / 256), dim3(256), 0, st, d.rtab, E, K, w.rpT);
+  hipLaunchKernelGGL(mem_prep_kernel<KP>, dim3((B * N + 3) / 4), dim3(256), 0, st, d.cost, mem, budget, N, K, n_mem, B,
+                     w.sidx, w.sdel, w.scost, mem_copy, w.mflags);
+  hipLaunchKernelGGL(mem_fwd_kernel<KP>, dim3(B * w.nchunk), dim3(kThreads), 0, st, redge_dev, budget, N, K, n_mem, B, w,
+                     table, res, hdr, opt, status);
+}
+
+bool chain_mem_supported(int k, int n_tables) { return k <= 32 && n_tables <= 12; }
+
+hipError_t launch_chain_mem_fwd(const cfp_chain_desc &d, const uint8_t *mem, int n_mem, const int32_t *budget,
+                                const int32_t *redge_dev, uint8_t *table, uint8_t *mem_copy, uint8_t *region,
+                                SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st) {
+  if (d.k <= 16)
+    launch_mem<16>(d, mem, n_mem, budget, redge_dev, table, mem_copy, region, res, hdr, opt, status, st);
+  else
+    launch_mem<32>(d, mem, n_mem, budget, redge_dev, table, mem_copy, region, res, hdr, opt, status, st);
+  return hipGetLastError();
+}
+
+}  // namespace cfp

@@ -3,15 +3,6 @@
 
 namespace cfp {
 
-hipError_t launch_chain_mem_fwd(const cfp_chain_desc &, const uint8_t *, int, const int32_t *, const int32_t *,
-                                uint8_t *, uint8_t *, SearchResult *, const WsHeader *, int64_t *, int32_t *,
-                                hipStream_t) {
-  return hipErrorNotSupported;
-}
-hipError_t launch_traceback_mem(int, int, int, int, const uint8_t *, const uint8_t *, const SearchResult *,
-                                int32_t *, hipStream_t) {
-  return hipErrorNotSupported;
-}
 hipError_t launch_scan(const cfp_chain_desc &, const int32_t *, uint8_t *, size_t, uint8_t *, int, SearchResult *,
                        const WsHeader *, int64_t *, int32_t *, hipStream_t) {
   return hipErrorNotSupported;

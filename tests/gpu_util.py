@@ -52,3 +52,23 @@ def assert_chain_parity(cost, rtab, redge, label=""):
     np.testing.assert_array_equal(g_opt, o_opt, err_msg=f"opt {label}")
     np.testing.assert_array_equal(g_plan, o_plan, err_msg=f"plan {label}")
     return g_opt, g_plan
+
+
+def run_mem(cost, rtab, redge, mem, n_mem, budget):
+    import torch
+    from paper_2504_00598_amd import search
+    res = search.dp_chain_mem(dev(cost), dev(rtab), redge, dev(mem), n_mem, dev(np.asarray(budget, np.int32)))
+    torch.cuda.synchronize()
+    return res.opt.cpu().numpy(), res.status.cpu().numpy(), res.plan.cpu().numpy()
+
+
+def assert_mem_parity(cost, rtab, redge, mem, n_mem, budget, label=""):
+    cost = np.asarray(cost, np.int32)
+    mem = np.asarray(mem, np.uint8)
+    budget = np.asarray(budget, np.int32)
+    g_opt, g_st, g_plan = run_mem(cost, rtab, redge, mem, n_mem, budget)
+    o_opt, o_plan, o_st = O.chain_mem(cost, rtab, redge, mem, budget, nthreads=oracle_threads())
+    np.testing.assert_array_equal(g_st, o_st, err_msg=f"status {label}")
+    np.testing.assert_array_equal(g_opt, o_opt, err_msg=f"opt {label}")
+    np.testing.assert_array_equal(g_plan, o_plan, err_msg=f"plan {label}")
+    return g_opt, g_plan

@@ -83,9 +83,11 @@ def test_workspace_sizes():
     d = HostDesc(N=1152, K=64, B=256)
     chain = lib.cfp_workspace_bytes(d.ref, L.CFP_V_CHAIN, 0)
     assert chain >= 256 * 1152 * 64  # one argmin byte per (search, block, state)
-    mem = lib.cfp_workspace_bytes(d.ref, L.CFP_V_MEM, 1024)
-    assert mem >= 256 * 1152 * 64 * 1024
-    assert lib.cfp_workspace_bytes(d.ref, L.CFP_V_MEM, 0) == 0
+    assert lib.cfp_workspace_bytes(d.ref, L.CFP_V_MEM, 1024) == 0  # memory variant: K <= 32
+    dm = HostDesc(N=288, K=32, B=16)
+    mem = lib.cfp_workspace_bytes(dm.ref, L.CFP_V_MEM, 1024)
+    assert mem >= 16 * 288 * 32 * 1024  # one argmin byte per (search, block, state, bucket)
+    assert lib.cfp_workspace_bytes(dm.ref, L.CFP_V_MEM, 0) == 0
     assert lib.cfp_workspace_bytes(d.ref, 9, 0) == 0
     d.c.k = 513
     assert lib.cfp_workspace_bytes(d.ref, L.CFP_V_CHAIN, 0) == 0
