@@ -1,11 +1,15 @@
-"""Benchmark of the chain search on one MI355X.
+"""Benchmark of the plan search on one MI355X.
 
-A step is one whole search of the batched chain workload (N=1152 blocks,
-K=64 strategies, 256 independent searches, 12 shared resharding tables): the
-forward min-plus pass plus the traceback of every plan, with all inputs
-already resident in device memory.  Prints one JSON line.
+A step is one whole search of a batch of synthetic chains: the forward pass
+plus the traceback of every plan, with every input already resident in
+device memory.  The default workload is the batched chain of 1152 blocks
+(96 GPT-like layers of 12 ParallelBlocks), 64 strategies per block, 256
+independent searches sharing 12 resharding tables.  Prints one JSON line.
 
     python bench.py [--steps K] [--warmup W] [--config NAME] [--no-cpu]
+
+Other workloads (--config): chain_gpt_n24_k16, mem_llama_n288_k32,
+chain_wide_n512_k256, scan_n4096_k512.
 """
 from __future__ import annotations
 
@@ -23,31 +27,124 @@ sys.path.insert(0, ROOT)
 METRIC = "min-plus cell updates/sec (K² per block per search) + search latency"
 # VALU roofline: 256 CUs x 64 lanes x 2.4 GHz = 39.32e12 32-bit lane-ops/s; a
 # min-plus cell needs one add and one min, and gfx950 does two cells in
-# three instructions (two saturating adds + one three-input min).
+# three instructions (two adds + one three-input min).
 VALU_LANE_OPS = 256 * 64 * 2.4e9
 INSTR_PER_CELL = 1.5
 PEAK_CELLS = VALU_LANE_OPS / INSTR_PER_CELL
 DEFAULT_CONFIG = "chain_gpt_n1152_k64"
 
 
-def cells_of(cfg) -> int:
-    """Min-plus cell updates of one pass: (N-1) steps of K*K per search."""
-    return cfg.B * (cfg.N - 1) * cfg.K * cfg.K
+def oracle_threads() -> int:
+    return max(1, min(16, os.cpu_count() or 1))
 
 
-def cpu_baseline(cfg, data, budget_s: float = 20.0) -> dict:
-    """The oracle (plain C, one search per thread) on a bounded sample."""
+def cells_of(cfg, data) -> int:
+    """Min-plus cell updates of one pass, K*K per block step per search (and
+    per memory bucket within the budget for the memory variant)."""
+    steps = cfg.N - 1
+    if cfg.form == "mem":
+        return int(sum(steps * cfg.K * cfg.K * (int(bb) + 1) for bb in data["budget"]))
+    return cfg.B * steps * cfg.K * cfg.K
+
+
+def scan_gemm_cells(cfg) -> int:
+    """Cells of the scan's min-plus matrix products: N-1 products of K^3."""
+    return cfg.B * (cfg.N - 1) * cfg.K ** 3
+
+
+def run_oracle(cfg, data, n=None, threads=None):
     from oracle import oracle as O
 
+    n = cfg.B if n is None else n
+    threads = threads or oracle_threads()
+    if cfg.form == "mem":
+        return O.chain_mem(data["cost"][:n], data["rtab"], data["redge"], data["mem"][:n], data["budget"][:n],
+                           nthreads=threads)
+    return O.chain(data["cost"][:n], data["rtab"], data["redge"], nthreads=threads)
+
+
+def cpu_baseline(cfg, data, budget_s: float = 10.0) -> dict:
+    """The oracle (plain C, int64, one search per thread) on a bounded sample:
+    whole searches of the same workload, repeated until about budget_s."""
     threads = max(1, min(os.cpu_count() or 1, cfg.B))
-    per_search = (cfg.N - 1) * cfg.K * cfg.K
-    # size the sample to about budget_s seconds at ~1 ns per cell per thread
-    n = int(min(cfg.B, max(threads, budget_s * 1e9 * threads / per_search / 4)))
+    per_search = cells_of(cfg, data) / cfg.B
+    n = cfg.B
     t0 = time.perf_counter()
-    O.chain(data["cost"][:n], data["rtab"], data["redge"], nthreads=min(threads, n))
+    run_oracle(cfg, data, n=min(n, threads), threads=threads)
+    first = time.perf_counter() - t0
+    # as many whole searches as fit the budget (at least one round of threads)
+    n = int(min(cfg.B, max(threads, threads * budget_s / max(first, 1e-6) / 2)))
+    reps, done, t0 = 0, 0, time.perf_counter()
+    while True:
+        run_oracle(cfg, data, n=n, threads=min(threads, n))
+        reps += 1
+        done += n
+        if time.perf_counter() - t0 > budget_s / 2 or reps >= 50:
+            break
     dt = time.perf_counter() - t0
-    return {"value": n * per_search / dt, "unit": "cell/s", "cores": min(threads, n), "kind": "oracle",
-            "sample": f"{n} of {cfg.B} searches of {cfg.name} (forward + traceback), {dt:.2f} s"}
+    return {"value": done * per_search / dt, "unit": "cell/s", "cores": min(threads, n), "kind": "oracle",
+            "sample": f"{reps} x {n} of {cfg.B} searches of {cfg.name} (forward + traceback), {dt:.2f} s"}
+
+
+class Runner:
+    """Device buffers and the two calls of one search pass."""
+
+    def __init__(self, cfg, data):
+        import torch
+
+        from paper_2504_00598_amd import _lib as L
+
+        self.L, self.cfg = L, cfg
+        cost = torch.from_numpy(data["cost"]).cuda()
+        rtab = torch.from_numpy(data["rtab"]).cuda()
+        self.desc = L.Desc(cost, rtab, data["redge"])
+        self.variant = {"chain": L.CFP_V_CHAIN, "mem": L.CFP_V_MEM, "scan": L.CFP_V_SCAN}[cfg.form]
+        self.n_mem = cfg.M if cfg.form == "mem" else 0
+        if cfg.form == "mem":
+            self.mem = torch.from_numpy(data["mem"]).cuda()
+            self.budget = torch.from_numpy(data["budget"]).cuda()
+        self.ws = torch.empty(L.cfp_workspace_bytes(self.desc, self.variant, self.n_mem), dtype=torch.uint8,
+                              device="cuda")
+        self.opt = torch.empty(cfg.B, dtype=torch.int64, device="cuda")
+        self.status = torch.empty(cfg.B, dtype=torch.int32, device="cuda")
+        self.plan = torch.empty((cfg.B, cfg.N), dtype=torch.int32, device="cuda")
+        self.stream = torch.cuda.current_stream()
+
+    def forward(self):
+        L = self.L
+        if self.variant == L.CFP_V_CHAIN:
+            L.cfp_dp_chain(self.desc, ws=self.ws, opt=self.opt, status=self.status, stream=self.stream)
+        elif self.variant == L.CFP_V_MEM:
+            L.cfp_dp_chain_mem(self.desc, self.mem, self.n_mem, self.budget, ws=self.ws, opt=self.opt,
+                               status=self.status, stream=self.stream)
+        else:
+            L.cfp_minplus_scan(self.desc, ws=self.ws, opt=self.opt, status=self.status, stream=self.stream)
+
+    def traceback(self):
+        self.L.cfp_traceback(self.desc, self.variant, self.ws, n_mem=self.n_mem, plan=self.plan, stream=self.stream)
+
+
+def search_latency_us(stream) -> dict:
+    """Wall time of one whole search of the single-chain workload (N=24,
+    K=16, one search): forward + traceback + copy of the plan to the host."""
+    import torch
+
+    from paper_2504_00598_amd import _lib as L
+    from workloads import configs
+
+    small = configs.make("chain_gpt_n24_k16")
+    sd = L.Desc(torch.from_numpy(small["cost"]).cuda(), torch.from_numpy(small["rtab"]).cuda(), small["redge"])
+    sws = torch.empty(L.cfp_workspace_bytes(sd, L.CFP_V_CHAIN), dtype=torch.uint8, device="cuda")
+    lat = []
+    for it in range(60):
+        t = time.perf_counter()
+        L.cfp_dp_chain(sd, ws=sws, stream=stream)
+        p = L.cfp_traceback(sd, L.CFP_V_CHAIN, sws, stream=stream)
+        p.cpu()
+        if it >= 10:
+            lat.append((time.perf_counter() - t) * 1e6)
+    return {"workload": "chain_gpt_n24_k16", "median": float(np.median(lat)), "p10": float(np.percentile(lat, 10)),
+            "p90": float(np.percentile(lat, 90))}
 
 
 def main() -> int:
@@ -59,35 +156,20 @@ def main() -> int:
     ap.add_argument("--no-cpu", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py runs on one GPU only: the search batch is not sharded across GPUs "
-              "(searches are independent; a multi-GPU run would split the batch).", file=sys.stderr)
+        print("bench.py runs on one GPU only: the searches of a batch are independent, so a run on several GPUs "
+              "would only split the batch; no multi-GPU path is built.", file=sys.stderr)
         return 2
 
     import torch
 
-    from paper_2504_00598_amd import _lib as L
     from workloads import configs
 
     cfg = configs.BY_NAME[args.config]
-    if cfg.form != "chain":
-        print("bench.py times the chain workloads; use the parity tests for the others", file=sys.stderr)
-        return 2
     data = configs.make(cfg)
-    cost = torch.from_numpy(data["cost"]).cuda()
-    rtab = torch.from_numpy(data["rtab"]).cuda()
-    desc = L.Desc(cost, rtab, data["redge"])
-    ws = torch.empty(L.cfp_workspace_bytes(desc, L.CFP_V_CHAIN), dtype=torch.uint8, device="cuda")
-    opt = torch.empty(cfg.B, dtype=torch.int64, device="cuda")
-    status = torch.empty(cfg.B, dtype=torch.int32, device="cuda")
-    plan = torch.empty((cfg.B, cfg.N), dtype=torch.int32, device="cuda")
-    stream = torch.cuda.current_stream()
-
-    def step():
-        L.cfp_dp_chain(desc, ws=ws, opt=opt, status=status, stream=stream)
-        L.cfp_traceback(desc, L.CFP_V_CHAIN, ws, plan=plan, stream=stream)
-
+    r = Runner(cfg, data)
     for _ in range(args.warmup):
-        step()
+        r.forward()
+        r.traceback()
     torch.cuda.synchronize()
 
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
@@ -95,44 +177,29 @@ def main() -> int:
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for a, m, b in ev:
-        a.record(stream)
-        L.cfp_dp_chain(desc, ws=ws, opt=opt, status=status, stream=stream)
-        m.record(stream)
-        L.cfp_traceback(desc, L.CFP_V_CHAIN, ws, plan=plan, stream=stream)
-        b.record(stream)
+        a.record(r.stream)
+        r.forward()
+        m.record(r.stream)
+        r.traceback()
+        b.record(r.stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     fwd_ms = float(np.mean([a.elapsed_time(m) for a, m, _ in ev]))
     tb_ms = float(np.mean([m.elapsed_time(b) for _, m, b in ev]))
     ms_per_step = wall * 1e3 / args.steps
 
-    cells = cells_of(cfg)
+    cells = cells_of(cfg, data)
     value = cells / (ms_per_step * 1e-3)
-    fwd_cells_s = cells / (fwd_ms * 1e-3)
+    work = scan_gemm_cells(cfg) if cfg.form == "scan" else cells
+    fwd_cells_s = work / (fwd_ms * 1e-3)
 
-    # search latency of the single-chain workload (N=24, K=16, batch 1): forward + traceback + sync
-    small = configs.make("chain_gpt_n24_k16")
-    sc = torch.from_numpy(small["cost"]).cuda()
-    sr = torch.from_numpy(small["rtab"]).cuda()
-    sd = L.Desc(sc, sr, small["redge"])
-    sws = torch.empty(L.cfp_workspace_bytes(sd, L.CFP_V_CHAIN), dtype=torch.uint8, device="cuda")
-    lat = []
-    for it in range(60):
-        t = time.perf_counter()
-        o, s_, _ = L.cfp_dp_chain(sd, ws=sws, stream=stream)
-        p = L.cfp_traceback(sd, L.CFP_V_CHAIN, sws, stream=stream)
-        p.cpu()
-        if it >= 10:
-            lat.append((time.perf_counter() - t) * 1e6)
+    o_opt, o_plan, o_st = run_oracle(cfg, data)
+    parity = bool(np.array_equal(r.opt.cpu().numpy(), o_opt) and np.array_equal(r.plan.cpu().numpy(), o_plan)
+                  and np.array_equal(r.status.cpu().numpy(), o_st))
 
-    # parity of this run's answer with the oracle (whole batch)
-    from oracle import oracle as O
-
-    o_opt, o_plan, o_st = O.chain(data["cost"], data["rtab"], data["redge"],
-                                  nthreads=max(1, min(16, os.cpu_count() or 1)))
-    parity = bool(np.array_equal(opt.cpu().numpy(), o_opt) and np.array_equal(plan.cpu().numpy(), o_plan)
-                  and np.array_equal(status.cpu().numpy(), o_st))
-
+    wl = {"workload": cfg.name, "blocks": cfg.N, "strategies": cfg.K, "searches": cfg.B, "resharding_tables": 12}
+    if cfg.form == "mem":
+        wl.update({"memory_buckets": cfg.M, "budgets": "1023-32b"})
     out = {
         "metric": METRIC,
         "value": value,
@@ -146,16 +213,16 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "u32",
         "data": "synthetic",
-        "config": {"workload": cfg.name, "blocks": cfg.N, "strategies": cfg.K, "searches": cfg.B,
-                   "resharding_tables": 12},
+        "config": wl,
         "forward_ms": fwd_ms,
         "traceback_ms": tb_ms,
-        "search_latency_us": {"workload": "chain_gpt_n24_k16", "median": float(np.median(lat)),
-                              "p10": float(np.percentile(lat, 10)), "p90": float(np.percentile(lat, 90))},
+        "search_latency_us": search_latency_us(r.stream),
         "parity_vs_oracle": parity,
-        "roofline": {"bound": "alu", "achieved": fwd_cells_s / 1e12, "peak": PEAK_CELLS / 1e12,
-                     "unit": "Tcell/s", "frac": fwd_cells_s / PEAK_CELLS, "traffic": None},
+        "roofline": {"bound": "alu", "achieved": fwd_cells_s / 1e12, "peak": PEAK_CELLS / 1e12, "unit": "Tcell/s",
+                     "frac": fwd_cells_s / PEAK_CELLS, "traffic": None},
     }
+    if cfg.form == "scan":
+        out["roofline"]["cells_counted"] = "min-plus matrix-product cells (N-1)*K^3 per search"
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(cfg, data)
     print(json.dumps(out), flush=True)

@@ -18,8 +18,8 @@
 // chunks of a search share one XCD and its L2.
 //
 // Arithmetic.  Column m carries an exact int64 offset o[m] = min_s D[s][m];
-// LDS holds Q[s][m] = min(D[s][m] - o[m], cap) with cap = 2^(32-b) - 1.  A
-// candidate is the saturating sum (Q[t][m-d] << b) + ((R[t][s] << b) | t)
+// LDS holds Q[s][m] = min(D[s][m] - o[m], cap) << b with cap = 2^(32-b) - 1.
+// A candidate is the saturating sum Q[t][m-d] + ((R[t][s] << b) | t)
 // with the resharding column of state s taken from SGPRs; its value is
 // relative to o[m-d], and o[m-d] - o[m] >= 0 (fewer buckets never cost
 // less) converts it.  The best candidate of any state is at most R_max
@@ -37,17 +37,18 @@ constexpr int kMemChunk = 64;  // buckets per workgroup
 constexpr int kMemShift = 16;  // largest supported mem entry (halo width)
 constexpr int64_t kOffInf = (int64_t)1 << 62;
 constexpr int kSpinLimit = 1 << 22;
+constexpr int kMemThreads = 512;  // 8 waves: two per SIMD, so one wave's waits overlap the other's work
 
 enum { MEMF_BAD = 1, MEMF_TIMEOUT = 2, MEMF_OVERFLOW = 4 };
 
-// Per-search, per-block order of the states by memory shift (stable), with
-// their shifts and costs; copies mem for the traceback; validates mem and the
-// budget.  One wave per (b, i) row.
+// Per-search, per-block order of the states by memory shift (stable), as
+// records (state | shift << 8, cost), so that a wave reads the records of its
+// states with one scalar load; copies mem for the traceback; validates mem and
+// the budget.  One wave per (b, i) row.
 template <int KP>
 __global__ __launch_bounds__(256) void mem_prep_kernel(const int32_t *__restrict__ cost, const uint8_t *__restrict__ mem,
                                                        const int32_t *__restrict__ budget, int N, int K, int M, int B,
-                                                       uint8_t *__restrict__ sidx, uint8_t *__restrict__ sdel,
-                                                       int32_t *__restrict__ scost, uint8_t *__restrict__ mem_copy,
+                                                       uint2 *__restrict__ srec, uint8_t *__restrict__ mem_copy,
                                                        int32_t *__restrict__ mflags) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
@@ -73,10 +74,9 @@ __global__ __launch_bounds__(256) void mem_prep_kernel(const int32_t *__restrict
     rank += (ko < key) || (ko == key && o < lane);
   }
   if (lane < KP) {
-    const size_t obase = (size_t)row * KP;
-    sidx[obase + rank] = (uint8_t)lane;
-    sdel[obase + rank] = (uint8_t)(lane < K ? d : 0);
-    scost[obase + rank] = lane < K ? c : CFP_COST_INF;
+    // record: x = state | shift << 8, y = cost
+    srec[(size_t)row * KP + rank] = make_uint2((uint32_t)lane | ((uint32_t)(lane < K ? d : 0) << 8),
+                                               (uint32_t)(lane < K ? c : CFP_COST_INF));
   }
 }
 
@@ -91,8 +91,7 @@ __global__ void mem_pack_rtab_kernel(const int32_t *__restrict__ rtab, int E, in
 }
 
 struct MemWs {
-  uint8_t *sidx, *sdel;
-  int32_t *scost;
+  uint2 *srec;       // [B][N][KP] records sorted by shift
   uint32_t *rpT;
   int32_t *mflags;   // [B]
   int32_t *pub;      // [B][nchunk]: last step published by each chunk
@@ -102,23 +101,26 @@ struct MemWs {
 };
 
 template <int KP>
-__global__ __launch_bounds__(kThreads) void mem_fwd_kernel(const int32_t *__restrict__ redge, const int32_t *__restrict__ budget,
+__global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__restrict__ redge, const int32_t *__restrict__ budget,
+                                                           const uint2 *__restrict__ srec, const uint32_t *__restrict__ rpT,
                                                            int N, int K, int M, int B, MemWs w, uint8_t *__restrict__ table,
                                                            SearchResult *__restrict__ res, const WsHeader *__restrict__ hdr,
                                                            int64_t *__restrict__ opt, int32_t *__restrict__ status) {
   constexpr int BITS = Pow2Bits<KP>::value;
   constexpr uint32_t CAP = (1u << (32 - BITS)) - 1u;
-  constexpr int SW = KP / 4;                 // states per wave
+  constexpr int NW = kMemThreads / 64;       // waves per workgroup
+  constexpr int SW = KP / NW;                // states per wave
   constexpr int H = kMemShift, C = kMemChunk;
   constexpr int COLS = H + C;
 
   __shared__ uint32_t Q[KP][COLS];
   __shared__ int64_t off[COLS];
-  __shared__ uint32_t part[4][C];
-  __shared__ uint32_t reach[4][C];
+  __shared__ uint32_t part[NW][C];
+  __shared__ uint32_t reach[NW][C];
   __shared__ int abort_flag;
 
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave: per-state data comes by scalar loads
   const int b = blockIdx.x % B, j = blockIdx.x / B;
   const int m0 = j * C;
   const int Bb = budget[b];
@@ -140,7 +142,7 @@ __global__ __launch_bounds__(kThreads) void mem_fwd_kernel(const int32_t *__rest
   int flags = 0;
 
   // Halo of chunk 0: buckets below 0 are infeasible.
-  for (int x = tid; x < KP * H; x += kThreads) Q[x / H][x % H] = CAP;
+  for (int x = tid; x < KP * H; x += kMemThreads) Q[x / H][x % H] = CAP << BITS;
   if (tid < H) off[tid] = kOffInf;
   __syncthreads();
 
@@ -166,41 +168,54 @@ __global__ __launch_bounds__(kThreads) void mem_fwd_kernel(const int32_t *__rest
     part[wid][lane] = pm;
     reach[wid][lane] = pr;
     __syncthreads();
-    const uint32_t cm = umin(umin(part[0][lane], part[1][lane]), umin(part[2][lane], part[3][lane]));
-    const bool feas = (reach[0][lane] | reach[1][lane] | reach[2][lane] | reach[3][lane]) != 0;
+    uint32_t cm = part[0][lane], rr = reach[0][lane];
+#pragma unroll
+    for (int x = 1; x < NW; ++x) {
+      cm = umin(cm, part[x][lane]);
+      rr |= reach[x][lane];
+    }
+    const bool feas = rr != 0;
     if (feas && cm >= 0x80000000u) flags |= MEMF_OVERFLOW;
     const int64_t onew = (feas && cm < kSat) ? off[H + lane] + (int64_t)cm : kOffInf;
-    const size_t sbase = (rowbase + i) * KP;
+    const uint2 *rec = srec + (rowbase + i) * KP + wid * SW;
 #pragma unroll
     for (int k = 0; k < SW; ++k) {
-      const int s = w.sidx[sbase + wid * SW + k];
-      const uint32_t q = (onew < kOffInf && y[k] < kSat) ? umin(y[k] - cm, CAP) : CAP;
+      const int s = rec[k].x & 0xFF;
+      const uint32_t q = ((onew < kOffInf && y[k] < kSat) ? umin(y[k] - cm, CAP) : CAP) << BITS;
       Q[s][H + lane] = q;
-      if (lane >= C - H) my_ring[((size_t)i * KP + s) * H + (lane - (C - H))] = q;
+      if (lane >= C - H)
+        __hip_atomic_store(&my_ring[((size_t)i * KP + s) * H + (lane - (C - H))], q, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
     }
     __syncthreads();  // every wave has read the old offsets
     if (wid == 0) {
       off[H + lane] = onew;
-      if (lane >= C - H) my_roff[(size_t)i * H + (lane - (C - H))] = onew;
+      if (lane >= C - H)
+        __hip_atomic_store(&my_roff[(size_t)i * H + (lane - (C - H))], onew, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
     }
-    __threadfence();
+    // Publish: the ring entries are device-scope stores; once every wave has
+    // seen them complete (vmcnt 0), one device-scope store raises the flag.
+    // Only device-scope accesses touch the ring and the flags, so no cache
+    // write-back is needed.
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (tid == 0) __hip_atomic_store(&w.pub[chunk_id], i, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    if (tid == 0) __hip_atomic_store(&w.pub[chunk_id], i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     // Halo for step i+1: the top buckets of the chunk below, at step i.
     if (j > 0 && i + 1 < N) {
       if (tid == 0) {
         int spins = 0;
-        while (__hip_atomic_load(&w.pub[chunk_id - 1], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < i) {
+        while (__hip_atomic_load(&w.pub[chunk_id - 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < i) {
           if (++spins > kSpinLimit) {
             abort_flag = 1;
             atomicOr(&w.mflags[b], MEMF_TIMEOUT);
             break;
           }
-          __builtin_amdgcn_s_sleep(2);
+          __builtin_amdgcn_s_sleep(1);
         }
       }
       __syncthreads();
-      for (int x = tid; x < KP * H; x += kThreads)
+      for (int x = tid; x < KP * H; x += kMemThreads)
         Q[x / H][x % H] = __hip_atomic_load(&lo_ring[(size_t)i * KP * H + x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (tid < H) off[tid] = __hip_atomic_load(&lo_roff[(size_t)i * H + tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __syncthreads();
@@ -210,12 +225,11 @@ __global__ __launch_bounds__(kThreads) void mem_fwd_kernel(const int32_t *__rest
   if (tid == 0) abort_flag = 0;
   // Block 0.
   {
-    const size_t sbase = rowbase * KP;
+    const uint2 *rec = srec + rowbase * KP + wid * SW;
 #pragma unroll
     for (int k = 0; k < SW; ++k) {
-      const int pos = wid * SW + k;
-      const int d = w.sdel[sbase + pos];
-      const int32_t c = w.scost[sbase + pos];
+      const int d = (rec[k].x >> 8) & 0xFF;
+      const int32_t c = (int32_t)rec[k].y;
       rk[k] = active && m >= d && c != CFP_COST_INF;
       y[k] = rk[k] ? (uint32_t)c : kSat;
     }
@@ -226,30 +240,42 @@ __global__ __launch_bounds__(kThreads) void mem_fwd_kernel(const int32_t *__rest
 
   for (int i = 1; i < N; ++i) {
     const int e = redge[i];
-    const size_t sbase = (rowbase + i) * KP;
+    const uint2 *rec = srec + (rowbase + i) * KP + wid * SW;
     uint32_t A[KP];
     int dprev = -1;
     uint32_t goff = 0;
     bool srcok = false;
+    // resharding column of the next state, loaded one state ahead (SGPRs)
+    uint32_t colc[KP], coln[KP];
+    {
+      const uint32_t *col0 = rpT + ((size_t)e * KP + (rec[0].x & 0xFF)) * KP;
+#pragma unroll
+      for (int t = 0; t < KP; ++t) coln[t] = col0[t];
+    }
 #pragma unroll
     for (int k = 0; k < SW; ++k) {
-      const int pos = wid * SW + k;
-      const int s = w.sidx[sbase + pos];
-      const int d = w.sdel[sbase + pos];
-      const int32_t c = w.scost[sbase + pos];
+      const int s = rec[k].x & 0xFF;
+      const int d = (rec[k].x >> 8) & 0xFF;
+      const int32_t c = (int32_t)rec[k].y;
+#pragma unroll
+      for (int t = 0; t < KP; ++t) colc[t] = coln[t];
+      if (k + 1 < SW) {
+        const uint32_t *col1 = rpT + ((size_t)e * KP + (rec[k + 1].x & 0xFF)) * KP;
+#pragma unroll
+        for (int t = 0; t < KP; ++t) coln[t] = col1[t];
+      }
       if (d != dprev) {
         dprev = d;
 #pragma unroll
-        for (int t = 0; t < KP; ++t) A[t] = Q[t][H + lane - d] << BITS;
+        for (int t = 0; t < KP; ++t) A[t] = Q[t][H + lane - d];
         const int64_t os = off[H + lane - d], od = off[H + lane];
         srcok = os < kOffInf;
         const int64_t g = srcok ? os - od : 0;
         goff = g > 0x7FFFFFFF ? 0x80000000u : (uint32_t)g;
       }
-      const uint32_t *col = w.rpT + ((size_t)e * KP + s) * KP;
-      uint32_t acc = sat_add(A[0], col[0]);
+      uint32_t acc = sat_add(A[0], colc[0]);
 #pragma unroll
-      for (int t = 1; t < KP; ++t) acc = umin(acc, sat_add(A[t], col[t]));
+      for (int t = 1; t < KP; ++t) acc = umin(acc, sat_add(A[t], colc[t]));
       if (active && s < K) table[((rowbase + i) * K + s) * (size_t)M + m] = (uint8_t)acc;
       const uint32_t v = acc >> BITS;
       rk[k] = active && srcok && v < CAP && c != CFP_COST_INF;
@@ -261,15 +287,10 @@ __global__ __launch_bounds__(kThreads) void mem_fwd_kernel(const int32_t *__rest
   // The chunk holding the budget bucket reports the search.
   if (abort_flag) flags |= MEMF_TIMEOUT;
   if (Bb >= m0 && Bb < m0 + C) {
-    __shared__ uint32_t fin[4];
     const int col = H + (Bb - m0);
-    uint32_t pk = kSat;
-    if (tid < KP && tid < K) pk = (Q[tid][col] << BITS) | (uint32_t)tid;
-    pk = wave_min(pk);
-    if (lane == 0) fin[wid] = pk;
-    __syncthreads();
     if (tid == 0) {
-      const uint32_t f = umin(umin(fin[0], fin[1]), umin(fin[2], fin[3]));
+      uint32_t f = kSat;
+      for (int s = 0; s < K; ++s) f = umin(f, Q[s][col] | (uint32_t)s);
       const int64_t o = off[col];
       const int sf = __hip_atomic_load(&w.mflags[b], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) | flags;
       int st = CFP_ST_OK;
@@ -294,6 +315,7 @@ __global__ __launch_bounds__(kThreads) void mem_fwd_kernel(const int32_t *__rest
 // the window are loaded into LDS for the only buckets it can reach,
 // [m - kMemShift*(kMemWin-1), m], then one thread follows them.
 constexpr int kMemWin = 12;
+constexpr int kMemWinWidth = (kMemShift * (kMemWin - 1) + 16 + 15) / 16 * 16;  // covers [lo & ~15, top]
 
 __device__ __forceinline__ int mem_index_bits(int k) {
   int b = 4;
@@ -305,6 +327,7 @@ __global__ __launch_bounds__(kThreads) void mem_tb_kernel(int N, int K, int M, c
                                                           const uint8_t *__restrict__ mem_copy,
                                                           const SearchResult *__restrict__ res,
                                                           int32_t *__restrict__ plan) {
+  // window rows are 16-byte aligned copies of [lo16, lo16 + width) of a table row
   extern __shared__ __align__(16) uint8_t win[];  // [kMemWin][K][width] then mem rows [kMemWin][K]
   __shared__ int cur_s, cur_m;
   const int b = blockIdx.x, tid = threadIdx.x;
@@ -314,8 +337,9 @@ __global__ __launch_bounds__(kThreads) void mem_tb_kernel(int N, int K, int M, c
     return;
   }
   const int mask = (1 << mem_index_bits(K)) - 1;
-  const int width = kMemShift * (kMemWin - 1) + 1;
+  const int width = kMemWinWidth;
   uint8_t *mrow = win + (size_t)kMemWin * K * width;
+  const bool vec = (M % 16) == 0;
   if (tid == 0) {
     cur_s = res[b].final_state;
     cur_m = res[b].final_m;
@@ -326,10 +350,44 @@ __global__ __launch_bounds__(kThreads) void mem_tb_kernel(int N, int K, int M, c
     const int steps = i < kMemWin ? i : kMemWin;
     const int mtop = cur_m;
     const int lo = mtop - kMemShift * (steps - 1) > 0 ? mtop - kMemShift * (steps - 1) : 0;
-    const int wd = mtop - lo + 1;
-    for (int x = tid; x < steps * K * wd; x += blockDim.x) {
-      const int k = x / (K * wd), t = (x / wd) % K, c = x % wd;
-      win[((size_t)k * K + t) * width + c] = table[(((size_t)b * N + (i - k)) * K + t) * M + lo + c];
+    const int lo16 = lo & ~15;
+    const int n16 = (mtop - lo16) / 16 + 1;  // 16-byte pieces covering [lo16, mtop]
+    if (vec) {
+      const int total = steps * K * n16;
+      for (int x0 = 0; x0 < total; x0 += 4 * kThreads) {
+        uint4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int x = x0 + u * kThreads + tid;
+          const int k = x / (K * n16), t = (x / n16) % K, c = x % n16;
+          if (x < total)
+            v[u] = *(const uint4 *)&table[(((size_t)b * N + (i - k)) * K + t) * M + lo16 + 16 * c];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int x = x0 + u * kThreads + tid;
+          const int k = x / (K * n16), t = (x / n16) % K, c = x % n16;
+          if (x < total) *(uint4 *)&win[((size_t)k * K + t) * width + 16 * c] = v[u];
+        }
+      }
+    } else {
+      const int wd = mtop - lo16 + 1;
+      const int total = steps * K * wd;
+      for (int x0 = 0; x0 < total; x0 += 16 * kThreads) {
+        uint8_t v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          const int x = x0 + u * kThreads + tid;
+          const int k = x / (K * wd), t = (x / wd) % K, c = x % wd;
+          v[u] = x < total ? table[(((size_t)b * N + (i - k)) * K + t) * M + lo16 + c] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          const int x = x0 + u * kThreads + tid;
+          const int k = x / (K * wd), t = (x / wd) % K, c = x % wd;
+          if (x < total) win[((size_t)k * K + t) * width + c] = v[u];
+        }
+      }
     }
     for (int x = tid; x < steps * K; x += blockDim.x)
       mrow[x] = mem_copy[((size_t)b * N + (i - x / K)) * K + x % K];
@@ -337,7 +395,7 @@ __global__ __launch_bounds__(kThreads) void mem_tb_kernel(int N, int K, int M, c
     if (tid == 0) {
       int s = cur_s, m = mtop;
       for (int k = 0; k < steps; ++k) {
-        int t = win[((size_t)k * K + s) * width + (m - lo)] & mask;
+        int t = win[((size_t)k * K + s) * width + (m - lo16)] & mask;
         if (t >= K) t = K - 1;
         m -= mrow[k * K + s];
         if (m < lo) m = lo;  // cannot happen on a consistent table; stay inside the window
@@ -354,7 +412,7 @@ __global__ __launch_bounds__(kThreads) void mem_tb_kernel(int N, int K, int M, c
 
 hipError_t launch_traceback_mem(int n, int k, int batch, int n_mem, const uint8_t *table, const uint8_t *mem,
                                 const SearchResult *res, int32_t *plan, hipStream_t st) {
-  const size_t lds = (size_t)kMemWin * k * (kMemShift * (kMemWin - 1) + 1) + (size_t)kMemWin * k;
+  const size_t lds = (size_t)kMemWin * k * kMemWinWidth + (size_t)kMemWin * k;
   hipLaunchKernelGGL(mem_tb_kernel, dim3(batch), dim3(kThreads), lds, st, n, k, n_mem, table, mem, res, plan);
   return hipGetLastError();
 }
@@ -363,9 +421,7 @@ size_t mem_region_bytes(int n, int k, int batch, int n_mem) {
   const int KP = k <= 16 ? 16 : 32;
   const int nchunk = (n_mem + kMemChunk - 1) / kMemChunk;
   size_t off = 0;
-  off = align_up(off + (size_t)batch * n * KP);      // sidx
-  off = align_up(off + (size_t)batch * n * KP);      // sdel
-  off = align_up(off + (size_t)batch * n * KP * 4);  // scost
+  off = align_up(off + (size_t)batch * n * KP * 8);  // srec
   off = align_up(off + (size_t)12 * KP * KP * 4);    // rpT (tables beyond 12 are rejected)
   off = align_up(off + (size_t)batch * 4);           // mflags
   off = align_up(off + (size_t)batch * nchunk * 4);  // pub
@@ -379,9 +435,7 @@ static MemWs carve(uint8_t *region, int n, int k, int batch, int n_mem) {
   MemWs w;
   w.nchunk = (n_mem + kMemChunk - 1) / kMemChunk;
   size_t off = 0;
-  w.sidx = region + off; off = align_up(off + (size_t)batch * n * KP);
-  w.sdel = region + off; off = align_up(off + (size_t)batch * n * KP);
-  w.scost = (int32_t *)(region + off); off = align_up(off + (size_t)batch * n * KP * 4);
+  w.srec = (uint2 *)(region + off); off = align_up(off + (size_t)batch * n * KP * 8);
   w.rpT = (uint32_t *)(region + off); off = align_up(off + (size_t)12 * KP * KP * 4);
   w.mflags = (int32_t *)(region + off); off = align_up(off + (size_t)batch * 4);
   w.pub = (int32_t *)(region + off); off = align_up(off + (size_t)batch * w.nchunk * 4);
@@ -406,9 +460,9 @@ static void launch_mem(const cfp_chain_desc &d, const uint8_t *mem, int n_mem, c
   hipLaunchKernelGGL(mem_init_kernel, dim3(64), dim3(256), 0, st, w.mflags, B, w.pub, B * w.nchunk);
   hipLaunchKernelGGL(mem_pack_rtab_kernel<KP>, dim3((E * KP * KP + 255) / 256), dim3(256), 0, st, d.rtab, E, K, w.rpT);
   hipLaunchKernelGGL(mem_prep_kernel<KP>, dim3((B * N + 3) / 4), dim3(256), 0, st, d.cost, mem, budget, N, K, n_mem, B,
-                     w.sidx, w.sdel, w.scost, mem_copy, w.mflags);
-  hipLaunchKernelGGL(mem_fwd_kernel<KP>, dim3(B * w.nchunk), dim3(kThreads), 0, st, redge_dev, budget, N, K, n_mem, B, w,
-                     table, res, hdr, opt, status);
+                     w.srec, mem_copy, w.mflags);
+  hipLaunchKernelGGL(mem_fwd_kernel<KP>, dim3(B * w.nchunk), dim3(kMemThreads), 0, st, redge_dev, budget, w.srec, w.rpT, N, K,
+                     n_mem, B, w, table, res, hdr, opt, status);
 }
 
 bool chain_mem_supported(int k, int n_tables) { return k <= 32 && n_tables <= 12; }
