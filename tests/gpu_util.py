@@ -72,3 +72,23 @@ def assert_mem_parity(cost, rtab, redge, mem, n_mem, budget, label=""):
     np.testing.assert_array_equal(g_opt, o_opt, err_msg=f"opt {label}")
     np.testing.assert_array_equal(g_plan, o_plan, err_msg=f"plan {label}")
     return g_opt, g_plan
+
+
+def run_scan(cost, rtab, redge):
+    import torch
+    from paper_2504_00598_amd import search
+    res = search.minplus_scan(dev(cost), dev(rtab), redge)
+    torch.cuda.synchronize()
+    return res.opt.cpu().numpy(), res.status.cpu().numpy(), res.plan.cpu().numpy()
+
+
+def assert_scan_parity(cost, rtab, redge, label=""):
+    cost = np.asarray(cost, np.int32)
+    if cost.ndim == 2:
+        cost = cost[None]
+    g_opt, g_st, g_plan = run_scan(cost, rtab, redge)
+    o_opt, o_plan, o_st = O.chain(cost, rtab, redge, nthreads=oracle_threads())
+    np.testing.assert_array_equal(g_st, o_st, err_msg=f"status {label}")
+    np.testing.assert_array_equal(g_opt, o_opt, err_msg=f"opt {label}")
+    np.testing.assert_array_equal(g_plan, o_plan, err_msg=f"plan {label}")
+    return g_opt, g_plan
