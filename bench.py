@@ -34,6 +34,58 @@ PEAK_CELLS = VALU_LANE_OPS / INSTR_PER_CELL
 DEFAULT_CONFIG = "chain_gpt_n1152_k64"
 
 
+# The kernel that dominates the forward pass of each workload, and the source
+# files it is built from.
+KERNELS = {
+    "chain_gpt_n24_k16": ("chain_fwd_res_kernel<16,12>", ["chain_fwd_res.hip", "res_common.h"]),
+    "chain_gpt_n1152_k64": ("chain_fwd_k64_kernel<12>", ["chain_fwd_k64.hip", "res_common.h"]),
+    "mem_llama_n288_k32": ("mem_fwd_kernel<32>", ["mem_fwd.hip", "res_common.h"]),
+    "chain_wide_n512_k256": ("chain_fwd_kernel<256>", ["chain_fwd.hip"]),
+    "scan_n4096_k512": ("scan_gemm_kernel", ["scan.hip"]),
+}
+COMMON_SOURCES = ["common.h", "cfp_internal.h", "../../include/cfp.h"]
+
+# HBM bytes per launch of the dominant kernel, from two rocprofv3 --pmc runs
+# of this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each scaled
+# by the factor that maps the counter onto the bytes of a plain 512 MiB copy
+# (bench.py --calibrate-copy: FETCH_SIZE reads 262159 KiB -> x2.000,
+# WRITE_SIZE reads 524288 KiB -> x1.000).  "sources" is sources_hash() of the
+# kernel when the counters were taken; a different hash means the kernel has
+# changed and the figure is withheld.
+FETCH_SCALE, WRITE_SCALE = 524288.0 / 262159.1, 524288.0 / 524288.0
+TRAFFIC = {
+    "chain_gpt_n24_k16": {"fetch_kib": 18.4, "write_kib": 0.5, "sources": "8f49cac9c912f637"},
+    "chain_gpt_n1152_k64": {"fetch_kib": 37915.9, "write_kib": 18456.0, "sources": "5a97ee1ff90b424c"},
+    "mem_llama_n288_k32": {"fetch_kib": 60535.6, "write_kib": 239222.6, "sources": "d668d626f64cdbd7"},
+    "chain_wide_n512_k256": {"fetch_kib": 31097.5, "write_kib": 8183.9, "sources": "16b4cb1f0976b7ba"},
+    # mean over the 12 matrix-product launches of one forward call
+    "scan_n4096_k512": {"fetch_kib": 3038953.7, "write_kib": 1398442.5, "sources": "de7227e316558ba4"},
+}
+
+
+def sources_hash(config: str) -> str:
+    """Hash of the kernel's sources with comments and blank space removed, so
+    that only a change of code withholds the traffic figure."""
+    import hashlib
+    import re
+
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2504_00598_amd", "csrc")
+    for f in KERNELS[config][1] + COMMON_SOURCES:
+        with open(os.path.join(csrc, f)) as fh:
+            code = re.sub(r"/\*.*?\*/", " ", fh.read(), flags=re.S)
+        code = re.sub(r"//[^\n]*", " ", code)
+        h.update(" ".join(code.split()).encode())
+    return h.hexdigest()[:16]
+
+
+def traffic_bytes(config: str):
+    t = TRAFFIC.get(config)
+    if t is None or t["sources"] != sources_hash(config):
+        return None
+    return (t["fetch_kib"] * FETCH_SCALE + t["write_kib"] * WRITE_SCALE) * 1024.0
+
+
 def oracle_threads() -> int:
     return max(1, min(16, os.cpu_count() or 1))
 
@@ -79,7 +131,7 @@ def cpu_baseline(cfg, data, budget_s: float = 10.0) -> dict:
         run_oracle(cfg, data, n=n, threads=min(threads, n))
         reps += 1
         done += n
-        if time.perf_counter() - t0 > budget_s / 2 or reps >= 50:
+        if time.perf_counter() - t0 > budget_s:
             break
     dt = time.perf_counter() - t0
     return {"value": done * per_search / dt, "unit": "cell/s", "cores": min(threads, n), "kind": "oracle",
@@ -95,7 +147,7 @@ class Runner:
         from paper_2504_00598_amd import _lib as L
 
         self.L, self.cfg = L, cfg
-        cost = torch.from_numpy(data["cost"]).cuda()
+        self.cost = cost = torch.from_numpy(data["cost"]).cuda()
         rtab = torch.from_numpy(data["rtab"]).cuda()
         self.desc = L.Desc(cost, rtab, data["redge"])
         self.variant = {"chain": L.CFP_V_CHAIN, "mem": L.CFP_V_MEM, "scan": L.CFP_V_SCAN}[cfg.form]
@@ -124,6 +176,34 @@ class Runner:
         self.L.cfp_traceback(self.desc, self.variant, self.ws, n_mem=self.n_mem, plan=self.plan, stream=self.stream)
 
 
+def pcie_inclusive(r, data, reps: int = 5) -> dict:
+    """Whole-job rate when the cost (and mem) tables start in pinned host
+    memory and the plans end there: host-to-device copy + forward + traceback
+    + device-to-host copy of the plans, wall time per pass."""
+    import torch
+
+    host = {"cost": torch.from_numpy(data["cost"]).pin_memory()}
+    if r.cfg.form == "mem":
+        host["mem"] = torch.from_numpy(data["mem"]).pin_memory()
+    plan = torch.empty(tuple(r.plan.shape), dtype=torch.int32).pin_memory()
+    dt = []
+    for it in range(reps + 1):
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        r.cost.copy_(host["cost"], non_blocking=True)
+        if "mem" in host:
+            r.mem.copy_(host["mem"], non_blocking=True)
+        r.forward()
+        r.traceback()
+        plan.copy_(r.plan, non_blocking=True)
+        torch.cuda.synchronize()
+        if it:
+            dt.append(time.perf_counter() - t)
+    ms = float(np.median(dt)) * 1e3
+    return {"ms_per_pass": ms, "cell_per_s": cells_of(r.cfg, data) / (ms * 1e-3),
+            "host_bytes": int(sum(v.numel() * v.element_size() for v in host.values()) + plan.numel() * 4)}
+
+
 def search_latency_us(stream) -> dict:
     """Wall time of one whole search of the single-chain workload (N=24,
     K=16, one search): forward + traceback + copy of the plan to the host."""
@@ -147,6 +227,23 @@ def search_latency_us(stream) -> dict:
             "p90": float(np.percentile(lat, 90))}
 
 
+COPY_BYTES = 512 << 20
+
+
+def calibrate_copy() -> int:
+    """A plain copy of COPY_BYTES bytes, three times: rocprofv3's FETCH_SIZE and
+    WRITE_SIZE of this dispatch give the counter-to-byte scale factors."""
+    import torch
+
+    a = torch.ones(COPY_BYTES // 4, dtype=torch.int32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": COPY_BYTES, "copy_bytes_written": COPY_BYTES, "copies": 3}), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -154,7 +251,11 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default=DEFAULT_CONFIG)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 512 MiB device-to-device copy (reference for the HBM byte counters)")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        return calibrate_copy()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the searches of a batch are independent, so a run on several GPUs "
               "would only split the batch; no multi-GPU path is built.", file=sys.stderr)
@@ -174,6 +275,10 @@ def main() -> int:
 
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
            torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    # the library brackets each launch of the dominant kernel with HIP events
+    # on the stream it is launched on
+    L = r.L
+    L.cfp_timer_start(args.steps * 64)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for a, m, b in ev:
@@ -184,6 +289,7 @@ def main() -> int:
         b.record(r.stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    kern_ms, kern_launches = L.cfp_timer_stop()
     fwd_ms = float(np.mean([a.elapsed_time(m) for a, m, _ in ev]))
     tb_ms = float(np.mean([m.elapsed_time(b) for _, m, b in ev]))
     ms_per_step = wall * 1e3 / args.steps
@@ -191,6 +297,10 @@ def main() -> int:
     cells = cells_of(cfg, data)
     value = cells / (ms_per_step * 1e-3)
     work = scan_gemm_cells(cfg) if cfg.form == "scan" else cells
+    # per launch: the algorithmic cells of one launch over its average duration
+    # (the scan's products differ in size per level: total cells over total time)
+    kern_avg_ms = kern_ms / max(kern_launches, 1)
+    kern_cells_s = work * args.steps / (kern_ms * 1e-3) if kern_launches else 0.0
     fwd_cells_s = work / (fwd_ms * 1e-3)
 
     o_opt, o_plan, o_st = run_oracle(cfg, data)
@@ -217,9 +327,12 @@ def main() -> int:
         "forward_ms": fwd_ms,
         "traceback_ms": tb_ms,
         "search_latency_us": search_latency_us(r.stream),
+        "pcie_inclusive": pcie_inclusive(r, data),
         "parity_vs_oracle": parity,
-        "roofline": {"bound": "alu", "achieved": fwd_cells_s / 1e12, "peak": PEAK_CELLS / 1e12, "unit": "Tcell/s",
-                     "frac": fwd_cells_s / PEAK_CELLS, "traffic": None},
+        "roofline": {"bound": "alu", "achieved": kern_cells_s / 1e12, "peak": PEAK_CELLS / 1e12, "unit": "Tcell/s",
+                     "frac": kern_cells_s / PEAK_CELLS, "traffic": traffic_bytes(cfg.name),
+                     "kernel": KERNELS[cfg.name][0], "kernel_launches_per_step": kern_launches / args.steps,
+                     "kernel_avg_us": kern_avg_ms * 1e3, "forward_call_cells_per_s": fwd_cells_s},
     }
     if cfg.form == "scan":
         out["roofline"]["cells_counted"] = "min-plus matrix-product cells (N-1)*K^3 per search"

@@ -39,7 +39,8 @@
  *    documented range, CFP_ST_INFEASIBLE when no plan exists (a block with
  *    every strategy unavailable, or no plan within the memory budget).  When
  *    status[b] != CFP_ST_OK, opt[b] = INT64_MAX and the traced plan is all -1.
- *  - No global mutable state: calls on different streams with different
+ *  - No global mutable state (apart from the opt-in benchmarking timer at
+ *    the end of this file): calls on different streams with different
  *    workspaces may run concurrently.
  */
 #ifndef CFP_H
@@ -71,7 +72,7 @@ enum {
   CFP_ST_OK = 0,
   CFP_ST_INFEASIBLE = 1, /* no plan (all strategies unavailable at a block, or budget too small) */
   CFP_ST_OVERFLOW = 2,   /* reserved: device arithmetic left its exact range (not reachable with valid inputs) */
-  CFP_ST_TIMEOUT = 3,    /* reserved: a bounded device wait expired */
+  CFP_ST_TIMEOUT = 3,    /* a bounded device wait of the memory variant's pipeline expired */
   CFP_ST_BADINPUT = 4    /* a device array value is outside its documented range */
 };
 
@@ -120,10 +121,17 @@ int cfp_dp_chain(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t *op
  *     D[i][s][m] = c[i][s] + min_t D[i-1][t][m - mem[i][s]] + R_{e(i)}[t][s]
  * with D[0][s][m] = c[0][s] if mem[0][s] <= m; the answer is
  * min_s D[N-1][s][budget[b]] (total memory <= budget, inclusive).
- *   mem    device [B][N][K] uint8, each entry in [0, n_mem)
+ *   mem    device [B][N][K] uint8, each entry in [0, n_mem) and at most 16
+ *          (the memory of one block is a small number of buckets; a larger
+ *          entry gives status CFP_ST_BADINPUT)
  *   n_mem  M, the number of memory buckets, 1 <= M <= 4096
  *   budget device [B] int32, each in [0, M)
- * ws must hold cfp_workspace_bytes(d, CFP_V_MEM, n_mem) bytes. */
+ * Supported for K <= 32 and n_tables <= 12 (CFP_ERR_UNSUPPORTED otherwise).
+ * The buckets of a search are cut into chunks of 64 that run as a pipeline of
+ * workgroups; a chunk that waits too long for the chunk below it (which
+ * cannot happen when the GPU is not shared) ends its search with
+ * CFP_ST_TIMEOUT.  ws must hold cfp_workspace_bytes(d, CFP_V_MEM, n_mem)
+ * bytes. */
 int cfp_dp_chain_mem(const cfp_chain_desc *d, const uint8_t *mem, int32_t n_mem, const int32_t *budget,
                      void *ws, size_t ws_bytes, int64_t *opt, int32_t *status, void *stream);
 
@@ -131,8 +139,12 @@ int cfp_dp_chain_mem(const cfp_chain_desc *d, const uint8_t *mem, int32_t n_mem,
  * block i becomes the transfer matrix T_i[t][s] = R_{e(i)}[t][s] + c[i][s]
  * (T_0[t][s] = c[0][s]), the matrices are composed by a tree of min-plus
  * matrix products (min-plus matrix product is associative), and a down-sweep
- * recovers every prefix vector D[i].  For long chains.  ws must hold
- * cfp_workspace_bytes(d, CFP_V_SCAN, 0) bytes. */
+ * recovers every prefix vector D[i].  For long chains.  Products are kept in
+ * 32-bit words relative to their minimum, so besides the R bound of
+ * cfp_r_limit the available costs of every block must lie within 2^30 of
+ * each other (max_s c[i][s] - min_s c[i][s] < 2^30 over available s);
+ * otherwise the search ends with CFP_ST_BADINPUT.  ws must hold
+ * cfp_workspace_bytes(d, CFP_V_SCAN, 0) bytes (about B * N * K * K * 4). */
 int cfp_minplus_scan(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t *opt, int32_t *status,
                      void *stream);
 
@@ -145,6 +157,21 @@ int cfp_minplus_scan(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t
  *   plan   device [B][N] int32; all -1 for a search whose status is not OK. */
 int cfp_traceback(const cfp_chain_desc *d, int32_t variant, int32_t n_mem, void *ws, size_t ws_bytes,
                   int32_t *plan, void *stream);
+
+/* Benchmarking aid (not needed for searching).  cfp_timer_start creates
+ * max_launches pairs of HIP events (1 <= max_launches <= 2^20) and arms
+ * recording: from then on every launch of a forward call's main kernel (the
+ * chain step kernel of cfp_dp_chain, the step kernel of cfp_dp_chain_mem,
+ * each min-plus matrix-product launch of cfp_minplus_scan) is bracketed by
+ * one pair recorded on the call's stream, until the pairs run out.
+ * cfp_timer_stop waits for the recorded events, writes the summed device
+ * time in milliseconds and the number of bracketed launches, disarms
+ * recording and destroys the events.  The timer is process-wide state behind
+ * a lock, meant for one benchmarking thread; it is the only global state of
+ * the library.  Returns CFP_OK, CFP_ERR_ARG (bad count, start while armed,
+ * stop while not armed) or CFP_ERR_HIP. */
+int cfp_timer_start(int32_t max_launches);
+int cfp_timer_stop(double *total_ms, int32_t *launches);
 
 /* Static string for a CFP_ERR_* or CFP_ST_* code (status codes are >= 0). */
 const char *cfp_status_string(int code);

@@ -34,7 +34,7 @@ CFP_COST_INF = 0x7FFFFFFF
 CFP_MAX_K = 512
 
 EXPORTED = ("cfp_r_limit", "cfp_workspace_bytes", "cfp_dp_chain", "cfp_dp_chain_mem", "cfp_minplus_scan",
-            "cfp_traceback", "cfp_status_string")
+            "cfp_traceback", "cfp_status_string", "cfp_timer_start", "cfp_timer_stop")
 
 
 class CfpError(RuntimeError):
@@ -79,6 +79,10 @@ def lib() -> ctypes.CDLL:
         L.cfp_minplus_scan.restype = ctypes.c_int
         L.cfp_traceback.argtypes = [D, I32, I32, P, ctypes.c_size_t, P, P]
         L.cfp_traceback.restype = ctypes.c_int
+        L.cfp_timer_start.argtypes = [I32]
+        L.cfp_timer_start.restype = ctypes.c_int
+        L.cfp_timer_stop.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I32)]
+        L.cfp_timer_stop.restype = ctypes.c_int
         L.cfp_status_string.argtypes = [ctypes.c_int]
         L.cfp_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -91,6 +95,21 @@ def status_string(code: int) -> str:
 
 def cfp_r_limit(variant: int, k: int) -> int:
     return int(lib().cfp_r_limit(variant, k))
+
+
+def cfp_timer_start(max_launches: int) -> None:
+    rc = lib().cfp_timer_start(int(max_launches))
+    if rc != CFP_OK:
+        raise CfpError("cfp_timer_start", rc)
+
+
+def cfp_timer_stop() -> tuple[float, int]:
+    """(summed device milliseconds, bracketed launches) of the armed timer."""
+    ms, n = ctypes.c_double(0.0), ctypes.c_int32(0)
+    rc = lib().cfp_timer_stop(ctypes.byref(ms), ctypes.byref(n))
+    if rc != CFP_OK:
+        raise CfpError("cfp_timer_stop", rc)
+    return ms.value, n.value
 
 
 # ------------------------------------------------------------- marshalling --

@@ -3,6 +3,8 @@
 // first HIP call, so argument errors never touch the device.
 #include <string.h>
 
+#include <atomic>
+#include <mutex>
 #include <vector>
 
 #include "cfp_internal.h"
@@ -41,6 +43,30 @@ WsLayout layout(int variant, int n, int k, int batch, int n_mem) {
   }
   L.total = off;
   return L;
+}
+
+// Benchmarking timer (cfp_timer_start / cfp_timer_stop).  Slot 2j and 2j+1
+// hold the events around the j-th recorded launch.
+namespace {
+std::mutex g_timer_mu;
+std::atomic<bool> g_timer_on{false};
+std::vector<hipEvent_t> g_timer_ev;
+size_t g_timer_used = 0;
+bool g_timer_open = false;
+}  // namespace
+
+void timer_begin(hipStream_t st) {
+  if (!g_timer_on.load(std::memory_order_acquire)) return;
+  std::lock_guard<std::mutex> lk(g_timer_mu);
+  g_timer_open = 2 * g_timer_used + 1 < g_timer_ev.size() &&
+                 hipEventRecord(g_timer_ev[2 * g_timer_used], st) == hipSuccess;
+}
+
+void timer_end(hipStream_t st) {
+  if (!g_timer_on.load(std::memory_order_acquire)) return;
+  std::lock_guard<std::mutex> lk(g_timer_mu);
+  if (g_timer_open && hipEventRecord(g_timer_ev[2 * g_timer_used + 1], st) == hipSuccess) ++g_timer_used;
+  g_timer_open = false;
 }
 
 }  // namespace cfp
@@ -193,6 +219,45 @@ int cfp_traceback(const cfp_chain_desc *d, int32_t variant, int32_t n_mem, void 
                                (const SearchResult *)(w + L.result), (uint16_t *)(w + L.maps),
                                (int32_t *)(w + L.bounds), L.nchunks, plan, st);
   return e == hipSuccess ? CFP_OK : CFP_ERR_HIP;
+}
+
+int cfp_timer_start(int32_t max_launches) {
+  if (max_launches < 1 || max_launches > (1 << 20)) return CFP_ERR_ARG;
+  std::lock_guard<std::mutex> lk(g_timer_mu);
+  if (g_timer_on.load()) return CFP_ERR_ARG;
+  g_timer_ev.assign(2 * (size_t)max_launches, nullptr);
+  for (auto &e : g_timer_ev)
+    if (hipEventCreate(&e) != hipSuccess) {
+      for (auto &f : g_timer_ev)
+        if (f) hipEventDestroy(f);
+      g_timer_ev.clear();
+      return CFP_ERR_HIP;
+    }
+  g_timer_used = 0;
+  g_timer_open = false;
+  g_timer_on.store(true, std::memory_order_release);
+  return CFP_OK;
+}
+
+int cfp_timer_stop(double *total_ms, int32_t *launches) {
+  std::lock_guard<std::mutex> lk(g_timer_mu);
+  if (!g_timer_on.load()) return CFP_ERR_ARG;
+  g_timer_on.store(false, std::memory_order_release);
+  int rc = CFP_OK;
+  double sum = 0.0;
+  for (size_t j = 0; j < g_timer_used; ++j) {
+    float ms = 0.f;
+    if (hipEventSynchronize(g_timer_ev[2 * j + 1]) != hipSuccess ||
+        hipEventElapsedTime(&ms, g_timer_ev[2 * j], g_timer_ev[2 * j + 1]) != hipSuccess)
+      rc = CFP_ERR_HIP;
+    sum += ms;
+  }
+  for (auto &e : g_timer_ev) hipEventDestroy(e);
+  g_timer_ev.clear();
+  if (total_ms) *total_ms = sum;
+  if (launches) *launches = (int32_t)g_timer_used;
+  g_timer_used = 0;
+  return rc;
 }
 
 const char *cfp_status_string(int code) {

@@ -85,4 +85,9 @@ hipError_t launch_scan(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_
                        int32_t *status, hipStream_t st);
 size_t scan_region_bytes(int n, int k, int batch);
 
+// Benchmarking timer: when armed, brackets each launch of a forward call's
+// main kernel with a pair of HIP events on that launch's stream.
+void timer_begin(hipStream_t st);
+void timer_end(hipStream_t st);
+
 }  // namespace cfp

@@ -181,15 +181,21 @@ hipError_t launch_chain_fwd(const cfp_chain_desc &d, const int32_t *redge_dev, u
                             SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
                             hipStream_t st) {
   (void)elem;
-  if (chain_fwd_res_supported(d.k, d.n_tables))
-    return launch_chain_fwd_res(d, redge_dev, table, res, hdr, opt, status, st);
+  if (chain_fwd_res_supported(d.k, d.n_tables)) {
+    timer_begin(st);
+    const hipError_t e = launch_chain_fwd_res(d, redge_dev, table, res, hdr, opt, status, st);
+    timer_end(st);
+    return e;
+  }
   const int k = d.k;
+  timer_begin(st);
   if (k <= 16) launch_kp<16>(d, redge_dev, table, res, hdr, opt, status, st);
   else if (k <= 32) launch_kp<32>(d, redge_dev, table, res, hdr, opt, status, st);
   else if (k <= 64) launch_kp<64>(d, redge_dev, table, res, hdr, opt, status, st);
   else if (k <= 128) launch_kp<128>(d, redge_dev, table, res, hdr, opt, status, st);
   else if (k <= 256) launch_kp<256>(d, redge_dev, table, res, hdr, opt, status, st);
   else launch_kp<512>(d, redge_dev, table, res, hdr, opt, status, st);
+  timer_end(st);
   return hipGetLastError();
 }
 

@@ -11,9 +11,11 @@
 // buckets m of the chunk, wave w over a quarter of the states.  Step i of a
 // chunk only reads buckets m - mem[i][s] >= m - kMemShift of step i-1, so a
 // chunk needs the top kMemShift buckets of the chunk below it: each chunk
-// publishes them in a device ring (one slot per step) and raises a flag;
-// the chunk above waits for the flag (release/acquire at agent scope, bounded
-// spin).  Chunks of one search have workgroup ids j*B + b, so a producer
+// publishes them in a device ring (one slot per step) and then raises a
+// counter; the chunk above waits for the counter (bounded spin).  The ring
+// and the counters are only touched by device-scope atomic stores and loads,
+// and the counter is raised after every ring store has completed, so no cache
+// write-back or invalidation is needed.  Chunks of one search have workgroup ids j*B + b, so a producer
 // always has a lower id than its consumer and, for B a multiple of 8, all
 // chunks of a search share one XCD and its L2.
 //
@@ -461,8 +463,10 @@ static void launch_mem(const cfp_chain_desc &d, const uint8_t *mem, int n_mem, c
   hipLaunchKernelGGL(mem_pack_rtab_kernel<KP>, dim3((E * KP * KP + 255) / 256), dim3(256), 0, st, d.rtab, E, K, w.rpT);
   hipLaunchKernelGGL(mem_prep_kernel<KP>, dim3((B * N + 3) / 4), dim3(256), 0, st, d.cost, mem, budget, N, K, n_mem, B,
                      w.srec, mem_copy, w.mflags);
+  timer_begin(st);
   hipLaunchKernelGGL(mem_fwd_kernel<KP>, dim3(B * w.nchunk), dim3(kMemThreads), 0, st, redge_dev, budget, w.srec, w.rpT, N, K,
                      n_mem, B, w, table, res, hdr, opt, status);
+  timer_end(st);
 }
 
 bool chain_mem_supported(int k, int n_tables) { return k <= 32 && n_tables <= 12; }

@@ -526,6 +526,7 @@ hipError_t launch_scan(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_
       const dim3 grid((KP / kTile) * (KP / kTile), pairs, B);
       // vector loads need unpadded rows and 16-byte aligned inputs
       const bool full = K == KP && ((uintptr_t)d.cost % 16) == 0 && ((uintptr_t)d.rtab % 16) == 0;
+      timer_begin(st);
       if (l == 1) {
         if (full) hipLaunchKernelGGL((scan_gemm_kernel<true, true>), grid, dim3(256), 0, st, a);
         else hipLaunchKernelGGL((scan_gemm_kernel<true, false>), grid, dim3(256), 0, st, a);
@@ -533,6 +534,7 @@ hipError_t launch_scan(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_
         if (full) hipLaunchKernelGGL((scan_gemm_kernel<false, true>), grid, dim3(256), 0, st, a);
         else hipLaunchKernelGGL((scan_gemm_kernel<false, false>), grid, dim3(256), 0, st, a);
       }
+      timer_end(st);
     }
     if (S.cnt[l - 1] & 1) hipLaunchKernelGGL(scan_carry_kernel, dim3(64, B), dim3(256), 0, st, a);
     hipLaunchKernelGGL(scan_tot_kernel, dim3((B * S.cnt[l] + 255) / 256), dim3(256), 0, st, a,
