@@ -11,7 +11,7 @@
 
 namespace cfp {
 
-WsLayout layout(int variant, int n, int k, int batch, int n_mem) {
+WsLayout layout(int variant, int n, int k, int batch, int n_mem, int n_tables) {
   WsLayout L;
   L.elem = k > 256 ? 2 : 1;
   size_t off = sizeof(WsHeader);
@@ -36,6 +36,10 @@ WsLayout layout(int variant, int n, int k, int batch, int n_mem) {
   off = align_up(off + (size_t)batch * L.nchunks * k * 2);
   L.bounds = off;
   off = align_up(off + (size_t)batch * L.nchunks * 4);
+  if (variant == CFP_V_CHAIN && chain_fwd_wide_supported(k)) {
+    L.wide = off;
+    off = align_up(off + wide_region_bytes(n, k, batch, n_tables));
+  }
   if (variant == CFP_V_SCAN) {
     L.scan = off;
     L.scan_bytes = scan_region_bytes(n, k, batch);
@@ -137,7 +141,7 @@ size_t cfp_workspace_bytes(const cfp_chain_desc *d, int32_t variant, int32_t n_m
   } else if (variant != CFP_V_CHAIN && variant != CFP_V_SCAN) {
     return 0;
   }
-  return layout(variant, d->n_blocks, d->k, d->batch, variant == CFP_V_MEM ? n_mem : 0).total;
+  return layout(variant, d->n_blocks, d->k, d->batch, variant == CFP_V_MEM ? n_mem : 0, d->n_tables).total;
 }
 
 int cfp_dp_chain(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t *opt, int32_t *status,
@@ -145,7 +149,7 @@ int cfp_dp_chain(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t *op
   int rc = check_desc(d);
   if (rc != CFP_OK) return rc;
   if (!opt || !status) return CFP_ERR_ARG;
-  WsLayout L = layout(CFP_V_CHAIN, d->n_blocks, d->k, d->batch, 0);
+  WsLayout L = layout(CFP_V_CHAIN, d->n_blocks, d->k, d->batch, 0, d->n_tables);
   if (!ws || ws_bytes < L.total) return CFP_ERR_WORKSPACE;
   hipStream_t st = (hipStream_t)stream;
   uint8_t *w = (uint8_t *)ws;
@@ -153,8 +157,8 @@ int cfp_dp_chain(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t *op
   WsHeader *hdr = (WsHeader *)w;
   if (launch_validate_rtab(d->rtab, d->n_tables, d->k, cfp_r_limit(CFP_V_CHAIN, d->k), hdr, st) != hipSuccess)
     return CFP_ERR_HIP;
-  if (launch_chain_fwd(*d, (const int32_t *)(w + L.redge), w + L.table, L.elem, (SearchResult *)(w + L.result),
-                       hdr, opt, status, st) != hipSuccess)
+  if (launch_chain_fwd(*d, (const int32_t *)(w + L.redge), w + L.table, L.elem, w + L.wide,
+                       (SearchResult *)(w + L.result), hdr, opt, status, st) != hipSuccess)
     return CFP_ERR_HIP;
   return CFP_OK;
 }
@@ -166,7 +170,7 @@ int cfp_dp_chain_mem(const cfp_chain_desc *d, const uint8_t *mem, int32_t n_mem,
   if (!mem || !budget || !opt || !status) return CFP_ERR_ARG;
   if (n_mem < 1) return CFP_ERR_ARG;
   if (n_mem > 4096 || !chain_mem_supported(d->k, d->n_tables)) return CFP_ERR_UNSUPPORTED;
-  WsLayout L = layout(CFP_V_MEM, d->n_blocks, d->k, d->batch, n_mem);
+  WsLayout L = layout(CFP_V_MEM, d->n_blocks, d->k, d->batch, n_mem, d->n_tables);
   if (!ws || ws_bytes < L.total) return CFP_ERR_WORKSPACE;
   hipStream_t st = (hipStream_t)stream;
   uint8_t *w = (uint8_t *)ws;
@@ -185,7 +189,7 @@ int cfp_minplus_scan(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t
   int rc = check_desc(d);
   if (rc != CFP_OK) return rc;
   if (!opt || !status) return CFP_ERR_ARG;
-  WsLayout L = layout(CFP_V_SCAN, d->n_blocks, d->k, d->batch, 0);
+  WsLayout L = layout(CFP_V_SCAN, d->n_blocks, d->k, d->batch, 0, d->n_tables);
   if (!ws || ws_bytes < L.total) return CFP_ERR_WORKSPACE;
   hipStream_t st = (hipStream_t)stream;
   uint8_t *w = (uint8_t *)ws;
@@ -206,7 +210,7 @@ int cfp_traceback(const cfp_chain_desc *d, int32_t variant, int32_t n_mem, void 
   if (variant != CFP_V_CHAIN && variant != CFP_V_MEM && variant != CFP_V_SCAN) return CFP_ERR_ARG;
   if (variant == CFP_V_MEM && (n_mem < 1 || n_mem > 4096 || !chain_mem_supported(d->k, d->n_tables)))
     return CFP_ERR_ARG;
-  WsLayout L = layout(variant, d->n_blocks, d->k, d->batch, variant == CFP_V_MEM ? n_mem : 0);
+  WsLayout L = layout(variant, d->n_blocks, d->k, d->batch, variant == CFP_V_MEM ? n_mem : 0, d->n_tables);
   if (!ws || ws_bytes < L.total) return CFP_ERR_WORKSPACE;
   hipStream_t st = (hipStream_t)stream;
   uint8_t *w = (uint8_t *)ws;
@@ -229,7 +233,7 @@ int cfp_timer_start(int32_t max_launches) {
   for (auto &e : g_timer_ev)
     if (hipEventCreate(&e) != hipSuccess) {
       for (auto &f : g_timer_ev)
-        if (f) hipEventDestroy(f);
+        if (f) (void)hipEventDestroy(f);
       g_timer_ev.clear();
       return CFP_ERR_HIP;
     }
@@ -252,7 +256,7 @@ int cfp_timer_stop(double *total_ms, int32_t *launches) {
       rc = CFP_ERR_HIP;
     sum += ms;
   }
-  for (auto &e : g_timer_ev) hipEventDestroy(e);
+  for (auto &e : g_timer_ev) (void)hipEventDestroy(e);
   g_timer_ev.clear();
   if (total_ms) *total_ms = sum;
   if (launches) *launches = (int32_t)g_timer_used;

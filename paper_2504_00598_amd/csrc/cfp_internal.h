@@ -48,6 +48,7 @@ struct WsLayout {
   size_t memreg_bytes = 0;
   size_t maps = 0;     // traceback chunk maps uint16 [B][nchunks][K]
   size_t bounds = 0;   // traceback chunk boundary states int32 [B][nchunks]
+  size_t wide = 0;     // chain variant, K > 64: packed tables and cost-row minima
   size_t scan = 0;     // scan variant: start of its private region
   size_t scan_bytes = 0;
   size_t total = 0;
@@ -55,14 +56,19 @@ struct WsLayout {
   int nchunks = 0;
 };
 
-WsLayout layout(int variant, int n, int k, int batch, int n_mem);
+WsLayout layout(int variant, int n, int k, int batch, int n_mem, int n_tables);
 
 // Launchers (return hipSuccess or the launch error).
 hipError_t launch_validate_rtab(const int32_t *rtab, int e, int k, int32_t limit, WsHeader *hdr,
                                 hipStream_t st);
 hipError_t launch_chain_fwd(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *table, int elem,
-                            SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
-                            hipStream_t st);
+                            uint8_t *wide, SearchResult *res, const WsHeader *hdr, int64_t *opt,
+                            int32_t *status, hipStream_t st);
+bool chain_fwd_wide_supported(int k);
+size_t wide_region_bytes(int n, int k, int batch, int n_tables);
+hipError_t launch_chain_fwd_wide(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *region, uint8_t *table,
+                                 SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
+                                 hipStream_t st);
 bool chain_fwd_res_supported(int k, int n_tables);
 hipError_t launch_chain_fwd_res(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *table, SearchResult *res,
                                 const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st);

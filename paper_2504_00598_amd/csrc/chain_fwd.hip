@@ -178,8 +178,8 @@ static void launch_kp(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t
 }
 
 hipError_t launch_chain_fwd(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *table, int elem,
-                            SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
-                            hipStream_t st) {
+                            uint8_t *wide, SearchResult *res, const WsHeader *hdr, int64_t *opt,
+                            int32_t *status, hipStream_t st) {
   (void)elem;
   if (chain_fwd_res_supported(d.k, d.n_tables)) {
     timer_begin(st);
@@ -187,14 +187,12 @@ hipError_t launch_chain_fwd(const cfp_chain_desc &d, const int32_t *redge_dev, u
     timer_end(st);
     return e;
   }
+  if (chain_fwd_wide_supported(d.k)) return launch_chain_fwd_wide(d, redge_dev, wide, table, res, hdr, opt, status, st);
   const int k = d.k;
   timer_begin(st);
   if (k <= 16) launch_kp<16>(d, redge_dev, table, res, hdr, opt, status, st);
   else if (k <= 32) launch_kp<32>(d, redge_dev, table, res, hdr, opt, status, st);
-  else if (k <= 64) launch_kp<64>(d, redge_dev, table, res, hdr, opt, status, st);
-  else if (k <= 128) launch_kp<128>(d, redge_dev, table, res, hdr, opt, status, st);
-  else if (k <= 256) launch_kp<256>(d, redge_dev, table, res, hdr, opt, status, st);
-  else launch_kp<512>(d, redge_dev, table, res, hdr, opt, status, st);
+  else launch_kp<64>(d, redge_dev, table, res, hdr, opt, status, st);
   timer_end(st);
   return hipGetLastError();
 }
