@@ -34,6 +34,18 @@ namespace cfp {
 
 constexpr int kWideThreads = 512;
 
+// Minimum over the 64 lanes of a wave, returned to every lane: DPP within
+// rows of 16, then the four row results through scalar registers.
+__device__ __forceinline__ uint32_t wave_min_fast(uint32_t x) {
+  x = umin(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0xB1, 0xF, 0xF, true));   // quad_perm [1,0,3,2]
+  x = umin(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x4E, 0xF, 0xF, true));   // quad_perm [2,3,0,1]
+  x = umin(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x141, 0xF, 0xF, true));  // row_half_mirror
+  x = umin(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x140, 0xF, 0xF, true));  // row_mirror
+  const uint32_t r0 = __builtin_amdgcn_readlane(x, 0), r1 = __builtin_amdgcn_readlane(x, 16);
+  const uint32_t r2 = __builtin_amdgcn_readlane(x, 32), r3 = __builtin_amdgcn_readlane(x, 48);
+  return umin(umin(r0, r1), umin(r2, r3));
+}
+
 template <int KP>
 struct WideShape {
   static constexpr int SQ = KP / 4;                // threads per table row (4 states each)
@@ -120,7 +132,7 @@ __global__ __launch_bounds__(kWideThreads, 1) void chain_fwd_wide_kernel(
     const int32_t c0 = avail(load_cost(0));
     const uint32_t q = c0 == CFP_COST_INF ? CAP : umin((uint32_t)c0 - (uint32_t)cmin, CAP);
     Qs[0][s] = q << LB;
-    const uint32_t m = wave_min(q);
+    const uint32_t m = wave_min_fast(q);
     if (lane == 0) wq[0][wid] = m;
   }
   __syncthreads();
@@ -138,6 +150,7 @@ __global__ __launch_bounds__(kWideThreads, 1) void chain_fwd_wide_kernel(
 #pragma unroll
     for (int c = 0; c < PF; ++c) load_chunk(1, c, ring[c]);
   }
+  int32_t cm_next = cmb[N > 1 ? 1 : 0];  // cmin of the next row, one step ahead
 
   for (int i = 1; i < N; ++i) {
     const int cur = (i - 1) & 1, nxt = i & 1;
@@ -175,7 +188,8 @@ __global__ __launch_bounds__(kWideThreads, 1) void chain_fwd_wide_kernel(
     uint32_t d = wq[cur][0];
 #pragma unroll
     for (int w = 1; w < CW; ++w) d = umin(d, wq[cur][w]);
-    const int32_t cm = cmb[i];
+    const int32_t cm = cm_next;
+    cm_next = cmb[i + 1 < N ? i + 1 : i];
     o += (int64_t)d + cm;
     infeasible |= cm == CFP_COST_INF;
     // used here by every thread, so the cost load cannot be sunk into the
@@ -203,7 +217,7 @@ __global__ __launch_bounds__(kWideThreads, 1) void chain_fwd_wide_kernel(
       const uint32_t v = (best >> LB) - d;  // >= 0: every candidate is >= the least Q
       const uint32_t q = ccur == CFP_COST_INF ? CAP : umin(v + ((uint32_t)ccur - (uint32_t)cm), CAP);
       Qs[nxt][s] = q << LB;
-      const uint32_t m = wave_min(q);
+      const uint32_t m = wave_min_fast(q);
       if (lane == 0) wq[nxt][wid] = m;
     }
     __syncthreads();
