@@ -164,13 +164,38 @@ static void chain_mem_one(int N, int K, const int32_t *c, const int32_t *rtab, c
 #undef DIDX
 }
 
+/* Budget frontier of one search: F[m] = least cost of a plan whose memory
+ * total is at most m, for every m in [0, M) (Sec. 4.4 with Eq. M as the
+ * constraint, every budget at once).  With D[i][s][m] meaning "total memory
+ * at most m", F[m] = min_s D[N-1][s][m].  D is [N][K][M]. */
+static void mem_frontier_one(int N, int K, const int32_t *c, const int32_t *rtab, const int32_t *redge,
+                             const uint8_t *mem, int M, int64_t *D, int64_t *F) {
+  int64_t opt;
+  int32_t status;
+  int32_t *plan = (int32_t *)malloc(sizeof(int32_t) * (size_t)N);
+  if (!plan) {
+    for (int m = 0; m < M; ++m) F[m] = -1;
+    return;
+  }
+  chain_mem_one(N, K, c, rtab, redge, mem, M - 1, D, &opt, plan, &status);
+  free(plan);
+  for (int m = 0; m < M; ++m) {
+    int64_t best = ORC_INF;
+    for (int s = 0; s < K; ++s) {
+      const int64_t v = D[((size_t)(N - 1) * K + s) * M + m];
+      if (v < best) best = v;
+    }
+    F[m] = best;
+  }
+}
+
 /* ------------------------------------------------------------ threading -- */
 
 typedef struct {
-  int N, K, B, variant;
+  int N, K, B, variant, M;
   const int32_t *cost, *rtab, *redge, *budget;
   const uint8_t *mem;
-  int64_t *opt;
+  int64_t *opt, *frontier;
   int32_t *plan, *status;
   int next; /* next search to take, guarded by lock */
   int failed;
@@ -188,6 +213,7 @@ static void *worker(void *arg) {
     if (b >= j->B) break;
     size_t need = (size_t)j->N * j->K;
     if (j->variant == 1) need *= (size_t)j->budget[b] + 1;
+    if (j->variant == 2) need *= (size_t)j->M;
     if (need > cap) {
       free(D);
       D = (int64_t *)malloc(need * sizeof(int64_t));
@@ -198,6 +224,9 @@ static void *worker(void *arg) {
     int32_t *plan = j->plan + (size_t)b * j->N;
     if (j->variant == 0)
       chain_one(j->N, j->K, c, j->rtab, j->redge, D, &j->opt[b], plan, &j->status[b]);
+    else if (j->variant == 2)
+      mem_frontier_one(j->N, j->K, c, j->rtab, j->redge, j->mem + (size_t)b * j->N * j->K, j->M, D,
+                       j->frontier + (size_t)b * j->M);
     else
       chain_mem_one(j->N, j->K, c, j->rtab, j->redge, j->mem + (size_t)b * j->N * j->K, j->budget[b], D,
                     &j->opt[b], plan, &j->status[b]);
@@ -253,6 +282,21 @@ int oracle_chain_mem(int N, int K, int B, int E, const int32_t *cost, const int3
   j.N = N; j.K = K; j.B = B; j.variant = 1;
   j.cost = cost; j.rtab = rtab; j.redge = redge; j.mem = mem; j.budget = budget;
   j.opt = opt; j.plan = plan; j.status = status;
+  return run(&j, nthreads);
+}
+
+/* Budget frontier of B searches: frontier [B][M] int64, entry m = least cost
+ * with memory total <= m (INT64_MAX where no plan fits). */
+int oracle_mem_frontier(int N, int K, int B, int E, const int32_t *cost, const int32_t *rtab,
+                        const int32_t *redge, const uint8_t *mem, int M, int64_t *frontier, int nthreads) {
+  if (N < 1 || K < 1 || B < 1 || E < 1 || M < 1) return -1;
+  for (int i = 1; i < N; ++i)
+    if (redge[i] < 0 || redge[i] >= E) return -1;
+  job_t j;
+  memset(&j, 0, sizeof j);
+  j.N = N; j.K = K; j.B = B; j.variant = 2; j.M = M;
+  j.cost = cost; j.rtab = rtab; j.redge = redge; j.mem = mem;
+  j.frontier = frontier;
   return run(&j, nthreads);
 }
 

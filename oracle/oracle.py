@@ -48,6 +48,8 @@ def lib():
         L.oracle_chain.restype = i
         L.oracle_chain_mem.argtypes = [i, i, i, i, P, P, P, P, P, P, P, P, i]
         L.oracle_chain_mem.restype = i
+        L.oracle_mem_frontier.argtypes = [i, i, i, i, P, P, P, P, i, P, i]
+        L.oracle_mem_frontier.restype = i
         L.oracle_chain_values.argtypes = [i, i, i, P, P, P, P]
         L.oracle_chain_values.restype = i
         L.oracle_plan_cost.argtypes = [i, i, P, P, P, P]
@@ -119,6 +121,28 @@ def chain_mem(cost, rtab, redge, mem, budget, nthreads: int | None = None):
     if single:
         return opt[0], plan[0], status[0]
     return opt, plan, status
+
+
+def mem_frontier(cost, rtab, redge, mem, n_mem: int, nthreads: int | None = None):
+    """Budget frontier [B][n_mem] int64: entry m is the least cost of a plan
+    whose memory total is at most m (INF64 where none fits)."""
+    cost = _c(cost, np.int32)
+    single = cost.ndim == 2
+    if single:
+        cost = cost[None]
+        mem = np.asarray(mem)[None]
+    B, N, K = cost.shape
+    rtab = _c(rtab, np.int32)
+    redge = _c(redge, np.int32)
+    mem = _c(mem, np.uint8)
+    E = rtab.shape[0]
+    assert mem.shape == (B, N, K)
+    out = np.empty((B, n_mem), np.int64)
+    rc = lib().oracle_mem_frontier(N, K, B, E, _ptr(cost), _ptr(rtab), _ptr(redge), _ptr(mem), int(n_mem),
+                                   _ptr(out), nthreads or default_threads())
+    if rc != 0 or (out < 0).any():
+        raise ValueError("oracle_mem_frontier rejected its arguments or ran out of memory")
+    return out[0] if single else out
 
 
 def chain_values(cost, rtab, redge):

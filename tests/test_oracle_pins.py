@@ -322,3 +322,50 @@ def test_chain_values_last_row_min_is_opt():
     opt, _, _ = O.chain(cost, rtab, redge)
     assert D[-1].min() == opt
     assert (D[0] == cost[0]).all()
+
+
+# ------------------------------------------------ budget frontier (f2) ----
+
+@pytest.mark.parametrize("N,K", [(1, 3), (2, 2), (3, 3), (4, 3), (5, 2)])
+def test_mem_frontier_vs_brute(N, K):
+    """Every entry of the frontier is the least Eq. T cost over the plans
+    whose Eq. M total is at most m (Sec. 4.4), enumerated directly."""
+    rs = np.random.default_rng(rng_seed + 40 + N * 7 + K)
+    for trial in range(4):
+        vals = 3 if trial % 2 else 50
+        cost = rs.integers(0, vals, size=(N, K)).astype(np.int32)
+        if trial == 3:
+            cost[rs.integers(0, N), rs.integers(0, K)] = brute.COST_INF
+        rtab = rs.integers(0, vals, size=(2, K, K)).astype(np.int32)
+        redge = rs.integers(0, 2, size=N).astype(np.int32)
+        mem = rs.integers(0, 4, size=(N, K)).astype(np.uint8)
+        M = int(mem.max(axis=1).sum()) + 2
+        F = O.mem_frontier(cost, rtab, redge, mem, M)
+        plans = brute.all_plans(N, K)
+        T = brute.eq_T(cost, rtab, redge, plans)
+        Mp = brute.eq_M(mem, plans)
+        for m in range(M):
+            fit = T[Mp <= m]
+            want = int(fit.min()) if fit.size else brute.INF64
+            assert F[m] == want, (trial, m)
+
+
+def test_mem_frontier_matches_single_budget_searches():
+    rs = np.random.default_rng(rng_seed + 41)
+    B, N, K = 3, 18, 5
+    cost = rs.integers(0, 1000, size=(B, N, K)).astype(np.int32)
+    rtab = rs.integers(0, 1000, size=(3, K, K)).astype(np.int32)
+    redge = rs.integers(0, 3, size=N).astype(np.int32)
+    mem = rs.integers(0, 6, size=(B, N, K)).astype(np.uint8)
+    M = 70
+    F = O.mem_frontier(cost, rtab, redge, mem, M)
+    for b in range(B):
+        prev = brute.INF64
+        for m in range(M):
+            o, p, st = O.chain_mem(cost[b], rtab, redge, mem[b], m)
+            assert F[b, m] == o
+            assert F[b, m] <= prev  # more memory never costs more
+            prev = F[b, m]
+        # with room for every plan the frontier ends at the unconstrained optimum
+        if int(mem[b].max(axis=1).sum()) < M:
+            assert F[b, -1] == O.chain(cost[b], rtab, redge)[0]
