@@ -139,9 +139,11 @@ def cpu_baseline(cfg, data, budget_s: float = 10.0) -> dict:
 
 
 class Runner:
-    """Device buffers and the two calls of one search pass."""
+    """Device buffers and the two calls of one search pass.  With frontier=True
+    (memory workload) the forward pass is the budget frontier: the least cost
+    at every budget 0 .. M-1, and the traceback returns the plans at M-1."""
 
-    def __init__(self, cfg, data):
+    def __init__(self, cfg, data, frontier: bool = False):
         import torch
 
         from paper_2504_00598_amd import _lib as L
@@ -161,11 +163,19 @@ class Runner:
         self.status = torch.empty(cfg.B, dtype=torch.int32, device="cuda")
         self.plan = torch.empty((cfg.B, cfg.N), dtype=torch.int32, device="cuda")
         self.stream = torch.cuda.current_stream()
+        self.frontier = None
+        if frontier:
+            if cfg.form != "mem":
+                raise ValueError("the budget frontier needs the memory workload")
+            self.frontier = torch.empty((cfg.B, cfg.M), dtype=torch.int64, device="cuda")
 
     def forward(self):
         L = self.L
         if self.variant == L.CFP_V_CHAIN:
             L.cfp_dp_chain(self.desc, ws=self.ws, opt=self.opt, status=self.status, stream=self.stream)
+        elif self.frontier is not None:
+            L.cfp_mem_frontier(self.desc, self.mem, self.n_mem, ws=self.ws, frontier=self.frontier,
+                               status=self.status, stream=self.stream)
         elif self.variant == L.CFP_V_MEM:
             L.cfp_dp_chain_mem(self.desc, self.mem, self.n_mem, self.budget, ws=self.ws, opt=self.opt,
                                status=self.status, stream=self.stream)
@@ -251,6 +261,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default=DEFAULT_CONFIG)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--frontier", action="store_true",
+                    help="memory workload only: time the budget frontier (every budget 0..M-1 in one pass)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 512 MiB device-to-device copy (reference for the HBM byte counters)")
     args = ap.parse_args()
@@ -267,7 +279,9 @@ def main() -> int:
 
     cfg = configs.BY_NAME[args.config]
     data = configs.make(cfg)
-    r = Runner(cfg, data)
+    if args.frontier:
+        data = dict(data, budget=np.full(cfg.B, cfg.M - 1, np.int32))  # the pass covers every budget
+    r = Runner(cfg, data, frontier=args.frontier)
     for _ in range(args.warmup):
         r.forward()
         r.traceback()
@@ -304,12 +318,19 @@ def main() -> int:
     fwd_cells_s = work / (fwd_ms * 1e-3)
 
     o_opt, o_plan, o_st = run_oracle(cfg, data)
-    parity = bool(np.array_equal(r.opt.cpu().numpy(), o_opt) and np.array_equal(r.plan.cpu().numpy(), o_plan)
+    g_opt = r.frontier[:, -1].cpu().numpy() if args.frontier else r.opt.cpu().numpy()
+    parity = bool(np.array_equal(g_opt, o_opt) and np.array_equal(r.plan.cpu().numpy(), o_plan)
                   and np.array_equal(r.status.cpu().numpy(), o_st))
+    if args.frontier:
+        from oracle import oracle as O
+
+        parity = parity and bool(np.array_equal(
+            r.frontier.cpu().numpy(),
+            O.mem_frontier(data["cost"], data["rtab"], data["redge"], data["mem"], cfg.M, nthreads=oracle_threads())))
 
     wl = {"workload": cfg.name, "blocks": cfg.N, "strategies": cfg.K, "searches": cfg.B, "resharding_tables": 12}
     if cfg.form == "mem":
-        wl.update({"memory_buckets": cfg.M, "budgets": "1023-32b"})
+        wl.update({"memory_buckets": cfg.M, "budgets": "every budget 0..M-1" if args.frontier else "1023-32b"})
     out = {
         "metric": METRIC,
         "value": value,

@@ -135,6 +135,25 @@ int cfp_dp_chain(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t *op
 int cfp_dp_chain_mem(const cfp_chain_desc *d, const uint8_t *mem, int32_t n_mem, const int32_t *budget,
                      void *ws, size_t ws_bytes, int64_t *opt, int32_t *status, void *stream);
 
+/* Budget frontier: the least cost at every memory budget, from one pass
+ * (Sec. 4.4 with Eq. M as the constraint).  D[i][s][m] is the least cost of a
+ * prefix ending in s with memory total at most m, so one pass at the largest
+ * budget M-1 holds every budget's answer in its last row:
+ *     frontier[b][m] = min_s D[N-1][s][m],   m = 0 .. M-1
+ * (INT64_MAX where no plan fits within m).  The frontier does not increase
+ * with m; its last entry equals cfp_dp_chain_mem at budget M-1, and
+ * cfp_traceback(d, CFP_V_MEM, n_mem, ...) on the same workspace returns the
+ * plans at budget M-1.
+ *   mem, n_mem  as for cfp_dp_chain_mem (K <= 32, n_tables <= 12)
+ *   frontier    device [B][n_mem] int64
+ *   status      device [B] int32: CFP_ST_OK, CFP_ST_INFEASIBLE when no plan
+ *               fits even M-1 buckets (frontier all INT64_MAX), or an error
+ *               status, in which case the frontier of that search is not
+ *               meaningful.
+ * ws must hold cfp_workspace_bytes(d, CFP_V_MEM, n_mem) bytes. */
+int cfp_mem_frontier(const cfp_chain_desc *d, const uint8_t *mem, int32_t n_mem, void *ws, size_t ws_bytes,
+                     int64_t *frontier, int32_t *status, void *stream);
+
 /* The same optimum as cfp_dp_chain computed as a min-plus parallel scan:
  * block i becomes the transfer matrix T_i[t][s] = R_{e(i)}[t][s] + c[i][s]
  * (T_0[t][s] = c[0][s]), the matrices are composed by a tree of min-plus

@@ -7,5 +7,6 @@ CFP (arXiv 2504.00598, Sec. 4.4) behind the C ABI of include/cfp.h.
 """
 from . import _lib  # noqa: F401
 from ._lib import (CFP_COST_INF, CFP_ST_BADINPUT, CFP_ST_INFEASIBLE, CFP_ST_OK, CFP_V_CHAIN, CFP_V_MEM,  # noqa: F401
-                   CFP_V_SCAN, CfpError, Desc, cfp_dp_chain, cfp_dp_chain_mem, cfp_minplus_scan, cfp_r_limit,
+                   CFP_V_SCAN, CfpError, Desc, cfp_dp_chain, cfp_dp_chain_mem, cfp_mem_frontier, cfp_minplus_scan,
+                   cfp_r_limit,
                    cfp_traceback, cfp_workspace_bytes, status_string)

@@ -33,8 +33,8 @@ CFP_V_SCAN = 2
 CFP_COST_INF = 0x7FFFFFFF
 CFP_MAX_K = 512
 
-EXPORTED = ("cfp_r_limit", "cfp_workspace_bytes", "cfp_dp_chain", "cfp_dp_chain_mem", "cfp_minplus_scan",
-            "cfp_traceback", "cfp_status_string", "cfp_timer_start", "cfp_timer_stop")
+EXPORTED = ("cfp_r_limit", "cfp_workspace_bytes", "cfp_dp_chain", "cfp_dp_chain_mem", "cfp_mem_frontier",
+            "cfp_minplus_scan", "cfp_traceback", "cfp_status_string", "cfp_timer_start", "cfp_timer_stop")
 
 
 class CfpError(RuntimeError):
@@ -75,6 +75,8 @@ def lib() -> ctypes.CDLL:
         L.cfp_dp_chain.restype = ctypes.c_int
         L.cfp_dp_chain_mem.argtypes = [D, P, I32, P, P, ctypes.c_size_t, P, P, P]
         L.cfp_dp_chain_mem.restype = ctypes.c_int
+        L.cfp_mem_frontier.argtypes = [D, P, I32, P, ctypes.c_size_t, P, P, P]
+        L.cfp_mem_frontier.restype = ctypes.c_int
         L.cfp_minplus_scan.argtypes = [D, P, ctypes.c_size_t, P, P, P]
         L.cfp_minplus_scan.restype = ctypes.c_int
         L.cfp_traceback.argtypes = [D, I32, I32, P, ctypes.c_size_t, P, P]
@@ -206,6 +208,28 @@ def cfp_dp_chain_mem(desc: Desc, mem, n_mem: int, budget, ws=None, opt=None, sta
     _check("cfp_dp_chain_mem", lib().cfp_dp_chain_mem(desc.ref, _ptr(mem), int(n_mem), _ptr(budget), _ptr(ws),
                                                       ws.numel(), _ptr(opt), _ptr(status), _stream(stream)))
     return opt, status, ws
+
+
+def cfp_mem_frontier(desc: Desc, mem, n_mem: int, ws=None, frontier=None, status=None, stream=None):
+    """Enqueue the budget-frontier search.  mem [B][N][K] uint8 is a device
+    tensor.  Returns (frontier [B][n_mem] int64, status, ws)."""
+    import torch
+
+    if mem.dtype != torch.uint8 or not mem.is_cuda:
+        raise TypeError("mem must be a uint8 device tensor")
+    if tuple(mem.shape) != (desc.B, desc.N, desc.K):
+        raise ValueError("mem is [B][N][K]")
+    mem = mem.contiguous()
+    dev = desc.cost.device
+    need = cfp_workspace_bytes(desc, CFP_V_MEM, n_mem)
+    ws = _alloc(need, dev) if ws is None else ws
+    frontier = torch.empty((desc.B, int(n_mem)), dtype=torch.int64, device=dev) if frontier is None else frontier
+    status = torch.empty(desc.B, dtype=torch.int32, device=dev) if status is None else status
+    if tuple(frontier.shape) != (desc.B, int(n_mem)) or frontier.dtype != torch.int64:
+        raise ValueError("frontier is [B][n_mem] int64")
+    _check("cfp_mem_frontier", lib().cfp_mem_frontier(desc.ref, _ptr(mem), int(n_mem), _ptr(ws), ws.numel(),
+                                                      _ptr(frontier), _ptr(status), _stream(stream)))
+    return frontier, status, ws
 
 
 def cfp_minplus_scan(desc: Desc, ws=None, opt=None, status=None, stream=None):

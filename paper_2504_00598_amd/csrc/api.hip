@@ -29,6 +29,10 @@ WsLayout layout(int variant, int n, int k, int batch, int n_mem, int n_tables) {
     L.memreg = off;
     L.memreg_bytes = mem_region_bytes(n, k, batch, n_mem);
     off = align_up(off + L.memreg_bytes);
+    L.fbudget = off;
+    off = align_up(off + (size_t)batch * 4);
+    L.fopt = off;
+    off = align_up(off + (size_t)batch * 8);
   } else {
     off = align_up(off + cells * L.elem);
   }
@@ -179,7 +183,31 @@ int cfp_dp_chain_mem(const cfp_chain_desc *d, const uint8_t *mem, int32_t n_mem,
   if (launch_validate_rtab(d->rtab, d->n_tables, d->k, cfp_r_limit(CFP_V_MEM, d->k), hdr, st) != hipSuccess)
     return CFP_ERR_HIP;
   if (launch_chain_mem_fwd(*d, mem, n_mem, budget, (const int32_t *)(w + L.redge), w + L.table, w + L.mem,
-                           w + L.memreg, (SearchResult *)(w + L.result), hdr, opt, status, st) != hipSuccess)
+                           w + L.memreg, (SearchResult *)(w + L.result), hdr, opt, status, nullptr, st) != hipSuccess)
+    return CFP_ERR_HIP;
+  return CFP_OK;
+}
+
+int cfp_mem_frontier(const cfp_chain_desc *d, const uint8_t *mem, int32_t n_mem, void *ws, size_t ws_bytes,
+                     int64_t *frontier, int32_t *status, void *stream) {
+  int rc = check_desc(d);
+  if (rc != CFP_OK) return rc;
+  if (!mem || !frontier || !status) return CFP_ERR_ARG;
+  if (n_mem < 1) return CFP_ERR_ARG;
+  if (n_mem > 4096 || !chain_mem_supported(d->k, d->n_tables)) return CFP_ERR_UNSUPPORTED;
+  WsLayout L = layout(CFP_V_MEM, d->n_blocks, d->k, d->batch, n_mem, d->n_tables);
+  if (!ws || ws_bytes < L.total) return CFP_ERR_WORKSPACE;
+  hipStream_t st = (hipStream_t)stream;
+  uint8_t *w = (uint8_t *)ws;
+  if ((rc = upload_header(d, CFP_V_MEM, n_mem, L, ws, st)) != CFP_OK) return rc;
+  WsHeader *hdr = (WsHeader *)w;
+  int32_t *budget = (int32_t *)(w + L.fbudget);
+  if (launch_fill_i32(budget, d->batch, n_mem - 1, st) != hipSuccess) return CFP_ERR_HIP;
+  if (launch_validate_rtab(d->rtab, d->n_tables, d->k, cfp_r_limit(CFP_V_MEM, d->k), hdr, st) != hipSuccess)
+    return CFP_ERR_HIP;
+  if (launch_chain_mem_fwd(*d, mem, n_mem, budget, (const int32_t *)(w + L.redge), w + L.table, w + L.mem,
+                           w + L.memreg, (SearchResult *)(w + L.result), hdr, (int64_t *)(w + L.fopt), status,
+                           frontier, st) != hipSuccess)
     return CFP_ERR_HIP;
   return CFP_OK;
 }

@@ -46,6 +46,8 @@ struct WsLayout {
   size_t mem = 0;      // memory variant: copy of mem [B][N][K]
   size_t memreg = 0;   // memory variant: state order, packed tables, chunk flags and halo ring
   size_t memreg_bytes = 0;
+  size_t fbudget = 0;  // memory variant: budgets [B] i32 and optima [B] i64 of a frontier call
+  size_t fopt = 0;
   size_t maps = 0;     // traceback chunk maps uint16 [B][nchunks][K]
   size_t bounds = 0;   // traceback chunk boundary states int32 [B][nchunks]
   size_t wide = 0;     // chain variant, K > 64: packed tables and cost-row minima
@@ -80,7 +82,8 @@ size_t mem_region_bytes(int n, int k, int batch, int n_mem);
 hipError_t launch_chain_mem_fwd(const cfp_chain_desc &d, const uint8_t *mem, int n_mem, const int32_t *budget,
                                 const int32_t *redge_dev, uint8_t *table, uint8_t *mem_copy, uint8_t *region,
                                 SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
-                                hipStream_t st);
+                                int64_t *frontier, hipStream_t st);
+hipError_t launch_fill_i32(int32_t *p, int n, int32_t v, hipStream_t st);
 hipError_t launch_traceback_chain(int n, int k, int batch, int elem, const uint8_t *table,
                                   const SearchResult *res, uint16_t *maps, int32_t *bounds, int nchunks,
                                   int32_t *plan, hipStream_t st);

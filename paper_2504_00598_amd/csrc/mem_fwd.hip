@@ -107,7 +107,8 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
                                                            const uint2 *__restrict__ srec, const uint32_t *__restrict__ rpT,
                                                            int N, int K, int M, int B, MemWs w, uint8_t *__restrict__ table,
                                                            SearchResult *__restrict__ res, const WsHeader *__restrict__ hdr,
-                                                           int64_t *__restrict__ opt, int32_t *__restrict__ status) {
+                                                           int64_t *__restrict__ opt, int32_t *__restrict__ status,
+                                                           int64_t *__restrict__ frontier) {
   constexpr int BITS = Pow2Bits<KP>::value;
   constexpr uint32_t CAP = (1u << (32 - BITS)) - 1u;
   constexpr int NW = kMemThreads / 64;       // waves per workgroup
@@ -128,6 +129,7 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
   const int Bb = budget[b];
   const int mf = w.mflags[b];  // written by the prep kernel earlier in the stream
   if (mf & MEMF_BAD) {
+    if (frontier && tid < C && m0 + tid < M) frontier[(size_t)b * M + m0 + tid] = INT64_MAX;
     if (j == 0 && tid == 0) {
       status[b] = CFP_ST_BADINPUT;
       opt[b] = INT64_MAX;
@@ -285,6 +287,11 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
     }
     finish_step(i);
   }
+
+  // Budget frontier: the exact offset of column m is min_s D[N-1][s][m], the
+  // least cost with memory total at most m.
+  if (frontier && wid == 0 && m < M)
+    frontier[(size_t)b * M + m] = (active && off[H + lane] < kOffInf) ? off[H + lane] : INT64_MAX;
 
   // The chunk holding the budget bucket reports the search.
   if (abort_flag) flags |= MEMF_TIMEOUT;
@@ -456,7 +463,8 @@ __global__ void mem_init_kernel(int32_t *mflags, int nb, int32_t *pub, int np) {
 template <int KP>
 static void launch_mem(const cfp_chain_desc &d, const uint8_t *mem, int n_mem, const int32_t *budget,
                        const int32_t *redge_dev, uint8_t *table, uint8_t *mem_copy, uint8_t *region,
-                       SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st) {
+                       SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status, int64_t *frontier,
+                       hipStream_t st) {
   const int N = d.n_blocks, K = d.k, B = d.batch, E = d.n_tables;
   MemWs w = carve(region, N, K, B, n_mem);
   hipLaunchKernelGGL(mem_init_kernel, dim3(64), dim3(256), 0, st, w.mflags, B, w.pub, B * w.nchunk);
@@ -465,7 +473,7 @@ static void launch_mem(const cfp_chain_desc &d, const uint8_t *mem, int n_mem, c
                      w.srec, mem_copy, w.mflags);
   timer_begin(st);
   hipLaunchKernelGGL(mem_fwd_kernel<KP>, dim3(B * w.nchunk), dim3(kMemThreads), 0, st, redge_dev, budget, w.srec, w.rpT, N, K,
-                     n_mem, B, w, table, res, hdr, opt, status);
+                     n_mem, B, w, table, res, hdr, opt, status, frontier);
   timer_end(st);
 }
 
@@ -473,11 +481,21 @@ bool chain_mem_supported(int k, int n_tables) { return k <= 32 && n_tables <= 12
 
 hipError_t launch_chain_mem_fwd(const cfp_chain_desc &d, const uint8_t *mem, int n_mem, const int32_t *budget,
                                 const int32_t *redge_dev, uint8_t *table, uint8_t *mem_copy, uint8_t *region,
-                                SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st) {
+                                SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
+                                int64_t *frontier, hipStream_t st) {
   if (d.k <= 16)
-    launch_mem<16>(d, mem, n_mem, budget, redge_dev, table, mem_copy, region, res, hdr, opt, status, st);
+    launch_mem<16>(d, mem, n_mem, budget, redge_dev, table, mem_copy, region, res, hdr, opt, status, frontier, st);
   else
-    launch_mem<32>(d, mem, n_mem, budget, redge_dev, table, mem_copy, region, res, hdr, opt, status, st);
+    launch_mem<32>(d, mem, n_mem, budget, redge_dev, table, mem_copy, region, res, hdr, opt, status, frontier, st);
+  return hipGetLastError();
+}
+
+__global__ void fill_i32_kernel(int32_t *p, int n, int32_t v) {
+  for (int x = blockIdx.x * blockDim.x + threadIdx.x; x < n; x += gridDim.x * blockDim.x) p[x] = v;
+}
+
+hipError_t launch_fill_i32(int32_t *p, int n, int32_t v, hipStream_t st) {
+  hipLaunchKernelGGL(fill_i32_kernel, dim3((n + 255) / 256 < 64 ? (n + 255) / 256 : 64), dim3(256), 0, st, p, n, v);
   return hipGetLastError();
 }
 

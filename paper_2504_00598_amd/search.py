@@ -30,6 +30,15 @@ def dp_chain_mem(cost, rtab, redge, mem, n_mem, budget, ws=None, stream=None) ->
     return Result(opt, status, plan, ws)
 
 
+def mem_frontier(cost, rtab, redge, mem, n_mem, ws=None, stream=None):
+    """Least cost at every memory budget 0 .. n_mem-1 (frontier [B][n_mem]
+    int64), the status of each search, and the plans at budget n_mem-1."""
+    d = L.Desc(cost, rtab, redge)
+    frontier, status, ws = L.cfp_mem_frontier(d, mem, n_mem, ws=ws, stream=stream)
+    plan = L.cfp_traceback(d, L.CFP_V_MEM, ws, n_mem=n_mem, stream=stream)
+    return frontier, status, plan, ws
+
+
 def minplus_scan(cost, rtab, redge, ws=None, stream=None) -> Result:
     d = L.Desc(cost, rtab, redge)
     opt, status, ws = L.cfp_minplus_scan(d, ws=ws, stream=stream)

@@ -74,6 +74,29 @@ def assert_mem_parity(cost, rtab, redge, mem, n_mem, budget, label=""):
     return g_opt, g_plan
 
 
+def run_frontier(cost, rtab, redge, mem, n_mem):
+    import torch
+    from paper_2504_00598_amd import search
+    frontier, status, plan, _ = search.mem_frontier(dev(cost), dev(rtab), redge, dev(mem), n_mem)
+    torch.cuda.synchronize()
+    return frontier.cpu().numpy(), status.cpu().numpy(), plan.cpu().numpy()
+
+
+def assert_frontier_parity(cost, rtab, redge, mem, n_mem, label=""):
+    """Frontier, status and the plans at the top budget against the oracle."""
+    cost = np.asarray(cost, np.int32)
+    mem = np.asarray(mem, np.uint8)
+    g_f, g_st, g_plan = run_frontier(cost, rtab, redge, mem, n_mem)
+    o_f = O.mem_frontier(cost, rtab, redge, mem, n_mem, nthreads=oracle_threads())
+    top = np.full(cost.shape[0], n_mem - 1, np.int32)
+    o_opt, o_plan, o_st = O.chain_mem(cost, rtab, redge, mem, top, nthreads=oracle_threads())
+    np.testing.assert_array_equal(g_st, o_st, err_msg=f"status {label}")
+    np.testing.assert_array_equal(g_f, o_f, err_msg=f"frontier {label}")
+    np.testing.assert_array_equal(g_f[:, -1], o_opt, err_msg=f"top budget {label}")
+    np.testing.assert_array_equal(g_plan, o_plan, err_msg=f"plan {label}")
+    return g_f
+
+
 def run_scan(cost, rtab, redge):
     import torch
     from paper_2504_00598_amd import search

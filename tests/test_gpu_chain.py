@@ -105,3 +105,20 @@ def test_repeat_is_bit_identical():
         again = run_chain(d["cost"], d["rtab"], d["redge"])
         for a, b in zip(first, again):
             np.testing.assert_array_equal(a, b)
+
+
+@pytest.mark.parametrize("K", [16, 64, 100, 256])
+def test_periodic_layers(K):
+    """Every layer of 12 blocks repeats the same costs (profiles of one
+    distinct segment reused for every instance, Sec. 4.1): a search space
+    full of equal-cost plans, so the lowest-index rule decides the plan."""
+    need_gpu()
+    rs = np.random.default_rng(30 + K)
+    B, N = 4, 240
+    layer = rs.integers(0, 30, size=(B, 12, K)).astype(np.int32)
+    cost = np.tile(layer, (1, N // 12, 1))
+    rtab = rs.integers(0, 30, size=(12, K, K)).astype(np.int32)
+    rtab[:, np.arange(K), np.arange(K)] = 0
+    redge = (np.arange(N) % 12).astype(np.int32)
+    say("periodic layers", K)
+    assert_chain_parity(cost, rtab, redge, f"periodic K={K}")

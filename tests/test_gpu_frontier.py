@@ -1,0 +1,89 @@
+"""GPU parity of cfp_mem_frontier (least cost at every memory budget from one
+pass) against the oracle's frontier, and of the plans it leaves for the top
+budget against the oracle's search at that budget."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from tests.gpu_util import assert_frontier_parity, need_gpu, run_frontier, say
+from workloads import configs, gen
+
+pytestmark = pytest.mark.gpu
+INF = gen.COST_INF
+INF64 = np.iinfo(np.int64).max
+
+
+def case(seed, B, N, K, E, lo, hi, mhi):
+    rs = np.random.default_rng(seed)
+    cost = rs.integers(lo, hi, size=(B, N, K)).astype(np.int32)
+    rtab = rs.integers(lo, hi, size=(E, K, K)).astype(np.int32)
+    rtab[:, np.arange(K), np.arange(K)] = 0
+    redge = (np.arange(N) % E).astype(np.int32)
+    mem = rs.integers(0, mhi, size=(B, N, K)).astype(np.uint8)
+    return cost, rtab, redge, mem
+
+
+def test_config_full():
+    need_gpu()
+    say("frontier mem_llama_n288_k32")
+    d = configs.make("mem_llama_n288_k32")
+    f = assert_frontier_parity(d["cost"], d["rtab"], d["redge"], d["mem"], d["M"], "mem config")
+    # more memory never costs more, and every configured budget reads off the frontier
+    assert (np.diff(f, axis=1) <= 0).all()
+
+
+@pytest.mark.parametrize("N,K,M", [(1, 5, 10), (3, 4, 1), (2, 3, 7), (13, 16, 64), (40, 32, 65), (70, 20, 130),
+                                   (25, 32, 200), (90, 9, 300)])
+def test_shapes(N, K, M):
+    need_gpu()
+    say("frontier shape", N, K, M)
+    cost, rtab, redge, mem = case([N, K, M, 1], 5, N, K, 12, 10_000, 1_000_000, min(9, M))
+    assert_frontier_parity(cost, rtab, redge, mem, M, f"N={N} K={K} M={M}")
+
+
+@pytest.mark.parametrize("K", [4, 32])
+def test_heavy_ties(K):
+    need_gpu()
+    cost, rtab, redge, mem = case([8, K], 4, 30, K, 3, 0, 3, 3)
+    assert_frontier_parity(cost, rtab, redge, mem, 100, f"ties K={K}")
+
+
+def test_periodic_layers():
+    """Every layer of 12 blocks repeats the same costs and memory (profiles of
+    one distinct segment reused, Sec. 4.1): many plans tie, at every budget."""
+    need_gpu()
+    rs = np.random.default_rng(21)
+    B, N, K, M = 3, 96, 16, 400
+    layer_c = rs.integers(0, 50, size=(B, 12, K)).astype(np.int32)
+    layer_m = rs.integers(0, 5, size=(B, 12, K)).astype(np.uint8)
+    cost = np.tile(layer_c, (1, N // 12, 1))
+    mem = np.tile(layer_m, (1, N // 12, 1))
+    rtab = rs.integers(0, 50, size=(12, K, K)).astype(np.int32)
+    redge = (np.arange(N) % 12).astype(np.int32)
+    assert_frontier_parity(cost, rtab, redge, mem, M, "periodic")
+
+
+def test_large_shifts_and_general_edges():
+    need_gpu()
+    rs = np.random.default_rng(12)
+    B, N, K, E, M = 3, 50, 12, 5, 700
+    cost = rs.integers(0, 10**6, size=(B, N, K)).astype(np.int32)
+    rtab = rs.integers(0, 10**6, size=(E, K, K)).astype(np.int32)
+    redge = rs.integers(0, E, size=N).astype(np.int32)
+    mem = rs.integers(0, 17, size=(B, N, K)).astype(np.uint8)
+    assert_frontier_parity(cost, rtab, redge, mem, M, "shift16")
+
+
+def test_statuses():
+    need_gpu()
+    from paper_2504_00598_amd import CFP_ST_BADINPUT, CFP_ST_INFEASIBLE
+    cost, rtab, redge, mem = case(13, 4, 20, 8, 2, 0, 100, 5)
+    cost[0][cost[0] % 3 == 0] = INF
+    cost[1, 5, :] = INF                         # no plan at any budget
+    mem[2, 3, 2] = 40                           # beyond the largest supported shift
+    f, st, plan = run_frontier(cost, rtab, redge, mem, 64)
+    assert st[1] == CFP_ST_INFEASIBLE and (f[1] == INF64).all() and (plan[1] == -1).all()
+    assert st[2] == CFP_ST_BADINPUT and (f[2] == INF64).all() and (plan[2] == -1).all()
+    good = [0, 3]
+    assert_frontier_parity(cost[good], rtab, redge, mem[good], 64, "inf")

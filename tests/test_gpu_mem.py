@@ -86,3 +86,17 @@ def test_budget_out_of_range_is_bad_input():
     cost, rtab, redge, mem = mem_case(13, 2, 10, 4, 2, 0, 100, 0, 3, 32)
     opt, st, plan = run_mem(cost, rtab, redge, mem, 32, np.array([31, 32], np.int32))
     assert st[0] == 0 and st[1] == CFP_ST_BADINPUT
+
+
+def test_periodic_layers():
+    """Repeated layers (the same costs and memory every 12 blocks): many tied
+    plans at every budget."""
+    need_gpu()
+    rs = np.random.default_rng(31)
+    B, N, K, M = 4, 96, 32, 300
+    cost = np.tile(rs.integers(0, 40, size=(B, 12, K)).astype(np.int32), (1, N // 12, 1))
+    mem = np.tile(rs.integers(0, 5, size=(B, 12, K)).astype(np.uint8), (1, N // 12, 1))
+    rtab = rs.integers(0, 40, size=(12, K, K)).astype(np.int32)
+    redge = (np.arange(N) % 12).astype(np.int32)
+    budget = np.array([60, 120, 200, 299], np.int32)
+    assert_mem_parity(cost, rtab, redge, mem, M, budget, "periodic")
