@@ -145,6 +145,23 @@ def mem_frontier(cost, rtab, redge, mem, n_mem: int, nthreads: int | None = None
     return out[0] if single else out
 
 
+def expand_boundary(rbound, last, first):
+    """Resharding tables of a segment chain written out plan by plan: the
+    cost between plan t of one segment and plan s of the next is the boundary
+    block pair's, R_e[t][s] = rbound[e][last[t]][first[s]] (Sec. 4.2: only
+    the dependent block pairs at segment boundaries are profiled)."""
+    rbound = np.asarray(rbound, np.int64)
+    last = np.asarray(last, np.int64)
+    first = np.asarray(first, np.int64)
+    return np.ascontiguousarray(rbound[:, last[:, None], first[None, :]].astype(np.int32))
+
+
+def segments(cost, rbound, last, first, redge, nthreads: int | None = None):
+    """Segment-level search: the chain search of Eq. T over segments with the
+    boundary-pair resharding tables expanded to K x K."""
+    return chain(cost, expand_boundary(rbound, last, first), redge, nthreads=nthreads)
+
+
 def chain_values(cost, rtab, redge):
     """Forward values D[i][s] (int64) of one chain, cost [N][K]."""
     cost = _c(cost, np.int32)

@@ -369,3 +369,70 @@ def test_mem_frontier_matches_single_budget_searches():
         # with room for every plan the frontier ends at the unconstrained optimum
         if int(mem[b].max(axis=1).sum()) < M:
             assert F[b, -1] == O.chain(cost[b], rtab, redge)[0]
+
+
+# ---------------------------------------- segments with boundary resharding ----
+
+def seg_eq_T(cost, rbound, last, first, redge, plan):
+    """Eq. T of one plan of a segment chain, from its definition: segment
+    costs plus the boundary block pair's resharding at every boundary."""
+    t = 0
+    for i, x in enumerate(plan):
+        if cost[i, x] == brute.COST_INF:
+            return brute.INF64
+        t += int(cost[i, x])
+    for i in range(1, len(plan)):
+        t += int(rbound[redge[i], last[plan[i - 1]], first[plan[i]]])
+    return t
+
+
+def digit_maps(P, S):
+    """Plan t = sum_j x_j S^j of P blocks with S strategies: first block x_0,
+    last block x_{P-1} (the numbering used for segments of P blocks)."""
+    t = np.arange(S ** P)
+    return (t // S ** (P - 1)).astype(np.uint8), (t % S).astype(np.uint8)
+
+
+@pytest.mark.parametrize("N,P,S", [(1, 2, 2), (2, 2, 2), (3, 2, 2), (4, 2, 2), (3, 1, 3), (2, 3, 2)])
+def test_segments_vs_brute(N, P, S):
+    rs = np.random.default_rng(rng_seed + 60 + N * 10 + P * 3 + S)
+    K = S ** P
+    last, first = digit_maps(P, S)
+    for trial in range(4):
+        vals = 3 if trial % 2 else 100
+        cost = rs.integers(0, vals, size=(N, K)).astype(np.int32)
+        if trial == 3:
+            cost[rs.integers(0, N), rs.integers(0, K)] = brute.COST_INF
+        rbound = rs.integers(0, vals, size=(2, S, S)).astype(np.int32)
+        redge = rs.integers(0, 2, size=N).astype(np.int32)
+        opt, plan, st = O.segments(cost, rbound, last, first, redge)
+        plans = brute.all_plans(N, K)
+        T = np.array([seg_eq_T(cost, rbound, last, first, redge, p) for p in plans])
+        best = T.min()
+        assert opt == best
+        assert seg_eq_T(cost, rbound, last, first, redge, plan) == opt
+        ties = plans[T == best]
+        order = np.lexsort([ties[:, i] for i in range(N)])
+        np.testing.assert_array_equal(plan, ties[order[0]])  # lowest index at every choice
+
+
+def test_segments_zero_boundary_is_sum_of_minima():
+    rs = np.random.default_rng(rng_seed + 61)
+    N, K = 12, 81
+    last, first = digit_maps(4, 3)
+    cost = rs.integers(0, 10**6, size=(N, K)).astype(np.int32)
+    rbound = np.zeros((1, 3, 3), np.int32)
+    opt, plan, st = O.segments(cost, rbound, last, first, np.zeros(N, np.int32))
+    assert opt == int(cost.min(axis=1).sum())
+    np.testing.assert_array_equal(plan, cost.argmin(axis=1))
+
+
+def test_expand_boundary_layout():
+    # R[t][s] takes the row from t's last block and the column from s's first block
+    rb = np.arange(2 * 3 * 3, dtype=np.int32).reshape(2, 3, 3)
+    last, first = digit_maps(2, 3)  # t = x0 + 3 x1: last = x1, first = x0
+    R = O.expand_boundary(rb, last, first)
+    for e in range(2):
+        for t in range(9):
+            for s in range(9):
+                assert R[e, t, s] == rb[e, t // 3, s % 3]
