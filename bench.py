@@ -8,8 +8,9 @@ independent searches sharing 12 resharding tables.  Prints one JSON line.
 
     python bench.py [--steps K] [--warmup W] [--config NAME] [--no-cpu]
 
-Other workloads (--config): chain_gpt_n24_k16, mem_llama_n288_k32,
-chain_wide_n512_k256, scan_n4096_k512.
+Other workloads (--config): chain_gpt_n24_k16, mem_llama_n288_k32 (with
+--frontier: every budget in one pass), chain_wide_n512_k256, scan_n4096_k512,
+seg_gpt_n96_k81 (segment-level search with boundary resharding).
 """
 from __future__ import annotations
 
@@ -42,6 +43,7 @@ KERNELS = {
     "mem_llama_n288_k32": ("mem_fwd_kernel<32>", ["mem_fwd.hip", "res_common.h"]),
     "chain_wide_n512_k256": ("chain_fwd_wide_kernel<256>", ["chain_fwd_wide.hip"]),
     "scan_n4096_k512": ("scan_gemm_kernel", ["scan.hip"]),
+    "seg_gpt_n96_k81": ("seg_fwd_kernel<2>", ["seg_fwd.hip"]),
 }
 COMMON_SOURCES = ["common.h", "cfp_internal.h", "../../include/cfp.h"]
 
@@ -112,6 +114,9 @@ def run_oracle(cfg, data, n=None, threads=None):
     if cfg.form == "mem":
         return O.chain_mem(data["cost"][:n], data["rtab"], data["redge"], data["mem"][:n], data["budget"][:n],
                            nthreads=threads)
+    if cfg.form == "seg":
+        return O.segments(data["cost"][:n], data["rbound"], data["last"], data["first"], data["redge"],
+                          nthreads=threads)
     return O.chain(data["cost"][:n], data["rtab"], data["redge"], nthreads=threads)
 
 
@@ -150,6 +155,18 @@ class Runner:
 
         self.L, self.cfg = L, cfg
         self.cost = cost = torch.from_numpy(data["cost"]).cuda()
+        self.stream = torch.cuda.current_stream()
+        self.opt = torch.empty(cfg.B, dtype=torch.int64, device="cuda")
+        self.status = torch.empty(cfg.B, dtype=torch.int32, device="cuda")
+        self.plan = torch.empty((cfg.B, cfg.N), dtype=torch.int32, device="cuda")
+        self.frontier = None
+        if cfg.form == "seg":
+            self.variant = L.CFP_V_SEG
+            self.sdesc = L.SegDesc(cost, torch.from_numpy(data["rbound"]).cuda(),
+                                   torch.from_numpy(data["last"]).cuda(), torch.from_numpy(data["first"]).cuda(),
+                                   data["redge"])
+            self.ws = torch.empty(L.cfp_segment_workspace_bytes(self.sdesc), dtype=torch.uint8, device="cuda")
+            return
         rtab = torch.from_numpy(data["rtab"]).cuda()
         self.desc = L.Desc(cost, rtab, data["redge"])
         self.variant = {"chain": L.CFP_V_CHAIN, "mem": L.CFP_V_MEM, "scan": L.CFP_V_SCAN}[cfg.form]
@@ -159,11 +176,6 @@ class Runner:
             self.budget = torch.from_numpy(data["budget"]).cuda()
         self.ws = torch.empty(L.cfp_workspace_bytes(self.desc, self.variant, self.n_mem), dtype=torch.uint8,
                               device="cuda")
-        self.opt = torch.empty(cfg.B, dtype=torch.int64, device="cuda")
-        self.status = torch.empty(cfg.B, dtype=torch.int32, device="cuda")
-        self.plan = torch.empty((cfg.B, cfg.N), dtype=torch.int32, device="cuda")
-        self.stream = torch.cuda.current_stream()
-        self.frontier = None
         if frontier:
             if cfg.form != "mem":
                 raise ValueError("the budget frontier needs the memory workload")
@@ -171,7 +183,9 @@ class Runner:
 
     def forward(self):
         L = self.L
-        if self.variant == L.CFP_V_CHAIN:
+        if self.variant == L.CFP_V_SEG:
+            L.cfp_dp_segments(self.sdesc, ws=self.ws, opt=self.opt, status=self.status, stream=self.stream)
+        elif self.variant == L.CFP_V_CHAIN:
             L.cfp_dp_chain(self.desc, ws=self.ws, opt=self.opt, status=self.status, stream=self.stream)
         elif self.frontier is not None:
             L.cfp_mem_frontier(self.desc, self.mem, self.n_mem, ws=self.ws, frontier=self.frontier,
@@ -183,6 +197,9 @@ class Runner:
             L.cfp_minplus_scan(self.desc, ws=self.ws, opt=self.opt, status=self.status, stream=self.stream)
 
     def traceback(self):
+        if self.variant == self.L.CFP_V_SEG:
+            self.L.cfp_traceback_segments(self.sdesc, self.ws, plan=self.plan, stream=self.stream)
+            return
         self.L.cfp_traceback(self.desc, self.variant, self.ws, n_mem=self.n_mem, plan=self.plan, stream=self.stream)
 
 
@@ -329,6 +346,9 @@ def main() -> int:
             O.mem_frontier(data["cost"], data["rtab"], data["redge"], data["mem"], cfg.M, nthreads=oracle_threads())))
 
     wl = {"workload": cfg.name, "blocks": cfg.N, "strategies": cfg.K, "searches": cfg.B, "resharding_tables": 12}
+    if cfg.form == "seg":
+        wl = {"workload": cfg.name, "segments": cfg.N, "plans": cfg.K, "searches": cfg.B,
+              "boundary_tables": "2 x 3 x 3", "blocks_per_segment": 4, "strategies_per_block": 3}
     if cfg.form == "mem":
         wl.update({"memory_buckets": cfg.M, "budgets": "every budget 0..M-1" if args.frontier else "1023-32b"})
     out = {
@@ -357,6 +377,9 @@ def main() -> int:
     }
     if cfg.form == "scan":
         out["roofline"]["cells_counted"] = "min-plus matrix-product cells (N-1)*K^3 per search"
+    if cfg.form == "seg":
+        out["roofline"]["cells_counted"] = ("chain-equivalent K^2 per segment step; the factorised step does "
+                                            "K + L*F work, so the fraction is not a VALU utilisation")
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(cfg, data)
     print(json.dumps(out), flush=True)

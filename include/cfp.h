@@ -77,7 +77,7 @@ enum {
 };
 
 /* Forward variants (the argument `variant` of cfp_workspace_bytes / cfp_traceback). */
-enum { CFP_V_CHAIN = 0, CFP_V_MEM = 1, CFP_V_SCAN = 2 };
+enum { CFP_V_CHAIN = 0, CFP_V_MEM = 1, CFP_V_SCAN = 2, CFP_V_SEG = 3 };
 
 /* Largest supported number of strategies per block. */
 #define CFP_MAX_K 512
@@ -96,8 +96,9 @@ typedef struct {
 /* Exclusive upper bound on resharding-table entries for which `variant` with
  * K strategies is exact.  The kernels carry (cost, argmin) packed in one
  * 32-bit word with ceil(log2 K) index bits (at least 4), so the bound depends
- * on K: 2^(30-b) for K <= 64, 2^(32-b) - 1 for K > 64 (chain and scan), and
- * 2^(31-b) for the memory variant, with b = max(4, ceil(log2 K)).  Returns 0
+ * on K: 2^(30-b) for K <= 64, 2^(32-b) - 1 for K > 64 (chain and scan),
+ * 2^(31-b) for the memory variant and 2^(32-b) - 1 for the boundary tables of
+ * the segment search, with b = max(4, ceil(log2 K)).  Returns 0
  * for an unsupported K or variant. */
 int32_t cfp_r_limit(int32_t variant, int32_t k);
 
@@ -176,6 +177,42 @@ int cfp_minplus_scan(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t
  *   plan   device [B][N] int32; all -1 for a search whose status is not OK. */
 int cfp_traceback(const cfp_chain_desc *d, int32_t variant, int32_t n_mem, void *ws, size_t ws_bytes,
                   int32_t *plan, void *stream);
+
+/* Segment-level search (Sec. 4.2-4.4).  The units are model segments; the
+ * plan t of a segment combines the strategies of its blocks (K = prod of the
+ * block strategy counts, e.g. 3^4 = 81 for four blocks of three strategies,
+ * Sec. 6.5).  Resharding between consecutive segments is profiled only for
+ * the boundary block pair (Sec. 4.2), so Eq. T's resharding term is
+ *     R_{e(i)}[t][s] = rbound[e(i)][last[t]][first[s]]
+ * with last[t] the strategy of the last block of plan t and first[s] that of
+ * the first block of plan s.  The result is exactly cfp_dp_chain's on that
+ * expanded table (same optimum, same lowest-index plan), found with O(K + L F)
+ * work per segment instead of O(K^2). */
+typedef struct {
+  int32_t n_segments;    /* N >= 1 */
+  int32_t k;             /* plans per segment, 1 <= K <= CFP_MAX_K */
+  int32_t batch;         /* independent searches B >= 1 */
+  int32_t n_tables;      /* distinct boundary tables E >= 1 */
+  int32_t n_last;        /* L: strategies of a segment's last block, 1..8 */
+  int32_t n_first;       /* F: strategies of a segment's first block, 1..8 */
+  const int32_t *cost;   /* device [B][N][K]; each entry in [0, CFP_COST_INF] */
+  const int32_t *rbound; /* device [E][L][F]; each entry in [0, cfp_r_limit(CFP_V_SEG, K)) */
+  const uint8_t *last;   /* device [K]; each entry < L (else status CFP_ST_BADINPUT) */
+  const uint8_t *first;  /* device [K]; each entry < F (else status CFP_ST_BADINPUT) */
+  const int32_t *redge;  /* HOST [N]; redge[i] in [0, E): table of the boundary (i-1 -> i) */
+} cfp_segment_desc;
+
+/* Workspace bytes of a segment search (0 for an invalid descriptor). */
+size_t cfp_segment_workspace_bytes(const cfp_segment_desc *d);
+
+/* Forward segment search; opt/status as for cfp_dp_chain.  CFP_ERR_UNSUPPORTED
+ * when K > CFP_MAX_K or L or F exceeds 8. */
+int cfp_dp_segments(const cfp_segment_desc *d, void *ws, size_t ws_bytes, int64_t *opt, int32_t *status,
+                    void *stream);
+
+/* Plans [B][N] of a workspace filled by cfp_dp_segments with the same
+ * descriptor (lowest optimal final plan, lowest predecessor at every step). */
+int cfp_traceback_segments(const cfp_segment_desc *d, void *ws, size_t ws_bytes, int32_t *plan, void *stream);
 
 /* Benchmarking aid (not needed for searching).  cfp_timer_start creates
  * max_launches pairs of HIP events (1 <= max_launches <= 2^20) and arms

@@ -7,6 +7,7 @@ CFP (arXiv 2504.00598, Sec. 4.4) behind the C ABI of include/cfp.h.
 """
 from . import _lib  # noqa: F401
 from ._lib import (CFP_COST_INF, CFP_ST_BADINPUT, CFP_ST_INFEASIBLE, CFP_ST_OK, CFP_V_CHAIN, CFP_V_MEM,  # noqa: F401
-                   CFP_V_SCAN, CfpError, Desc, cfp_dp_chain, cfp_dp_chain_mem, cfp_mem_frontier, cfp_minplus_scan,
+                   CFP_V_SCAN, CFP_V_SEG, CfpError, Desc, SegDesc, cfp_dp_chain, cfp_dp_chain_mem, cfp_dp_segments,
+                   cfp_mem_frontier, cfp_minplus_scan, cfp_traceback_segments,
                    cfp_r_limit,
                    cfp_traceback, cfp_workspace_bytes, status_string)

@@ -30,11 +30,13 @@ CFP_ST_BADINPUT = 4
 CFP_V_CHAIN = 0
 CFP_V_MEM = 1
 CFP_V_SCAN = 2
+CFP_V_SEG = 3
 CFP_COST_INF = 0x7FFFFFFF
 CFP_MAX_K = 512
 
 EXPORTED = ("cfp_r_limit", "cfp_workspace_bytes", "cfp_dp_chain", "cfp_dp_chain_mem", "cfp_mem_frontier",
-            "cfp_minplus_scan", "cfp_traceback", "cfp_status_string", "cfp_timer_start", "cfp_timer_stop")
+            "cfp_minplus_scan", "cfp_traceback", "cfp_segment_workspace_bytes", "cfp_dp_segments",
+            "cfp_traceback_segments", "cfp_status_string", "cfp_timer_start", "cfp_timer_stop")
 
 
 class CfpError(RuntimeError):
@@ -51,6 +53,22 @@ class cfp_chain_desc(ctypes.Structure):
         ("n_tables", ctypes.c_int32),
         ("cost", ctypes.c_void_p),
         ("rtab", ctypes.c_void_p),
+        ("redge", ctypes.c_void_p),
+    ]
+
+
+class cfp_segment_desc(ctypes.Structure):
+    _fields_ = [
+        ("n_segments", ctypes.c_int32),
+        ("k", ctypes.c_int32),
+        ("batch", ctypes.c_int32),
+        ("n_tables", ctypes.c_int32),
+        ("n_last", ctypes.c_int32),
+        ("n_first", ctypes.c_int32),
+        ("cost", ctypes.c_void_p),
+        ("rbound", ctypes.c_void_p),
+        ("last", ctypes.c_void_p),
+        ("first", ctypes.c_void_p),
         ("redge", ctypes.c_void_p),
     ]
 
@@ -81,6 +99,13 @@ def lib() -> ctypes.CDLL:
         L.cfp_minplus_scan.restype = ctypes.c_int
         L.cfp_traceback.argtypes = [D, I32, I32, P, ctypes.c_size_t, P, P]
         L.cfp_traceback.restype = ctypes.c_int
+        SD = ctypes.POINTER(cfp_segment_desc)
+        L.cfp_segment_workspace_bytes.argtypes = [SD]
+        L.cfp_segment_workspace_bytes.restype = ctypes.c_size_t
+        L.cfp_dp_segments.argtypes = [SD, P, ctypes.c_size_t, P, P, P]
+        L.cfp_dp_segments.restype = ctypes.c_int
+        L.cfp_traceback_segments.argtypes = [SD, P, ctypes.c_size_t, P, P]
+        L.cfp_traceback_segments.restype = ctypes.c_int
         L.cfp_timer_start.argtypes = [I32]
         L.cfp_timer_start.restype = ctypes.c_int
         L.cfp_timer_stop.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I32)]
@@ -159,6 +184,64 @@ class Desc:
     @property
     def ref(self):
         return ctypes.byref(self.c)
+
+
+class SegDesc:
+    """A cfp_segment_desc plus the objects that keep its memory alive.  cost
+    [B][N][K] int32, rbound [E][L][F] int32, last/first [K] uint8 are device
+    tensors; redge [N] is host data."""
+
+    def __init__(self, cost, rbound, last, first, redge):
+        import torch
+
+        for name, t, dt in (("cost", cost, torch.int32), ("rbound", rbound, torch.int32),
+                            ("last", last, torch.uint8), ("first", first, torch.uint8)):
+            if not isinstance(t, torch.Tensor) or t.dtype != dt or not t.is_cuda or not t.is_contiguous():
+                raise TypeError(f"{name} must be a contiguous {dt} device tensor")
+        if cost.dim() != 3 or rbound.dim() != 3:
+            raise ValueError("cost is [B][N][K] and rbound is [E][L][F]")
+        B, N, K = cost.shape
+        if tuple(last.shape) != (K,) or tuple(first.shape) != (K,):
+            raise ValueError("last and first have K entries")
+        self.redge = np.ascontiguousarray(np.asarray(redge, dtype=np.int32))
+        if self.redge.shape != (N,):
+            raise ValueError("redge must have N entries")
+        self.cost, self.rbound, self.last, self.first = cost, rbound, last, first
+        E, Lc, Fc = rbound.shape
+        self.B, self.N, self.K, self.E, self.L, self.F = int(B), int(N), int(K), int(E), int(Lc), int(Fc)
+        self.c = cfp_segment_desc(self.N, self.K, self.B, self.E, self.L, self.F, _ptr(cost), _ptr(rbound),
+                                  _ptr(last), _ptr(first), self.redge.ctypes.data_as(ctypes.c_void_p).value)
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.c)
+
+
+def cfp_segment_workspace_bytes(desc: SegDesc) -> int:
+    return int(lib().cfp_segment_workspace_bytes(desc.ref))
+
+
+def cfp_dp_segments(desc: SegDesc, ws=None, opt=None, status=None, stream=None):
+    """Enqueue the segment search.  Returns (opt, status, ws)."""
+    import torch
+
+    dev = desc.cost.device
+    ws = _alloc(cfp_segment_workspace_bytes(desc), dev) if ws is None else ws
+    opt = torch.empty(desc.B, dtype=torch.int64, device=dev) if opt is None else opt
+    status = torch.empty(desc.B, dtype=torch.int32, device=dev) if status is None else status
+    _check("cfp_dp_segments", lib().cfp_dp_segments(desc.ref, _ptr(ws), ws.numel(), _ptr(opt), _ptr(status),
+                                                    _stream(stream)))
+    return opt, status, ws
+
+
+def cfp_traceback_segments(desc: SegDesc, ws, plan=None, stream=None):
+    """Enqueue the plan recovery of a segment search.  Returns plan [B][N]."""
+    import torch
+
+    plan = torch.empty((desc.B, desc.N), dtype=torch.int32, device=desc.cost.device) if plan is None else plan
+    _check("cfp_traceback_segments", lib().cfp_traceback_segments(desc.ref, _ptr(ws), ws.numel(), _ptr(plan),
+                                                                  _stream(stream)))
+    return plan
 
 
 def cfp_workspace_bytes(desc: Desc, variant: int, n_mem: int = 0) -> int:

@@ -133,6 +133,8 @@ int32_t cfp_r_limit(int32_t variant, int32_t k) {
       return k <= 64 ? (int32_t)(1u << (30 - b)) : (int32_t)((1u << (32 - b)) - 1u);
     case CFP_V_MEM:
       return k <= 32 ? (int32_t)(1u << (31 - b)) : 0;
+    case CFP_V_SEG:
+      return (int32_t)((1u << (32 - b)) - 1u);
     default:
       return 0;
   }
@@ -290,6 +292,82 @@ int cfp_timer_stop(double *total_ms, int32_t *launches) {
   if (launches) *launches = (int32_t)g_timer_used;
   g_timer_used = 0;
   return rc;
+}
+
+}  // extern "C"
+
+namespace {
+
+bool seg_desc_ok(const cfp_segment_desc *d) {
+  if (!d) return false;
+  if (d->n_segments < 1 || d->k < 1 || d->batch < 1 || d->n_tables < 1) return false;
+  if (!d->cost || !d->rbound || !d->last || !d->first || !d->redge) return false;
+  return true;
+}
+
+int check_seg(const cfp_segment_desc *d) {
+  if (!d) return CFP_ERR_ARG;
+  if (d->k > CFP_MAX_K || d->n_last > 8 || d->n_first > 8) return CFP_ERR_UNSUPPORTED;
+  if (!seg_desc_ok(d) || d->n_last < 1 || d->n_first < 1) return CFP_ERR_ARG;
+  for (int i = 1; i < d->n_segments; ++i)
+    if (d->redge[i] < 0 || d->redge[i] >= d->n_tables) return CFP_ERR_RANGE;
+  return CFP_OK;
+}
+
+// The fields the workspace header and the traceback read, as a chain descriptor.
+cfp_chain_desc as_chain(const cfp_segment_desc *d) {
+  cfp_chain_desc c;
+  c.n_blocks = d->n_segments;
+  c.k = d->k;
+  c.batch = d->batch;
+  c.n_tables = d->n_tables;
+  c.cost = d->cost;
+  c.rtab = d->rbound;
+  c.redge = d->redge;
+  return c;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t cfp_segment_workspace_bytes(const cfp_segment_desc *d) {
+  if (check_seg(d) != CFP_OK) return 0;
+  return layout(CFP_V_SEG, d->n_segments, d->k, d->batch, 0, d->n_tables).total;
+}
+
+int cfp_dp_segments(const cfp_segment_desc *d, void *ws, size_t ws_bytes, int64_t *opt, int32_t *status,
+                    void *stream) {
+  int rc = check_seg(d);
+  if (rc != CFP_OK) return rc;
+  if (!opt || !status) return CFP_ERR_ARG;
+  WsLayout L = layout(CFP_V_SEG, d->n_segments, d->k, d->batch, 0, d->n_tables);
+  if (!ws || ws_bytes < L.total) return CFP_ERR_WORKSPACE;
+  hipStream_t st = (hipStream_t)stream;
+  uint8_t *w = (uint8_t *)ws;
+  const cfp_chain_desc c = as_chain(d);
+  if ((rc = upload_header(&c, CFP_V_SEG, 0, L, ws, st)) != CFP_OK) return rc;
+  WsHeader *hdr = (WsHeader *)w;
+  if (launch_validate_range(d->rbound, (size_t)d->n_tables * d->n_last * d->n_first, cfp_r_limit(CFP_V_SEG, d->k),
+                            hdr, st) != hipSuccess)
+    return CFP_ERR_HIP;
+  if (launch_seg_fwd(*d, (const int32_t *)(w + L.redge), w + L.table, (SearchResult *)(w + L.result), hdr, opt,
+                     status, st) != hipSuccess)
+    return CFP_ERR_HIP;
+  return CFP_OK;
+}
+
+int cfp_traceback_segments(const cfp_segment_desc *d, void *ws, size_t ws_bytes, int32_t *plan, void *stream) {
+  int rc = check_seg(d);
+  if (rc != CFP_OK) return rc;
+  if (!plan) return CFP_ERR_ARG;
+  WsLayout L = layout(CFP_V_SEG, d->n_segments, d->k, d->batch, 0, d->n_tables);
+  if (!ws || ws_bytes < L.total) return CFP_ERR_WORKSPACE;
+  uint8_t *w = (uint8_t *)ws;
+  const hipError_t e = launch_traceback_chain(d->n_segments, d->k, d->batch, L.elem, w + L.table,
+                                              (const SearchResult *)(w + L.result), (uint16_t *)(w + L.maps),
+                                              (int32_t *)(w + L.bounds), L.nchunks, plan, (hipStream_t)stream);
+  return e == hipSuccess ? CFP_OK : CFP_ERR_HIP;
 }
 
 const char *cfp_status_string(int code) {

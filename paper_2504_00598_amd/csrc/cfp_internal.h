@@ -63,6 +63,10 @@ WsLayout layout(int variant, int n, int k, int batch, int n_mem, int n_tables);
 // Launchers (return hipSuccess or the launch error).
 hipError_t launch_validate_rtab(const int32_t *rtab, int e, int k, int32_t limit, WsHeader *hdr,
                                 hipStream_t st);
+hipError_t launch_validate_range(const int32_t *a, size_t count, int32_t limit, WsHeader *hdr, hipStream_t st);
+bool seg_supported(int k, int n_last, int n_first);
+hipError_t launch_seg_fwd(const cfp_segment_desc &d, const int32_t *redge_dev, uint8_t *table, SearchResult *res,
+                          const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st);
 hipError_t launch_chain_fwd(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *table, int elem,
                             uint8_t *wide, SearchResult *res, const WsHeader *hdr, int64_t *opt,
                             int32_t *status, hipStream_t st);

@@ -24,7 +24,10 @@ __global__ void validate_rtab_kernel(const int32_t *__restrict__ rtab, size_t co
 }
 
 hipError_t launch_validate_rtab(const int32_t *rtab, int e, int k, int32_t limit, WsHeader *hdr, hipStream_t st) {
-  size_t count = (size_t)e * k * k;
+  return launch_validate_range(rtab, (size_t)e * k * k, limit, hdr, st);
+}
+
+hipError_t launch_validate_range(const int32_t *rtab, size_t count, int32_t limit, WsHeader *hdr, hipStream_t st) {
   int grid = (int)((count + kThreads - 1) / kThreads);
   if (grid > 1024) grid = 1024;
   hipLaunchKernelGGL(validate_rtab_kernel, dim3(grid), dim3(kThreads), 0, st, rtab, count, limit, hdr);

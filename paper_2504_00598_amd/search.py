@@ -39,6 +39,15 @@ def mem_frontier(cost, rtab, redge, mem, n_mem, ws=None, stream=None):
     return frontier, status, plan, ws
 
 
+def dp_segments(cost, rbound, last, first, redge, ws=None, stream=None) -> Result:
+    """Segment-level search with boundary resharding: cost [B][N][K], rbound
+    [E][L][F], last/first [K] (device tensors), redge [N] (host)."""
+    d = L.SegDesc(cost, rbound, last, first, redge)
+    opt, status, ws = L.cfp_dp_segments(d, ws=ws, stream=stream)
+    plan = L.cfp_traceback_segments(d, ws, stream=stream)
+    return Result(opt, status, plan, ws)
+
+
 def minplus_scan(cost, rtab, redge, ws=None, stream=None) -> Result:
     d = L.Desc(cost, rtab, redge)
     opt, status, ws = L.cfp_minplus_scan(d, ws=ws, stream=stream)

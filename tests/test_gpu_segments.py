@@ -1,0 +1,125 @@
+"""GPU parity of cfp_dp_segments + cfp_traceback_segments (segment-level
+search with boundary-pair resharding) against the oracle: the chain search
+over the expanded K x K tables.  Optimum, status and plan bit for bit."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from tests.gpu_util import dev, need_gpu, oracle_threads, say
+from workloads import configs, gen
+
+pytestmark = pytest.mark.gpu
+INF = gen.COST_INF
+
+
+def run_seg(cost, rbound, last, first, redge):
+    import torch
+    from paper_2504_00598_amd import search
+    res = search.dp_segments(dev(cost), dev(rbound), dev(np.asarray(last, np.uint8)),
+                             dev(np.asarray(first, np.uint8)), redge)
+    torch.cuda.synchronize()
+    return res.opt.cpu().numpy(), res.status.cpu().numpy(), res.plan.cpu().numpy()
+
+
+def assert_seg_parity(cost, rbound, last, first, redge, label=""):
+    cost = np.asarray(cost, np.int32)
+    if cost.ndim == 2:
+        cost = cost[None]
+    g_opt, g_st, g_plan = run_seg(cost, rbound, last, first, redge)
+    o_opt, o_plan, o_st = O.segments(cost, rbound, last, first, redge, nthreads=oracle_threads())
+    np.testing.assert_array_equal(g_st, o_st, err_msg=f"status {label}")
+    np.testing.assert_array_equal(g_opt, o_opt, err_msg=f"opt {label}")
+    np.testing.assert_array_equal(g_plan, o_plan, err_msg=f"plan {label}")
+    return g_opt, g_plan
+
+
+def seg_case(seed, B, N, P, S, E, lo, hi):
+    rs = np.random.default_rng(seed)
+    K = S ** P
+    last, first = gen.digit_maps(P, S)
+    cost = rs.integers(lo, hi, size=(B, N, K)).astype(np.int32)
+    # boundary entries inside the exact range for this K (2^23 - 1 at K = 512)
+    rhi = min(hi, (1 << (32 - max(4, int(np.ceil(np.log2(K)))))) - 1)
+    rbound = rs.integers(min(lo, rhi - 1), rhi, size=(E, S, S)).astype(np.int32)
+    redge = rs.integers(0, E, size=N).astype(np.int32)
+    return cost, rbound, last, first, redge
+
+
+def test_config_full():
+    need_gpu()
+    say("config seg_gpt_n96_k81")
+    d = configs.make("seg_gpt_n96_k81")
+    assert_seg_parity(d["cost"], d["rbound"], d["last"], d["first"], d["redge"], "seg config")
+
+
+@pytest.mark.parametrize("N,P,S", [(1, 1, 2), (2, 1, 5), (5, 2, 3), (50, 4, 3), (30, 3, 4), (20, 5, 2), (40, 4, 4),
+                                   (10, 2, 8), (8, 3, 8), (70, 2, 7)])
+def test_shapes(N, P, S):
+    need_gpu()
+    say("seg shape", N, P, S)
+    cost, rbound, last, first, redge = seg_case([N, P, S], 5, N, P, S, 3, 10_000, 10_000_000)
+    assert_seg_parity(cost, rbound, last, first, redge, f"N={N} P={P} S={S}")
+
+
+def test_general_maps_unequal_boundaries():
+    """Arbitrary plan-to-boundary maps with different strategy counts on the
+    two sides (L = 3 last-block strategies, F = 5 first-block ones)."""
+    need_gpu()
+    rs = np.random.default_rng(77)
+    B, N, K, L, F = 6, 60, 100, 3, 5
+    last = rs.integers(0, L, size=K).astype(np.uint8)
+    first = rs.integers(0, F, size=K).astype(np.uint8)
+    cost = rs.integers(0, 10**6, size=(B, N, K)).astype(np.int32)
+    rbound = rs.integers(0, 10**6, size=(4, L, F)).astype(np.int32)
+    redge = rs.integers(0, 4, size=N).astype(np.int32)
+    assert_seg_parity(cost, rbound, last, first, redge, "general maps")
+
+
+@pytest.mark.parametrize("S", [2, 3])
+def test_heavy_ties(S):
+    need_gpu()
+    cost, rbound, last, first, redge = seg_case([9, S], 8, 40, 4, S, 2, 0, 3)
+    assert_seg_parity(cost, rbound, last, first, redge, f"ties S={S}")
+
+
+def test_unavailable_and_statuses():
+    need_gpu()
+    from paper_2504_00598_amd import CFP_ST_BADINPUT, CFP_ST_INFEASIBLE, cfp_r_limit, CFP_V_SEG
+    cost, rbound, last, first, redge = seg_case(10, 4, 20, 4, 3, 2, 0, 1000)
+    cost[0][cost[0] % 4 == 0] = INF
+    cost[1, 7, :] = INF                     # no plan
+    cost[2, 3, 5] = -1                      # negative cost
+    opt, st, plan = run_seg(cost, rbound, last, first, redge)
+    assert st[1] == CFP_ST_INFEASIBLE and st[2] == CFP_ST_BADINPUT
+    assert (plan[1] == -1).all() and (plan[2] == -1).all()
+    assert_seg_parity(cost[[0, 3]], rbound, last, first, redge, "inf")
+    # boundary entry at the exact-range limit, and a map entry out of range
+    rb = rbound.copy()
+    rb[1, 2, 0] = cfp_r_limit(CFP_V_SEG, 81)
+    _, st, _ = run_seg(cost[[0, 3]], rb, last, first, redge)
+    assert (st == CFP_ST_BADINPUT).all()
+    bad_last = last.copy()
+    bad_last[17] = 3
+    _, st, _ = run_seg(cost[[0, 3]], rbound, bad_last, first, redge)
+    assert (st == CFP_ST_BADINPUT).all()
+
+
+def test_max_boundary_values():
+    need_gpu()
+    from paper_2504_00598_amd import cfp_r_limit, CFP_V_SEG
+    cost, rbound, last, first, redge = seg_case(11, 4, 64, 4, 3, 2, 0, 10**7)
+    rbound[:] = cfp_r_limit(CFP_V_SEG, 81) - 1
+    rbound[:, np.arange(3), np.arange(3)] = 0
+    assert_seg_parity(cost, rbound, last, first, redge, "max r")
+
+
+def test_repeat_is_bit_identical():
+    need_gpu()
+    d = configs.make("seg_gpt_n96_k81", batch=32)
+    a = run_seg(d["cost"], d["rbound"], d["last"], d["first"], d["redge"])
+    for _ in range(3):
+        b = run_seg(d["cost"], d["rbound"], d["last"], d["first"], d["redge"])
+        for x, y in zip(a, b):
+            np.testing.assert_array_equal(x, y)

@@ -12,6 +12,9 @@ so every table is drawn from `workloads.gen` with a fixed seed.
     chain_wide_n512_k256   N=512  K=256 B=64   c,R ~ U[1e4,1e7), 25% of the
                                                off-diagonal R entries are 0
     scan_n4096_k512        N=4096 K=512 B=4    c,R ~ U[1e4,1e6)
+    seg_gpt_n96_k81        N=96 segments, K=81 plans (4 blocks x 3 strategies),
+                           B=256, c ~ U[4e4,4e7), boundary tables 2 x 3 x 3
+                           ~ U[1e4,1e7) with a zero diagonal
 
 All share 12 resharding tables with edge (i-1 -> i) using table i mod 12, and
 R has a zero diagonal.
@@ -62,6 +65,12 @@ CONFIGS = [
     Config(4, "chain_wide_n512_k256", "chain", 512, 256, 64, (10_000, 10_000_000), (10_000, 10_000_000),
            zero_frac_offdiag=0.25),
     Config(5, "scan_n4096_k512", "scan", 4096, 512, 4, (10_000, 1_000_000), (10_000, 1_000_000)),
+    # segment-level search: 96 GPT-like layers as segments of 4 blocks x 3
+    # strategies (81 plans), boundary resharding between the last and first
+    # blocks (3 x 3), one table for the boundary after the first layer's
+    # segment and one for the boundaries between repeated layers
+    Config(6, "seg_gpt_n96_k81", "seg", 96, 81, 256, (40_000, 40_000_000), (10_000, 10_000_000),
+           extra={"blocks": 4, "strategies": 3, "tables": 2}),
 ]
 
 BY_NAME = {c.name: c for c in CONFIGS}
@@ -82,6 +91,18 @@ def make(cfg: Config | str | int, batch: int | None = None) -> dict:
     elif isinstance(cfg, int):
         cfg = BY_IDX[cfg]
     B = cfg.B if batch is None else batch
+    if cfg.form == "seg":
+        P, S, E = cfg.extra["blocks"], cfg.extra["strategies"], cfg.extra["tables"]
+        last, first = gen.digit_maps(P, S)
+        redge = np.ones(cfg.N, np.int32)
+        redge[:2] = 0
+        return {
+            "cost": gen.make_cost(cfg.seed, B, cfg.N, cfg.K, *cfg.c_range),
+            "rbound": gen.make_rbound(cfg.seed, E, S, *cfg.r_range),
+            "last": last,
+            "first": first,
+            "redge": redge,
+        }
     out = {
         "cost": gen.make_cost(cfg.seed, B, cfg.N, cfg.K, *cfg.c_range),
         "rtab": gen.make_rtab(cfg.seed, N_TABLES, cfg.K, *cfg.r_range, zeros=cfg.zeros),

@@ -22,6 +22,7 @@ Tags and element orders:
     TAG_ZERO = 3   per table, the off-diagonal entries are ranked by
                    (u_k, flat index) and the smallest `zeros` are set to 0
     TAG_MEM  = 4   mem[b][i][s]    k = (b*N + i)*K + s
+    TAG_RB   = 5   rbound[e][l][f] k = (e*S + l)*S + f     (l == f set to 0)
 """
 from __future__ import annotations
 
@@ -35,6 +36,7 @@ TAG_COST = 1
 TAG_R = 2
 TAG_ZERO = 3
 TAG_MEM = 4
+TAG_RB = 5
 
 COST_INF = 0x7FFFFFFF  # "strategy unavailable" marker in a cost table
 
@@ -105,6 +107,22 @@ def make_rtab(seed: int, E: int, K: int, lo: int, hi: int, zeros: int = 0) -> np
 def make_mem(seed: int, B: int, N: int, K: int, lo: int, hi: int) -> np.ndarray:
     u = stream(seed, TAG_MEM, 0, B * N * K)
     return uniform_int(u, lo, hi).astype(np.uint8).reshape(B, N, K)
+
+
+def make_rbound(seed: int, E: int, S: int, lo: int, hi: int) -> np.ndarray:
+    """Boundary resharding tables [E][S][S] (last block strategy -> first
+    block strategy), uniform in [lo, hi), zero where the strategies match."""
+    u = stream(seed, TAG_RB, 0, E * S * S)
+    r = uniform_int(u, lo, hi).astype(np.int32).reshape(E, S, S)
+    r[:, np.arange(S), np.arange(S)] = 0
+    return r
+
+
+def digit_maps(P: int, S: int) -> tuple[np.ndarray, np.ndarray]:
+    """Plan t = sum_j x_j S^j of a segment of P blocks with S strategies each:
+    (last[t], first[t]) = (x_{P-1}, x_0)."""
+    t = np.arange(S ** P)
+    return (t // S ** (P - 1)).astype(np.uint8), (t % S).astype(np.uint8)
 
 
 def periodic_redge(N: int, E: int) -> np.ndarray:
