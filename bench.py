@@ -59,9 +59,12 @@ TRAFFIC = {
     "chain_gpt_n24_k16": {"fetch_kib": 18.4, "write_kib": 0.5, "sources": "8f49cac9c912f637"},
     "chain_gpt_n1152_k64": {"fetch_kib": 37915.9, "write_kib": 18456.0, "sources": "5a97ee1ff90b424c"},
     "mem_llama_n288_k32": {"fetch_kib": 60535.6, "write_kib": 239222.6, "sources": "d668d626f64cdbd7"},
-    "chain_wide_n512_k256": {"fetch_kib": 31097.5, "write_kib": 8183.9, "sources": "16b4cb1f0976b7ba"},
+    "chain_wide_n512_k256": {"fetch_kib": 30233.4, "write_kib": 8182.0, "sources": "eb76c9ed03780d22"},
     # mean over the 12 matrix-product launches of one forward call
     "scan_n4096_k512": {"fetch_kib": 3038953.7, "write_kib": 1398442.5, "sources": "de7227e316558ba4"},
+    "seg_gpt_n96_k81": {"fetch_kib": 3922.7, "write_kib": 1936.0, "sources": "db3445394db6f79e"},
+    # the memory workload run as a budget frontier (every chunk of every search active)
+    "mem_llama_n288_k32:frontier": {"fetch_kib": 78399.6, "write_kib": 307886.5, "sources": "30876301e6c50782"},
 }
 
 
@@ -81,8 +84,8 @@ def sources_hash(config: str) -> str:
     return h.hexdigest()[:16]
 
 
-def traffic_bytes(config: str):
-    t = TRAFFIC.get(config)
+def traffic_bytes(config: str, mode: str = ""):
+    t = TRAFFIC.get(config + (":" + mode if mode else ""))
     if t is None or t["sources"] != sources_hash(config):
         return None
     return (t["fetch_kib"] * FETCH_SCALE + t["write_kib"] * WRITE_SCALE) * 1024.0
@@ -371,7 +374,7 @@ def main() -> int:
         "pcie_inclusive": pcie_inclusive(r, data),
         "parity_vs_oracle": parity,
         "roofline": {"bound": "alu", "achieved": kern_cells_s / 1e12, "peak": PEAK_CELLS / 1e12, "unit": "Tcell/s",
-                     "frac": kern_cells_s / PEAK_CELLS, "traffic": traffic_bytes(cfg.name),
+                     "frac": kern_cells_s / PEAK_CELLS, "traffic": traffic_bytes(cfg.name, "frontier" if args.frontier else ""),
                      "kernel": KERNELS[cfg.name][0], "kernel_launches_per_step": kern_launches / args.steps,
                      "kernel_avg_us": kern_avg_ms * 1e3, "forward_call_cells_per_s": fwd_cells_s},
     }
