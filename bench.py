@@ -281,6 +281,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default=DEFAULT_CONFIG)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--sequential", action="store_true",
+                    help="scan workload only: run the sequential chain kernels instead of the min-plus scan")
     ap.add_argument("--frontier", action="store_true",
                     help="memory workload only: time the budget frontier (every budget 0..M-1 in one pass)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -299,6 +301,12 @@ def main() -> int:
 
     cfg = configs.BY_NAME[args.config]
     data = configs.make(cfg)
+    if args.sequential:
+        if cfg.form != "scan":
+            raise SystemExit("--sequential applies to the scan workload")
+        import dataclasses
+
+        cfg = dataclasses.replace(cfg, form="chain")
     if args.frontier:
         data = dict(data, budget=np.full(cfg.B, cfg.M - 1, np.int32))  # the pass covers every budget
     r = Runner(cfg, data, frontier=args.frontier)
@@ -349,6 +357,8 @@ def main() -> int:
             O.mem_frontier(data["cost"], data["rtab"], data["redge"], data["mem"], cfg.M, nthreads=oracle_threads())))
 
     wl = {"workload": cfg.name, "blocks": cfg.N, "strategies": cfg.K, "searches": cfg.B, "resharding_tables": 12}
+    if args.sequential:
+        wl["form"] = "sequential chain (not the scan)"
     if cfg.form == "seg":
         wl = {"workload": cfg.name, "segments": cfg.N, "plans": cfg.K, "searches": cfg.B,
               "boundary_tables": "2 x 3 x 3", "blocks_per_segment": 4, "strategies_per_block": 3}
@@ -374,8 +384,10 @@ def main() -> int:
         "pcie_inclusive": pcie_inclusive(r, data),
         "parity_vs_oracle": parity,
         "roofline": {"bound": "alu", "achieved": kern_cells_s / 1e12, "peak": PEAK_CELLS / 1e12, "unit": "Tcell/s",
-                     "frac": kern_cells_s / PEAK_CELLS, "traffic": traffic_bytes(cfg.name, "frontier" if args.frontier else ""),
-                     "kernel": KERNELS[cfg.name][0], "kernel_launches_per_step": kern_launches / args.steps,
+                     "frac": kern_cells_s / PEAK_CELLS,
+                     "traffic": None if args.sequential else traffic_bytes(cfg.name, "frontier" if args.frontier else ""),
+                     "kernel": "chain_fwd_split_kernel<512>" if args.sequential else KERNELS[cfg.name][0],
+                     "kernel_launches_per_step": kern_launches / args.steps,
                      "kernel_avg_us": kern_avg_ms * 1e3, "forward_call_cells_per_s": fwd_cells_s},
     }
     if cfg.form == "scan":

@@ -43,6 +43,8 @@ WsLayout layout(int variant, int n, int k, int batch, int n_mem, int n_tables) {
   if (variant == CFP_V_CHAIN && chain_fwd_wide_supported(k)) {
     L.wide = off;
     off = align_up(off + wide_region_bytes(n, k, batch, n_tables));
+    L.split = off;
+    off = align_up(off + split_region_bytes(k, batch));
   }
   if (variant == CFP_V_SCAN) {
     L.scan = off;
@@ -163,8 +165,14 @@ int cfp_dp_chain(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t *op
   WsHeader *hdr = (WsHeader *)w;
   if (launch_validate_rtab(d->rtab, d->n_tables, d->k, cfp_r_limit(CFP_V_CHAIN, d->k), hdr, st) != hipSuccess)
     return CFP_ERR_HIP;
-  if (launch_chain_fwd(*d, (const int32_t *)(w + L.redge), w + L.table, L.elem, w + L.wide,
-                       (SearchResult *)(w + L.result), hdr, opt, status, st) != hipSuccess)
+  hipError_t e;
+  if (chain_fwd_split_supported(d->k, d->n_tables, d->batch))
+    e = launch_chain_fwd_split(*d, (const int32_t *)(w + L.redge), w + L.split, w + L.table,
+                               (SearchResult *)(w + L.result), hdr, opt, status, st);
+  else
+    e = launch_chain_fwd(*d, (const int32_t *)(w + L.redge), w + L.table, L.elem, w + L.wide,
+                         (SearchResult *)(w + L.result), hdr, opt, status, st);
+  if (e != hipSuccess)
     return CFP_ERR_HIP;
   return CFP_OK;
 }

@@ -122,3 +122,45 @@ def test_periodic_layers(K):
     redge = (np.arange(N) % 12).astype(np.int32)
     say("periodic layers", K)
     assert_chain_parity(cost, rtab, redge, f"periodic K={K}")
+
+
+# K > 64 runs on one of two kernels: the split kernel (each search over P = K_P^2 / 4096
+# workgroups, K_P the padded K, tables in registers) when all B * P workgroups fit the
+# device's 256 compute units and there are at most 12 tables, else the wide kernel (one
+# workgroup per search streaming its tables).  Both must give the oracle's answer.
+
+@pytest.mark.parametrize("K,B", [(100, 65), (200, 17), (300, 5), (512, 5)])
+def test_wide_path_batches(K, B):
+    """Batches too large for the split kernel: the wide kernel."""
+    need_gpu()
+    from paper_2504_00598_amd import cfp_r_limit
+    say("wide path", K, B)
+    rhi = min(10_000_000, cfp_r_limit(0, K))
+    cost, rtab, redge = rand_case([3, K, B], B, 40, K, 12, 10_000, 10_000_000, rlo=10_000, rhi=rhi)
+    assert_chain_parity(cost, rtab, redge, f"wide K={K} B={B}")
+
+
+def test_wide_path_many_tables():
+    """More than 12 tables: the wide kernel even for a single search."""
+    need_gpu()
+    cost, rtab, redge = rand_case([4], 2, 60, 150, 17, 0, 10**6)
+    assert_chain_parity(cost, rtab, redge, "wide E=17")
+
+
+@pytest.mark.parametrize("N,K,B", [(300, 65, 4), (500, 128, 60), (400, 256, 16), (257, 257, 4), (200, 512, 4)])
+def test_split_path_long_chains(N, K, B):
+    """Few long chains spread over many workgroups (B * P = 256 at the largest)."""
+    need_gpu()
+    from paper_2504_00598_amd import cfp_r_limit
+    say("split path", N, K, B)
+    rhi = min(1_000_000, cfp_r_limit(0, K))
+    cost, rtab, redge = rand_case([5, N, K, B], B, N, K, 12, 10_000, 1_000_000, rlo=10_000, rhi=rhi)
+    assert_chain_parity(cost, rtab, redge, f"split N={N} K={K} B={B}")
+
+
+def test_long_chain_workload_sequential():
+    """The 4096-block K=512 workload of the scan through the chain search."""
+    need_gpu()
+    say("config scan_n4096_k512 through cfp_dp_chain")
+    d = configs.make("scan_n4096_k512")
+    assert_chain_parity(d["cost"], d["rtab"], d["redge"], "long chain sequential")
