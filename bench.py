@@ -41,7 +41,7 @@ KERNELS = {
     "chain_gpt_n24_k16": ("chain_fwd_res_kernel<16,12>", ["chain_fwd_res.hip", "res_common.h"]),
     "chain_gpt_n1152_k64": ("chain_fwd_k64_kernel<12>", ["chain_fwd_k64.hip", "res_common.h"]),
     "mem_llama_n288_k32": ("mem_fwd_kernel<32>", ["mem_fwd.hip", "res_common.h"]),
-    "chain_wide_n512_k256": ("chain_fwd_wide_kernel<256>", ["chain_fwd_wide.hip"]),
+    "chain_wide_n512_k256": ("chain_fwd_splitw_kernel<256>", ["chain_fwd_split.hip", "chain_fwd_wide.hip"]),
     "scan_n4096_k512": ("scan_gemm_kernel", ["scan.hip"]),
     "seg_gpt_n96_k81": ("seg_fwd_kernel<2>", ["seg_fwd.hip"]),
 }

@@ -167,8 +167,8 @@ int cfp_dp_chain(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t *op
     return CFP_ERR_HIP;
   hipError_t e;
   if (chain_fwd_split_supported(d->k, d->n_tables, d->batch))
-    e = launch_chain_fwd_split(*d, (const int32_t *)(w + L.redge), w + L.split, w + L.table,
-                               (SearchResult *)(w + L.result), hdr, opt, status, st);
+    e = launch_chain_fwd_split(*d, (const int32_t *)(w + L.redge), w + L.split, (uint32_t *)(w + L.wide),
+                               w + L.table, (SearchResult *)(w + L.result), hdr, opt, status, st);
   else
     e = launch_chain_fwd(*d, (const int32_t *)(w + L.redge), w + L.table, L.elem, w + L.wide,
                          (SearchResult *)(w + L.result), hdr, opt, status, st);

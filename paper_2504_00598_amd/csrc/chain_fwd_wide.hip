@@ -253,6 +253,12 @@ __global__ __launch_bounds__(kWideThreads, 1) void chain_fwd_wide_kernel(
 
 bool chain_fwd_wide_supported(int k) { return k > 64 && k <= 512; }
 
+void launch_pack_rtab(const int32_t *rtab, int E, int K, int KP, int lb, uint32_t *rpk, hipStream_t st) {
+  const size_t total = (size_t)E * KP * KP;
+  const int grid = (int)((total + 255) / 256 < 4096 ? (total + 255) / 256 : 4096);
+  hipLaunchKernelGGL(pack_rtab_kernel, dim3(grid), dim3(256), 0, st, rtab, E, K, KP, lb, rpk);
+}
+
 // Workspace region of the kernel: packed tables [E][KP][KP] u32, then the
 // cost-row minima [B][N] i32.
 static size_t wide_rpk_bytes(int k, int n_tables) {
