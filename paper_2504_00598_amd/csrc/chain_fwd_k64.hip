@@ -42,7 +42,11 @@ __global__ __launch_bounds__(kThreads, 1) void chain_fwd_k64_kernel(
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int myst = 16 * wid + (lane & 15);  // the state whose word this lane holds
   const int b = blockIdx.x;
-  CostStager<KP> cs(cost + (size_t)b * N * K, table + (size_t)b * N * K, N, K, tid);
+  // Cost blocks alternate between two stagers (block b in csb[b & 1]) so that a
+  // block is loaded two blocks (24 steps) before it is used: loaded one block
+  // ahead, its wait showed in the step time.
+  CostStager<KP> csb[2] = {CostStager<KP>(cost + (size_t)b * N * K, table + (size_t)b * N * K, N, K, tid),
+                           CostStager<KP>(cost + (size_t)b * N * K, table + (size_t)b * N * K, N, K, tid)};
 
   if (tid == 0) flags = 0;
 
@@ -64,10 +68,11 @@ __global__ __launch_bounds__(kThreads, 1) void chain_fwd_k64_kernel(
   int32_t ecur = load_edges(0), enext = N > U ? load_edges(1) : 0;
 
   const int nblk = (N + U - 1) / U;
-  cs.load(0);
+  csb[0].load(0);
   __syncthreads();  // flags initialised
-  cs.store(0, cadj[0], &flags);
-  if (nblk > 1) cs.load(1);
+  csb[0].store(0, cadj[0], &flags);
+  if (nblk > 1) csb[1].load(1);
+  if (nblk > 2) csb[0].load(2);
   __syncthreads();
 
   // Row 0.
@@ -78,8 +83,9 @@ __global__ __launch_bounds__(kThreads, 1) void chain_fwd_k64_kernel(
   }
   uint64_t dsum = 0;
 
-  auto step = [&](auto Jc, int blk, bool guard) __attribute__((always_inline)) {
+  auto step = [&](auto Jc, auto Pc, int blk, bool guard) __attribute__((always_inline)) {
     constexpr int J = decltype(Jc)::value;
+    constexpr int PB = decltype(Pc)::value;  // parity of blk
     const int i = blk * U + J;
     if (guard && (i < 1 || i >= N)) return;
     constexpr int cur = (J + 1) & 1, nxt = J & 1;  // parities of i-1 and i (U is even)
@@ -121,40 +127,44 @@ __global__ __launch_bounds__(kThreads, 1) void chain_fwd_k64_kernel(
     if (lane < 16) argb[blk & 1][J][myst] = (uint8_t)m;
     const uint32_t wm = group_min<16>(qv);
     if (lane == 0) wmin[nxt][wid] = wm;
-    if (J == 0) cs.flush(blk - 1, argb[(blk - 1) & 1]);
+    if (J == 0) csb[0].flush(blk - 1, argb[(blk - 1) & 1]);
     if (J == U - 1 && blk + 1 < nblk) {
-      cs.store(blk + 1, cadj[(blk + 1) & 1], &flags);
+      csb[1 - PB].store(blk + 1, cadj[(blk + 1) & 1], &flags);
+      if (blk + 3 < nblk) csb[1 - PB].load(blk + 3);
       if (EP == 0) ecur = enext;
-      if (blk + 2 < nblk) {
-        cs.load(blk + 2);
-        if (EP == 0) enext = load_edges(blk + 2);
-      }
+      if (EP == 0 && blk + 2 < nblk) enext = load_edges(blk + 2);
     }
   };
-  auto group = [&](int blk, bool guard) __attribute__((always_inline)) {
-    step(std::integral_constant<int, 0>{}, blk, guard);
-    step(std::integral_constant<int, 1>{}, blk, guard);
-    step(std::integral_constant<int, 2>{}, blk, guard);
-    step(std::integral_constant<int, 3>{}, blk, guard);
-    step(std::integral_constant<int, 4>{}, blk, guard);
-    step(std::integral_constant<int, 5>{}, blk, guard);
-    step(std::integral_constant<int, 6>{}, blk, guard);
-    step(std::integral_constant<int, 7>{}, blk, guard);
-    step(std::integral_constant<int, 8>{}, blk, guard);
-    step(std::integral_constant<int, 9>{}, blk, guard);
-    step(std::integral_constant<int, 10>{}, blk, guard);
-    step(std::integral_constant<int, 11>{}, blk, guard);
+  auto group = [&](auto Pc, int blk, bool guard) __attribute__((always_inline)) {
+    step(std::integral_constant<int, 0>{}, Pc, blk, guard);
+    step(std::integral_constant<int, 1>{}, Pc, blk, guard);
+    step(std::integral_constant<int, 2>{}, Pc, blk, guard);
+    step(std::integral_constant<int, 3>{}, Pc, blk, guard);
+    step(std::integral_constant<int, 4>{}, Pc, blk, guard);
+    step(std::integral_constant<int, 5>{}, Pc, blk, guard);
+    step(std::integral_constant<int, 6>{}, Pc, blk, guard);
+    step(std::integral_constant<int, 7>{}, Pc, blk, guard);
+    step(std::integral_constant<int, 8>{}, Pc, blk, guard);
+    step(std::integral_constant<int, 9>{}, Pc, blk, guard);
+    step(std::integral_constant<int, 10>{}, Pc, blk, guard);
+    step(std::integral_constant<int, 11>{}, Pc, blk, guard);
   };
+  const std::integral_constant<int, 0> even{};
+  const std::integral_constant<int, 1> odd{};
 
-  group(0, true);
-  int blk = 1;
-  for (; (blk + 1) * U <= N; ++blk) group(blk, false);
-  if (blk < nblk) group(blk, true);
+  group(even, 0, true);
+  int blk = 1;  // odd
+  for (; (blk + 2) * U <= N; blk += 2) {
+    group(odd, blk, false);
+    group(even, blk + 1, false);
+  }
+  if (blk < nblk) group(odd, blk, true);
+  if (blk + 1 < nblk) group(even, blk + 1, true);
   __syncthreads();
-  cs.flush((N - 1) / U, argb[((N - 1) / U) & 1]);
+  csb[0].flush((N - 1) / U, argb[((N - 1) / U) & 1]);
 
   const uint32_t pk = (lane < 16 && myst < K) ? (qv | (uint32_t)myst) : kSat;
-  finish_search(pk, cs.csum, dsum, BITS, QCAP, flags, hdr, b, opt, status, res);
+  finish_search(pk, csb[0].csum + csb[1].csum, dsum, BITS, QCAP, flags, hdr, b, opt, status, res);
 }
 
 template <int EP>

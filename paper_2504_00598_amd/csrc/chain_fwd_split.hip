@@ -183,6 +183,7 @@ __global__ __launch_bounds__(kSplitThreads, 1) void chain_fwd_split_kernel(
           w = kSat;
           break;
         }
+        __builtin_amdgcn_s_sleep(1);  // spaces the polls of the many waiting threads
       }
       yv[k] = (uint32_t)w;
       lm = umin(lm, yv[k]);
@@ -363,6 +364,7 @@ __global__ __launch_bounds__(kSplitWThreads, 1) void chain_fwd_splitw_kernel(
           __hip_atomic_store(&sflags[b], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           break;
         }
+        __builtin_amdgcn_s_sleep(1);  // spaces the polls of the many waiting threads
       }
     }
     rmin = block_min(yg);
