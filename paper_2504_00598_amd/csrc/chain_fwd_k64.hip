@@ -56,9 +56,11 @@ __global__ __launch_bounds__(kThreads, 1) void chain_fwd_k64_kernel(
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       const int t = 16 * wid + j;
-      rp[e][j] = (e < E && t < K && lane < K)
-                     ? (((uint32_t)rtab[((size_t)e * K + t) * K + lane] << BITS) | (uint32_t)t)
-                     : RP_NONE;
+      // every load is unconditional and in bounds (entry 0 for padding), so the
+      // 192 loads are in flight together instead of one after another
+      const bool ok = e < E && t < K && lane < K;
+      const uint32_t r = (uint32_t)rtab[ok ? ((size_t)e * K + t) * K + lane : 0];
+      rp[e][j] = ok ? ((r << BITS) | (uint32_t)t) : RP_NONE;
     }
 
   auto load_edges = [&](int blk) __attribute__((always_inline)) {

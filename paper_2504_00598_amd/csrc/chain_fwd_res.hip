@@ -93,8 +93,10 @@ __global__ __launch_bounds__(kThreads, 1) void chain_fwd_res_kernel(
 #pragma unroll
     for (int j = 0; j < TL; ++j) {
       const int t = t0 + j;
-      rp[e][j] = (e < E && t < K && s < K) ? (((uint32_t)rtab[((size_t)e * K + t) * K + s] << BITS) | (uint32_t)t)
-                                           : kSat;
+      // unconditional, in-bounds loads (entry 0 for padding) stay in flight together
+      const bool ok = e < E && t < K && s < K;
+      const uint32_t r = (uint32_t)rtab[ok ? ((size_t)e * K + t) * K + s : 0];
+      rp[e][j] = ok ? ((r << BITS) | (uint32_t)t) : kSat;
     }
 
   // Table index of every step of a block, per wave: lane r holds redge[blk*U + r].

@@ -80,8 +80,10 @@ __global__ __launch_bounds__(kSplitThreads, 1) void chain_fwd_split_kernel(
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       const int t = 16 * g + j;
-      rp[e][j] = (e < E && t < K && s < K) ? (((uint32_t)rtab[((size_t)e * K + t) * K + s] << BITS) | (uint32_t)t)
-                                           : kSat;
+      // unconditional, in-bounds loads (entry 0 for padding) stay in flight together
+      const bool ok = e < E && t < K && s < K;
+      const uint32_t r = (uint32_t)rtab[ok ? ((size_t)e * K + t) * K + s : 0];
+      rp[e][j] = ok ? ((r << BITS) | (uint32_t)t) : kSat;
     }
 
   // Block-wide minimum of one value per thread (one barrier).
