@@ -52,6 +52,7 @@ struct WsLayout {
   size_t bounds = 0;   // traceback chunk boundary states int32 [B][nchunks]
   size_t wide = 0;     // chain variant, K > 64: packed tables and cost-row minima
   size_t split = 0;    // chain variant, K > 64: exchange slots and flags of the split kernel
+  size_t wave = 0;     // chain variant, 32 < K <= 64 on long chains: packed tables, chunk records, checkpoints
   size_t scan = 0;     // scan variant: start of its private region
   size_t scan_bytes = 0;
   size_t total = 0;
@@ -71,6 +72,11 @@ hipError_t launch_seg_fwd(const cfp_segment_desc &d, const int32_t *redge_dev, u
 hipError_t launch_chain_fwd(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *table, int elem,
                             uint8_t *wide, SearchResult *res, const WsHeader *hdr, int64_t *opt,
                             int32_t *status, hipStream_t st);
+bool chain_wave_supported(int n, int k, int n_tables, int batch);
+size_t wave_region_bytes(int n, int k, int n_tables, int batch);
+hipError_t launch_chain_wave(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *region, uint8_t *table,
+                             SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
+                             hipStream_t st);
 bool chain_fwd_split_supported(int k, int n_tables, int batch);
 size_t split_region_bytes(int k, int batch);
 hipError_t launch_chain_fwd_split(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *region, uint32_t *rpk,

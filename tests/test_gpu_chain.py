@@ -164,3 +164,78 @@ def test_long_chain_workload_sequential():
     say("config scan_n4096_k512 through cfp_dp_chain")
     d = configs.make("scan_n4096_k512")
     assert_chain_parity(d["cost"], d["rtab"], d["redge"], "long chain sequential")
+
+
+# 32 < K <= 64 on long chains (at least 8 blocks of 12 rows) with at most 12 tables runs
+# chunk-parallel: the chains are cut into chunks that are searched concurrently from
+# arbitrary start rows and then repaired until their rows meet the speculative ones; a
+# chain whose rows never meet is finished sequentially.  Whatever happens inside, the
+# answer must be the oracle's.
+
+def _no_switch_tables(rs, E, K, lim):
+    """Resharding so dear that no plan ever switches strategy: the rows of two runs
+    started from different rows never become parallel, so no chunk's fix-up meets
+    its speculative run."""
+    rtab = rs.integers(lim - 1000, lim, size=(E, K, K)).astype(np.int32)
+    rtab[:, np.arange(K), np.arange(K)] = 0
+    return rtab
+
+
+@pytest.mark.parametrize("K,B", [(64, 3), (64, 70), (40, 9)])
+def test_chunked_rows_never_meet(K, B):
+    """Every chunk misses its checkpoints: the final pass reruns the chains."""
+    need_gpu()
+    from paper_2504_00598_amd import cfp_r_limit
+    rs = np.random.default_rng([40, K, B])
+    N = 600
+    cost = rs.integers(0, 50, size=(B, N, K)).astype(np.int32)
+    rtab = _no_switch_tables(rs, 12, K, cfp_r_limit(0, K))
+    redge = (np.arange(N) % 12).astype(np.int32)
+    say("chunked, no convergence", K, B)
+    assert_chain_parity(cost, rtab, redge, f"never meet K={K} B={B}")
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_chunked_some_chunks_meet(seed):
+    """A zero table (any row maps to a parallel one) placed on a few edges: chunks that
+    contain one meet their speculative run, the others do not, in a seeded pattern."""
+    need_gpu()
+    from paper_2504_00598_amd import cfp_r_limit
+    rs = np.random.default_rng([41, seed])
+    K, B, N = 64, 68, 900
+    cost = rs.integers(0, 1000, size=(B, N, K)).astype(np.int32)
+    rtab = _no_switch_tables(rs, 3, K, cfp_r_limit(0, K))
+    rtab[2] = 0
+    redge = rs.integers(0, 2, size=N).astype(np.int32)
+    resets = rs.choice(np.arange(1, N), size=int(rs.integers(1, 6)), replace=False)
+    redge[resets] = 2
+    say("chunked, partial convergence", seed, sorted(resets.tolist()))
+    assert_chain_parity(cost, rtab, redge, f"partial seed={seed}")
+
+
+@pytest.mark.parametrize("N,K,B", [(96, 64, 256), (100, 64, 255), (1000, 33, 67), (777, 48, 130), (1152, 64, 1),
+                                   (2000, 64, 8), (481, 63, 512)])
+def test_chunked_shapes(N, K, B):
+    """Ragged batches (searches beyond the last full group of a workgroup), ragged last
+    blocks, K below 64 and chunk counts from 2 to 64."""
+    need_gpu()
+    from paper_2504_00598_amd import cfp_r_limit
+    rhi = min(10_000_000, cfp_r_limit(0, K))
+    cost, rtab, redge = rand_case([42, N, K, B], B, N, K, 12, 10_000, 10_000_000, rlo=10_000, rhi=rhi)
+    if N % 2:
+        redge = (np.arange(N) % 12).astype(np.int32)  # the periodic (register-set) table selection
+    say("chunked shape", N, K, B)
+    assert_chain_parity(cost, rtab, redge, f"chunked N={N} K={K} B={B}")
+
+
+def test_chunked_ties_and_statuses():
+    """Tie-heavy values, unavailable strategies and bad inputs on the chunked path."""
+    need_gpu()
+    from paper_2504_00598_amd import CFP_ST_BADINPUT
+    cost, rtab, redge = rand_case([43], 70, 400, 64, 5, 0, 3, inf_frac=0.1)
+    cost[5, 250, :] = INF   # infeasible search, in a late chunk
+    assert_chain_parity(cost, rtab, redge, "chunked ties")
+    cost[9, 100, 3] = -7    # a negative cost is rejected by the library (the oracle has no such check)
+    opt, st, plan = run_chain(cost, rtab, redge)
+    assert st[9] == CFP_ST_BADINPUT and opt[9] == np.iinfo(np.int64).max and (plan[9] == -1).all()
+    assert st[5] != 0 and (st[np.r_[0:5, 6:9, 10:70]] == 0).all()
