@@ -39,7 +39,8 @@ DEFAULT_CONFIG = "chain_gpt_n1152_k64"
 # files it is built from.
 KERNELS = {
     "chain_gpt_n24_k16": ("chain_fwd_res_kernel<16,12>", ["chain_fwd_res.hip", "res_common.h"]),
-    "chain_gpt_n1152_k64": ("chain_fwd_k64_kernel<12>", ["chain_fwd_k64.hip", "res_common.h"]),
+    # speculative pass of the chunk-parallel search: it computes every step of every chain
+    "chain_gpt_n1152_k64": ("chain_wave_kernel<0, 12>", ["chain_wave.hip", "res_common.h"]),
     "mem_llama_n288_k32": ("mem_fwd_kernel<32>", ["mem_fwd.hip", "res_common.h"]),
     "chain_wide_n512_k256": ("chain_fwd_splitw_kernel<256>", ["chain_fwd_split.hip", "chain_fwd_wide.hip"]),
     "scan_n4096_k512": ("scan_gemm_kernel", ["scan.hip"]),

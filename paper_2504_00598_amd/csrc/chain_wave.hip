@@ -57,6 +57,10 @@ namespace cfp {
 
 namespace {
 
+// Four packed words as a native vector: copies stay in registers (a struct
+// copy of the HIP vector type goes through a private-memory temporary).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
 constexpr int kWSpec = 0, kWFix = 1, kWRepair = 2;
 constexpr int kWU = 12;                 // rows per block (checkpoint spacing)
 constexpr int kWWaves = 8;              // waves per workgroup of the speculative and fix-up passes
@@ -76,7 +80,7 @@ struct WaveRec {
 
 struct WaveArgs {
   const int32_t *cost;
-  const uint4 *rpk;     // packed tables [E][16 chunks][64 states] of 4 words
+  const u32x4 *rpk;     // packed tables [E][16 chunks][64 states] of 4 words
   const int32_t *redge;
   int N, K, E, B, P, CB, nblk, nq;  // nq = quads of 4 rows
   uint8_t *table;       // argmin entries [B][N][K]
@@ -121,7 +125,7 @@ __device__ __forceinline__ uint32_t wave_min64(uint32_t x) {
 // them, which waits the two states a DPP read of a fresh VALU result needs.
 #define CFP_W_ADD(T, C, W, J) "v_add_u32_dpp " T ", " C ", " W " row_newbcast:" J " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
 template <int J0, bool NOP>
-__device__ __forceinline__ void cand4_g2(uint32_t &a0, uint32_t &a1, uint32_t c0, uint32_t c1, const uint4 &w) {
+__device__ __forceinline__ void cand4_g2(uint32_t &a0, uint32_t &a1, uint32_t c0, uint32_t c1, const u32x4 &w) {
   uint32_t t0, t1, t2, t3;
   asm(
       ".if %[nop]\n s_nop 2\n .endif\n"
@@ -142,7 +146,7 @@ __device__ __forceinline__ void cand4_g2(uint32_t &a0, uint32_t &a1, uint32_t c0
         [j0] "i"(J0), [j1] "i"(J0 + 1), [j2] "i"(J0 + 2), [j3] "i"(J0 + 3), [nop] "i"(NOP ? 1 : 0));
 }
 template <int J0, bool NOP>
-__device__ __forceinline__ void cand4_g1(uint32_t &a0, uint32_t c0, const uint4 &w) {
+__device__ __forceinline__ void cand4_g1(uint32_t &a0, uint32_t c0, const u32x4 &w) {
   uint32_t t0, t1;
   asm(
       ".if %[nop]\n s_nop 2\n .endif\n"
@@ -161,7 +165,7 @@ __device__ __forceinline__ void cand4_g1(uint32_t &a0, uint32_t c0, const uint4 
 template <int NW>
 struct WaveSmem {
   static constexpr int CPT = kWTable16 / (64 * NW);  // 16-byte chunks per thread and table
-  uint4 tb[2][4][kWTable16];                          // packed tables of two quads of rows
+  u32x4 tb[2][4][kWTable16];                          // packed tables of two quads of rows
   uint8_t argb[NW][kWG][kWU][64];                     // argmin bytes of the block's rows, per wave and search
   int wdone[NW];                                      // fix-up: the wave's searches all met a checkpoint
 };
@@ -210,7 +214,7 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
   // its last row; everything is consumed at a quad's end, after its one wait.  (With stores in flight the wait covers
   // every outstanding load, so a load consumed earlier would stall the row.)
   // Array indices are literals only, so every array stays in registers.
-  uint4 sq[4][4];           // next quad's tables: [row in quad][chunk of this thread]
+  u32x4 sq[4][4];           // next quad's tables: [row in quad][chunk of this thread]
   // Costs of three consecutive quads, [quad mod 3][row in quad][search]: quad
   // q reads set q mod 3 while set (q+2) mod 3 is loaded.  A block of 12 rows
   // starts at a quad that is 0 mod 3, so every index is a constant.
@@ -219,7 +223,7 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
   {                                                                                \
     const int row = qbase + (V);                                                   \
     if (row <= ilast) {                                                            \
-      const uint4 *src = a.rpk + (size_t)edge(row) * kWTable16 + tid;              \
+      const u32x4 *src = a.rpk + (size_t)edge(row) * kWTable16 + tid;              \
       sq[V][0] = src[0];                                                           \
       sq[V][1] = src[64 * NW];                                                     \
       if constexpr (CPT == 4) {                                                    \
@@ -240,7 +244,7 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
   {                                                                                \
     const int row = qbase + (V);                                                   \
     if (row <= ilast) {                                                            \
-      uint4 *dst = sm.tb[(row >> 2) & 1][V] + tid;                                 \
+      u32x4 *dst = sm.tb[(row >> 2) & 1][V] + tid;                                 \
       dst[0] = sq[V][0];                                                           \
       dst[64 * NW] = sq[V][1];                                                     \
       if constexpr (CPT == 4) {                                                    \
@@ -316,9 +320,9 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
       uint8_t *dst = (g == 0 ? tb0 : tb1) - lane + (size_t)blk * U * K;
       for (int x = lane + 4 * r0; x < 4 * nr; x += 64) {  // piece x: row x / 4, bytes 16 (x % 4) ..
         const int r = x >> 2, c = (x & 3) * 16;
-        const uint4 v = *(const uint4 *)&sm.argb[wid][g][r][c];
+        const u32x4 v = *(const u32x4 *)&sm.argb[wid][g][r][c];
         if (K == 64) {
-          *(uint4 *)(dst + (size_t)r * K + c) = v;
+          *(u32x4 *)(dst + (size_t)r * K + c) = v;
         } else {
           const uint8_t *vb = (const uint8_t *)&v;
           for (int q = 0; q < 16 && c + q < K; ++q) dst[(size_t)r * K + c + q] = vb[q];
@@ -368,15 +372,22 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
       acc[g] = kSat;
     }
     // all sixteen table chunks of the row in flight at once
-    const uint4 *tb = sm.tb[(i >> 2) & 1][u];
-    uint4 w[16];
+    const u32x4 *tb = sm.tb[(i >> 2) & 1][u];
+    // The fix-up pass holds the checkpoint row besides, so it loads the row's
+    // table chunks in two halves to stay within the register file.
+    constexpr int WH = MODE == kWSpec ? 16 : 8;
+    u32x4 w[16];
 #pragma unroll
-    for (int cc_ = 0; cc_ < 16; ++cc_) w[cc_] = tb[cc_ * 64 + lane];
+    for (int cc_ = 0; cc_ < WH; ++cc_) w[cc_] = tb[cc_ * 64 + lane];
 #define CFP_CH(C, cc_)                                                                                   \
   if constexpr (G == 2) cand4_g2<4 * ((cc_) & 3), ((cc_) & 3) == 0>(acc[0], acc[G - 1], C[0], C[G - 1], w[cc_]); \
   else cand4_g1<4 * ((cc_) & 3), ((cc_) & 3) == 0>(acc[0], C[0], w[cc_]);
     CFP_CH(c0, 0) CFP_CH(c0, 1) CFP_CH(c0, 2) CFP_CH(c0, 3)
     CFP_CH(c1, 4) CFP_CH(c1, 5) CFP_CH(c1, 6) CFP_CH(c1, 7)
+    if constexpr (WH < 16) {
+#pragma unroll
+      for (int cc_ = 8; cc_ < 16; ++cc_) w[cc_] = tb[cc_ * 64 + lane];
+    }
     CFP_CH(c2, 8) CFP_CH(c2, 9) CFP_CH(c2, 10) CFP_CH(c2, 11)
     CFP_CH(c3, 12) CFP_CH(c3, 13) CFP_CH(c3, 14) CFP_CH(c3, 15)
 #undef CFP_CH
@@ -649,7 +660,7 @@ hipError_t launch_chain_wave(const cfp_chain_desc &d, const int32_t *redge_dev, 
   a.table = table;
   size_t off = 0;
   uint32_t *rpk = (uint32_t *)(region + off);
-  a.rpk = (const uint4 *)rpk;
+  a.rpk = (const u32x4 *)rpk;
   off += align_up((size_t)d.n_tables * 64 * 64 * 4);
   a.rec = (WaveRec *)(region + off);
   off += align_up((size_t)d.batch * c.P * sizeof(WaveRec));
