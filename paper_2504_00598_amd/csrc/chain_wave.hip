@@ -61,10 +61,10 @@ namespace {
 // copy of the HIP vector type goes through a private-memory temporary).
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kWSpec = 0, kWFix = 1, kWRepair = 2;
+constexpr int kWSpec = 0, kWRepair = 2;
 constexpr int kWU = 12;                 // rows per block (checkpoint spacing)
-constexpr int kWWaves = 8;              // waves per workgroup of the speculative and fix-up passes
-constexpr int kWG = 2;                  // searches per wave
+constexpr int kWWaves = 16;             // waves per workgroup of the speculative pass
+constexpr int kWG = 1;                  // searches per wave
 constexpr int kWTable16 = 64 * 64 / 4;  // 16-byte chunks of one packed table
 constexpr int kWMaxChunks = 64;         // chunks per search (the final pass reads one per lane)
 constexpr int kWMinBlocks = 4;          // least blocks of 12 rows per chunk
@@ -104,16 +104,20 @@ __global__ void wave_pack_kernel(const int32_t *__restrict__ rtab, int E, int K,
   }
 }
 
-// Minimum over the 64 lanes of a wave; every lane gets it.
-__device__ __forceinline__ uint32_t wave_min64(uint32_t x) {
+// Minimum over the 64 lanes of a wave as a scalar: row minima by DPP, then the
+// row broadcasts of lanes 15 and 31 fold rows 0..3 into row 3, read at lane 63.
+__device__ __forceinline__ uint32_t wave_min64_s(uint32_t x) {
   x = dpp_min<kQuadSwap1>(x);
   x = dpp_min<kQuadSwap2>(x);
   x = dpp_min<kHalfMirror>(x);
   x = dpp_min<kMirror>(x);
-  const auto h = __builtin_amdgcn_permlane32_swap(x, x, false, false);  // rows (0,1,0,1), (2,3,2,3)
-  x = umin(h[0], h[1]);
-  const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);  // rows (0,0,2,2), (1,1,3,3)
-  return umin(r[0], r[1]);
+  asm("s_nop 1\n"
+      "v_min_u32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
+      "s_nop 1\n"
+      "v_min_u32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf\n"
+      "s_nop 1\n"
+      : "+v"(x));
+  return __builtin_amdgcn_readlane(x, 63);
 }
 
 // Four candidates of predecessors 16k + J0 .. 16k + J0 + 3 for the wave's
@@ -167,7 +171,6 @@ struct WaveSmem {
   static constexpr int CPT = kWTable16 / (64 * NW);  // 16-byte chunks per thread and table
   u32x4 tb[2][4][kWTable16];                          // packed tables of two quads of rows
   uint8_t argb[NW][kWG][kWU][64];                     // argmin bytes of the block's rows, per wave and search
-  int wdone[NW];                                      // fix-up: the wave's searches all met a checkpoint
 };
 
 // State of a wave's searches.
@@ -175,9 +178,8 @@ template <int G>
 struct WaveChains {
   uint32_t qv[G];      // the lane's word of the current row
   uint64_t dsum[G];    // offset sum since the start row
-  int conv[G];         // fix-up: checkpoint quad met, -1 before
-  uint64_t dconv[G];   // fix-up: dsum at that checkpoint
   uint32_t flags[G];   // bit 0 a negative cost, bit 1 a row with no available strategy
+  uint32_t cor[G];     // speculative pass: OR of the lane's costs (bit 31 = a negative cost)
 };
 
 // Runs rows [12*blk0 (+1 for kSpec), min(12*blk1, N)) of the wave's G searches
@@ -185,16 +187,14 @@ struct WaveChains {
 // nvalid are real.
 //   kSpec:   the start row is row 12*blk0 from its costs alone; checkpoints are
 //            written.
-//   kFix:    the start row (row 12*blk0 - 1) is start[g]; the workgroup stops
-//            at the first checkpoint met by every search of every wave.
-//   kRepair: like kFix without checkpoints.
+//   kRepair: the start row (row 12*blk0 - 1) is start[g].
 template <int NW, int G, int MODE, int EP>
 __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, int blk0, int blk1,
                                          const uint32_t *const *start, WaveSmem<NW> &sm, WaveChains<G> &ch) {
   constexpr int U = kWU, CPT = WaveSmem<NW>::CPT;
   static_assert(G == 1 || G == 2, "one or two searches per wave");
-  static_assert(CPT == 2 || CPT == 4, "2 or 4 chunks per thread and table");
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  static_assert(CPT == 1 || CPT == 2 || CPT == 4, "1, 2 or 4 chunks per thread and table");
+  const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int N = a.N, K = a.K;
   const int i0 = blk0 * U + (MODE == kWSpec ? 1 : 0);  // first computed row
   const int ilast = min(blk1 * U, N) - 1;              // last row of the run
@@ -203,11 +203,12 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
   auto valid = [&](int g) __attribute__((always_inline)) { return g < nvalid && bw + g < a.B; };
   auto srch = [&](int g) __attribute__((always_inline)) { return min(bw + g, a.B - 1); };
   auto edge = [&](int row) __attribute__((always_inline)) { return EP ? row % (EP ? EP : 1) : a.redge[row]; };
-  // bases of the lane's cost and argmin entries of the two searches; a row adds row * K
-  const int32_t *cb0 = a.cost + (size_t)srch(0) * N * K + sl;
-  const int32_t *cb1 = a.cost + (size_t)srch(G - 1) * N * K + sl;
-  uint8_t *tb0 = a.table + (size_t)srch(0) * N * K + lane;
-  uint8_t *tb1 = a.table + (size_t)srch(G - 1) * N * K + lane;
+  // cost rows of the two searches (wave-uniform bases; a row adds row * K and
+  // the lane its state, so the loads take a scalar base and a lane offset)
+  const int32_t *cb0 = a.cost + (size_t)srch(0) * N * K;
+  const int32_t *cb1 = a.cost + (size_t)srch(G - 1) * N * K;
+  uint8_t *tb0 = a.table + (size_t)srch(0) * N * K;
+  uint8_t *tb1 = a.table + (size_t)srch(G - 1) * N * K;
 
   // Memory schedule.  The tables of the next quad are loaded during the first
   // three rows of a quad of four and the costs of the quad after the next in
@@ -221,36 +222,29 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
   uint32_t cs[3][4][2] = {};
 #define CFP_QLOAD(V)                                                               \
   {                                                                                \
-    const int row = qbase + (V);                                                   \
-    if (row <= ilast) {                                                            \
-      const u32x4 *src = a.rpk + (size_t)edge(row) * kWTable16 + tid;              \
-      sq[V][0] = src[0];                                                           \
-      sq[V][1] = src[64 * NW];                                                     \
-      if constexpr (CPT == 4) {                                                    \
-        sq[V][2] = src[128 * NW];                                                  \
-        sq[V][3] = src[192 * NW];                                                  \
-      }                                                                            \
+    const int row = min(qbase + (V), ilast); /* past the end: any in-range row */  \
+    const u32x4 *src = a.rpk + (size_t)edge(row) * kWTable16;                      \
+    sq[V][0] = src[tid];                                                           \
+    if constexpr (CPT >= 2) sq[V][1] = src[tid + 64 * NW];                         \
+    if constexpr (CPT == 4) {                                                      \
+      sq[V][2] = src[tid + 128 * NW];                                              \
+      sq[V][3] = src[tid + 192 * NW];                                              \
     }                                                                              \
   }
 #define CFP_CLOAD(V, DST)                                                          \
   {                                                                                \
-    const int row = cbase + (V);                                                   \
-    if (row <= ilast) {                                                            \
-      DST[V][0] = (uint32_t)cb0[(size_t)row * K];                                  \
-      if constexpr (G == 2) DST[V][1] = (uint32_t)cb1[(size_t)row * K];            \
-    }                                                                              \
+    const int row = min(cbase + (V), ilast);                                       \
+    DST[V][0] = (uint32_t)(cb0 + (size_t)row * K)[sl];                             \
+    if constexpr (G == 2) DST[V][1] = (uint32_t)(cb1 + (size_t)row * K)[sl];       \
   }
 #define CFP_QSTORE(V)                                                              \
   {                                                                                \
-    const int row = qbase + (V);                                                   \
-    if (row <= ilast) {                                                            \
-      u32x4 *dst = sm.tb[(row >> 2) & 1][V] + tid;                                 \
-      dst[0] = sq[V][0];                                                           \
-      dst[64 * NW] = sq[V][1];                                                     \
-      if constexpr (CPT == 4) {                                                    \
-        dst[128 * NW] = sq[V][2];                                                  \
-        dst[192 * NW] = sq[V][3];                                                  \
-      }                                                                            \
+    u32x4 *dst = sm.tb[((qbase + (V)) >> 2) & 1][V] + tid;                         \
+    dst[0] = sq[V][0];                                                             \
+    if constexpr (CPT >= 2) dst[64 * NW] = sq[V][1];                               \
+    if constexpr (CPT == 4) {                                                      \
+      dst[128 * NW] = sq[V][2];                                                    \
+      dst[192 * NW] = sq[V][3];                                                    \
     }                                                                              \
   }
 #define CFP_Q4(M) M(0) M(1) M(2) M(3)
@@ -259,11 +253,9 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
   // and the costs of the two quads after the first.
   {
     int qbase = i0 & ~3, cbase = qbase;
-#define CFP_QFIRST(V)                                 \
-  if (qbase + (V) >= i0) {                            \
-    CFP_QLOAD(V)                                      \
-    CFP_QSTORE(V)                                     \
-  }
+#define CFP_QFIRST(V) /* rows before i0 are staged too, and never read */ \
+  CFP_QLOAD(V)                                                             \
+  CFP_QSTORE(V)
     CFP_Q4(CFP_QFIRST)
 #undef CFP_QFIRST
     qbase += 4;
@@ -283,14 +275,12 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
 #pragma unroll
   for (int g = 0; g < G; ++g) {
     ch.flags[g] = 0;
-    ch.conv[g] = -1;
-    ch.dconv[g] = 0;
     if (MODE == kWSpec) {
-      const uint32_t cv = (uint32_t)(g == 0 ? cb0 : cb1)[(size_t)blk0 * U * K];
+      const uint32_t cv = (uint32_t)((g == 0 ? cb0 : cb1) + (size_t)blk0 * U * K)[sl];
       const bool avail = lane < K && cv != (uint32_t)CFP_COST_INF;
-      if (__ballot(lane < K && (int32_t)cv < 0)) ch.flags[g] |= 1;  // wave-uniform
+      ch.cor[g] = cv;
       const uint32_t x = avail ? cv : kWX;
-      const uint32_t d = __builtin_amdgcn_readfirstlane(wave_min64(x));
+      const uint32_t d = wave_min64_s(x);
       if (d == kWX) ch.flags[g] |= 2;
       ch.qv[g] = umin(x - d, kWQcap6 >> kWBits) << kWBits;
       ch.dsum[g] = d;
@@ -303,11 +293,6 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
       ch.dsum[g] = 0;
     }
   }
-  uint32_t ckv[G];
-  if (MODE == kWFix) {
-#pragma unroll
-    for (int g = 0; g < G; ++g) ckv[g] = a.ckrow[((size_t)srch(g) * a.nq + (i0 >> 2)) * 64 + lane];
-  }
   __syncthreads();  // the first quad's tables
 
   // Argmin bytes of rows [12 blk + r0, 12 blk + nr) of the wave's searches from
@@ -317,7 +302,7 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       if (!valid(g)) continue;
-      uint8_t *dst = (g == 0 ? tb0 : tb1) - lane + (size_t)blk * U * K;
+      uint8_t *dst = (g == 0 ? tb0 : tb1) + (size_t)blk * U * K;
       for (int x = lane + 4 * r0; x < 4 * nr; x += 64) {  // piece x: row x / 4, bytes 16 (x % 4) ..
         const int r = x >> 2, c = (x & 3) * 16;
         const u32x4 v = *(const u32x4 *)&sm.argb[wid][g][r][c];
@@ -331,15 +316,16 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
     }
   };
 
-  bool done = false;
-  // One row; J = row mod 12.
-  auto step = [&](auto Jc, auto Gd, int blk) __attribute__((always_inline)) {
+  // One row; J = row mod 12.  GUARD: the block may end before its 12th row;
+  // FIRST: the run's first block, whose rows before i0 are skipped and whose
+  // first quad's loads were issued before the loop.
+  auto step = [&](auto Jc, auto Gd, auto Fd, int blk) __attribute__((always_inline)) {
     constexpr int J = decltype(Jc)::value, u = J & 3;
-    constexpr bool GUARD = decltype(Gd)::value;
+    constexpr bool GUARD = decltype(Gd)::value, FIRST = decltype(Fd)::value;
     const int i = blk * U + J;
     if (GUARD && i > ilast) return;
-    if (i < i0) return;
-    if (i >= (i0 & ~3) + 4) {  // the next quad's loads (the first quad's: prologue)
+    if (FIRST && i < i0) return;
+    if (!FIRST || i >= (i0 & ~3) + 4) {  // the next quad's loads (the first quad's: prologue)
       // rows 0 and 1 at step 0, row 2 at step 1, row 3 at step 2: every load
       // has at least one row of compute before the quad's wait
       const int qbase = (i & ~3) + 4;
@@ -350,7 +336,7 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
       if constexpr (u == 1) CFP_QLOAD(2)
       if constexpr (u == 2) CFP_QLOAD(3)
     }
-    if (u == 3 && i >= (i0 & ~3) + 4) {  // costs two quads ahead, after this quad's table loads
+    if (u == 3 && (!FIRST || i >= (i0 & ~3) + 4)) {  // costs two quads ahead, after this quad's table loads
       const int cbase = (i & ~3) + 8;
       constexpr int nset = (J / 4 + 2) % 3;
       if constexpr (nset == 0) { CFP_Q4(CFP_C0) }
@@ -375,79 +361,65 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
     const u32x4 *tb = sm.tb[(i >> 2) & 1][u];
     // The fix-up pass holds the checkpoint row besides, so it loads the row's
     // table chunks in two halves to stay within the register file.
-    constexpr int WH = MODE == kWSpec ? 16 : 8;
+    constexpr int WH = (MODE == kWSpec && G == 2) ? 16 : 8;
     u32x4 w[16];
-#pragma unroll
-    for (int cc_ = 0; cc_ < WH; ++cc_) w[cc_] = tb[cc_ * 64 + lane];
-#define CFP_CH(C, cc_)                                                                                   \
-  if constexpr (G == 2) cand4_g2<4 * ((cc_) & 3), ((cc_) & 3) == 0>(acc[0], acc[G - 1], C[0], C[G - 1], w[cc_]); \
-  else cand4_g1<4 * ((cc_) & 3), ((cc_) & 3) == 0>(acc[0], C[0], w[cc_]);
-    CFP_CH(c0, 0) CFP_CH(c0, 1) CFP_CH(c0, 2) CFP_CH(c0, 3)
-    CFP_CH(c1, 4) CFP_CH(c1, 5) CFP_CH(c1, 6) CFP_CH(c1, 7)
-    if constexpr (WH < 16) {
-#pragma unroll
-      for (int cc_ = 8; cc_ < 16; ++cc_) w[cc_] = tb[cc_ * 64 + lane];
-    }
-    CFP_CH(c2, 8) CFP_CH(c2, 9) CFP_CH(c2, 10) CFP_CH(c2, 11)
-    CFP_CH(c3, 12) CFP_CH(c3, 13) CFP_CH(c3, 14) CFP_CH(c3, 15)
-#undef CFP_CH
+    // Candidates of every predecessor for the searches X (and Y): two
+    // searches share each table chunk read.
+#define CFP_CH2(C, cc_) cand4_g2<4 * ((cc_) & 3), ((cc_) & 3) == 0>(acc[0], acc[G - 1], C[0], C[G - 1], w[cc_]);
+#define CFP_CH1(X, C, cc_) cand4_g1<4 * ((cc_) & 3), ((cc_) & 3) == 0>(acc[X], C[X], w[cc_]);
+#define CFP_ROW(CH, ...)                                                                   \
+  {                                                                                        \
+    _Pragma("unroll") for (int cc_ = 0; cc_ < WH; ++cc_) w[cc_] = tb[cc_ * 64 + lane];     \
+    CH(__VA_ARGS__ c0, 0) CH(__VA_ARGS__ c0, 1) CH(__VA_ARGS__ c0, 2) CH(__VA_ARGS__ c0, 3) \
+    CH(__VA_ARGS__ c1, 4) CH(__VA_ARGS__ c1, 5) CH(__VA_ARGS__ c1, 6) CH(__VA_ARGS__ c1, 7) \
+    if constexpr (WH < 16) {                                                               \
+      _Pragma("unroll") for (int cc_ = 8; cc_ < 16; ++cc_) w[cc_] = tb[cc_ * 64 + lane];   \
+    }                                                                                      \
+    CH(__VA_ARGS__ c2, 8) CH(__VA_ARGS__ c2, 9) CH(__VA_ARGS__ c2, 10) CH(__VA_ARGS__ c2, 11) \
+    CH(__VA_ARGS__ c3, 12) CH(__VA_ARGS__ c3, 13) CH(__VA_ARGS__ c3, 14) CH(__VA_ARGS__ c3, 15) \
+  }
+    if constexpr (G == 2) CFP_ROW(CFP_CH2)
+    else CFP_ROW(CFP_CH1, 0,)
+#undef CFP_ROW
+#undef CFP_CH1
+#undef CFP_CH2
 
     // New row: add the cost, normalise by the row minimum, record the argmin.
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       const uint32_t cv = cs[(J / 4) % 3][u][g];
       const bool avail = lane < K && cv != (uint32_t)CFP_COST_INF;
-      if (__ballot(lane < K && (int32_t)cv < 0)) ch.flags[g] |= 1;  // wave-uniform
+      if (MODE == kWSpec) ch.cor[g] |= cv;
       const uint32_t x = avail ? (acc[g] >> kWBits) + cv : kWX;
-      const uint32_t d = __builtin_amdgcn_readfirstlane(wave_min64(x));
-      if (d == kWX) ch.flags[g] |= 2;
+      const uint32_t d = wave_min64_s(x);
+      if (MODE == kWSpec && d == kWX) ch.flags[g] |= 2;
       ch.qv[g] = umin(x - d, kWQcap6 >> kWBits) << kWBits;
       ch.dsum[g] += d;
       sm.argb[wid][g][J][lane] = (uint8_t)acc[g];
     }
 
-    // End of a block: the argmin rows (each wave writes back its own searches'
-    // bytes with 16-byte stores).
-    if (J == U - 1 || (GUARD && i == ilast)) flush(blk, J + 1);
-
-    // End of a quad: checkpoint (speculative pass) or comparison (fix-up pass).
-    const bool qend = u == 3 || i == ilast;
-    if (qend) {
-      const int q = i >> 2;
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        if (MODE == kWSpec && valid(g)) {
-          a.ckrow[((size_t)(bw + g) * a.nq + q) * 64 + lane] = ch.qv[g];
-          if (lane == 0) a.dck[(size_t)(bw + g) * a.nq + q] = (int64_t)ch.dsum[g];
-        }
-        if (MODE == kWFix && ch.conv[g] < 0 && __ballot(ch.qv[g] != ckv[g]) == 0) {
-          ch.conv[g] = q;
-          ch.dconv[g] = ch.dsum[g];
-        }
-      }
-      if (MODE == kWFix) {
-        bool mine = true;
-#pragma unroll
-        for (int g = 0; g < G; ++g) mine = mine && (ch.conv[g] >= 0 || !valid(g));
-        if (lane == 0) sm.wdone[wid] = mine;
-      }
-    }
-
-    // End of a quad: its successor's tables and costs in place, one barrier.
-    if (qend) {
-      const int qbase = (i & ~3) + 4;
-      CFP_Q4(CFP_QSTORE)
-      if (MODE == kWFix && i < ilast) {
-#pragma unroll
-        for (int g = 0; g < G; ++g) ckv[g] = a.ckrow[((size_t)srch(g) * a.nq + (i >> 2) + 1) * 64 + lane];
+    // End of a quad: the next quad's tables in place and one barrier, then the
+    // checkpoint (speculative pass) and, at the end of a block, the argmin rows
+    // (each wave writes back its own searches' bytes with 16-byte stores).  The
+    // stores come after the barrier's wait for the staged loads, so that wait
+    // does not cover them.
+    constexpr bool QEND = u == 3;
+    if (QEND || (GUARD && i == ilast)) {
+      {
+        const int qbase = (i & ~3) + 4;
+        CFP_Q4(CFP_QSTORE)
       }
       __syncthreads();
-      if (MODE == kWFix) {
-        bool all = true;
+      if (MODE == kWSpec) {
+        const int q = i >> 2;
 #pragma unroll
-        for (int w_ = 0; w_ < NW; ++w_) all = all && sm.wdone[w_];
-        done = all;
+        for (int g = 0; g < G; ++g) {
+          if (!valid(g)) continue;
+          (a.ckrow + ((size_t)(bw + g) * a.nq + q) * 64)[lane] = ch.qv[g];
+          if (lane == 0) a.dck[(size_t)(bw + g) * a.nq + q] = (int64_t)ch.dsum[g];
+        }
       }
+      if (J == U - 1 || (GUARD && i == ilast)) flush(blk, J + 1);
     }
   };
 #undef CFP_Q4
@@ -458,57 +430,178 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
 #undef CFP_C1
 #undef CFP_C2
 
-  // The fix-up pass stops at the first quad end where every search of every
-  // wave has met a checkpoint; the block's argmin rows so far are written first.
-  auto block = [&](auto Gd, int blk) __attribute__((always_inline)) {
-#define CFP_S(J_) step(std::integral_constant<int, J_>{}, Gd, blk);
-#define CFP_X(J_)                                \
-  if (MODE == kWFix && done) {                   \
-    flush(blk, J_ + 1);                          \
-    return;                                      \
-  }
-    CFP_S(0) CFP_S(1) CFP_S(2) CFP_S(3) CFP_X(3)
-    CFP_S(4) CFP_S(5) CFP_S(6) CFP_S(7) CFP_X(7)
-    CFP_S(8) CFP_S(9) CFP_S(10) CFP_S(11)
-#undef CFP_X
+  auto block = [&](auto Gd, auto Fd, int blk) __attribute__((always_inline)) {
+#define CFP_S(J_) step(std::integral_constant<int, J_>{}, Gd, Fd, blk);
+    CFP_S(0) CFP_S(1) CFP_S(2) CFP_S(3) CFP_S(4) CFP_S(5)
+    CFP_S(6) CFP_S(7) CFP_S(8) CFP_S(9) CFP_S(10) CFP_S(11)
 #undef CFP_S
   };
 
-  int blk = blk0;
   const int full_end = min(blk1, N / U);  // blocks with 12 rows
-  for (; blk < full_end; ++blk) {
-    block(std::false_type{}, blk);
-    if (MODE == kWFix && done) return;
+  if (blk0 >= full_end) {  // a single block, not full
+    block(std::true_type{}, std::true_type{}, blk0);
+    return;
   }
-  if (blk < blk1) block(std::true_type{}, blk);
+  block(std::false_type{}, std::true_type{}, blk0);
+  int blk = blk0 + 1;
+  for (; blk < full_end; ++blk) block(std::false_type{}, std::false_type{}, blk);
+  if (blk < blk1) block(std::true_type{}, std::false_type{}, blk);
 }
 
-// Speculative (MODE kWSpec, grid (ceil(B/16), P)) and fix-up (kWFix, grid
-// (ceil(B/16), P-1)) passes.
-template <int MODE, int EP>
-__global__ __launch_bounds__(64 * kWWaves, 2) void chain_wave_kernel(WaveArgs a) {
+// Speculative pass, grid (ceil(B/16), P).
+template <int EP>
+__global__ __launch_bounds__(64 * kWWaves) void chain_wave_kernel(WaveArgs a) {
   __shared__ __align__(16) WaveSmem<kWWaves> sm;
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int bw = blockIdx.x * kWWaves * kWG + wid * kWG;
-  const int p = MODE == kWFix ? blockIdx.y + 1 : blockIdx.y;
+  const int p = blockIdx.y;
   const int blk0 = p * a.CB, blk1 = min(blk0 + a.CB, a.nblk);
-  const uint32_t *start[kWG];
-#pragma unroll
-  for (int g = 0; g < kWG; ++g) start[g] = a.ckrow + ((size_t)min(bw + g, a.B - 1) * a.nq + 3 * blk0 - 1) * 64;
   WaveChains<kWG> ch;
-  wave_run<kWWaves, kWG, MODE, EP>(a, bw, kWG, blk0, blk1, start, sm, ch);
+  wave_run<kWWaves, kWG, kWSpec, EP>(a, bw, kWG, blk0, blk1, nullptr, sm, ch);
 #pragma unroll
   for (int g = 0; g < kWG; ++g) {
+    if (__ballot((int32_t)ch.cor[g] < 0)) ch.flags[g] |= 1;  // wave-uniform
     if (bw + g >= a.B) continue;
-    WaveRec &r = a.rec[(size_t)(bw + g) * a.P + p];
-    if (MODE == kWSpec) {
-      if (lane == 0) r.flags = (int32_t)ch.flags[g];
-    } else {
-      if (ch.conv[g] < 0) a.endrow[((size_t)(bw + g) * a.P + p) * 64 + lane] = ch.qv[g];
-      if (lane == 0) {
-        r.conv = ch.conv[g];
-        r.dfix = (int64_t)(ch.conv[g] >= 0 ? ch.dconv[g] : ch.dsum[g]);
+    if (lane == 0) a.rec[(size_t)(bw + g) * a.P + p].flags = (int32_t)ch.flags[g];
+  }
+}
+
+// Fix-up pass with independent waves.  Each wave carries two searches of one
+// chunk p >= 1, starting from the last checkpoint row of chunk p-1, and reads
+// the packed tables of every row straight from the table array (a few hundred
+// KiB that stays in the caches; every chunk starts at a multiple of 12 rows, so
+// all waves walk the same table sequence), one row ahead.  A wave stops at the
+// first quad end where both of its searches have met a checkpoint, so a slowly
+// converging search runs on alone instead of holding a workgroup of others.
+// Grid (ceil(B / (2 kWFixWaves)), P - 1); no barriers.
+constexpr int kWFixWaves = 4;
+
+template <int EP>
+__global__ __launch_bounds__(64 * kWFixWaves) void chain_wave_fix_kernel(WaveArgs a) {
+  const int lane = threadIdx.x & 63, wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int bw = (blockIdx.x * kWFixWaves + wid) * 2;
+  if (bw >= a.B) return;  // the whole wave
+  const bool two = bw + 1 < a.B;
+  const int b1 = two ? bw + 1 : bw;
+  const int p = blockIdx.y + 1;
+  const int blk0 = p * a.CB, blk1 = min(blk0 + a.CB, a.nblk);
+  const int N = a.N, K = a.K;
+  const int i0 = blk0 * kWU, ilast = min(blk1 * kWU, N) - 1;  // i0 is a multiple of 4
+  const int sl = min(lane, K - 1);
+  auto edge = [&](int row) __attribute__((always_inline)) { return EP ? row % (EP ? EP : 1) : a.redge[row]; };
+  const int32_t *cb0 = a.cost + (size_t)bw * N * K;  // wave-uniform bases
+  const int32_t *cb1 = a.cost + (size_t)b1 * N * K;
+  uint8_t *tb0 = a.table + (size_t)bw * N * K;
+  uint8_t *tb1 = a.table + (size_t)b1 * N * K;
+  const uint32_t *ck0 = a.ckrow + (size_t)bw * a.nq * 64;
+  const uint32_t *ck1 = a.ckrow + (size_t)b1 * a.nq * 64;
+
+  uint32_t qv[2] = {(ck0 + (size_t)(i0 / 4 - 1) * 64)[lane], (ck1 + (size_t)(i0 / 4 - 1) * 64)[lane]};
+  uint64_t dsum[2] = {0, 0}, dconv[2] = {0, 0};
+  int conv[2] = {-1, two ? -1 : 0};  // a missing second search counts as met
+
+  u32x4 wA[16], wB[16];
+  auto tload = [&](u32x4(&w)[16], int row) __attribute__((always_inline)) {
+    const u32x4 *src = a.rpk + (size_t)edge(row) * kWTable16;
+#pragma unroll
+    for (int c = 0; c < 16; ++c) w[c] = src[lane + c * 64];
+  };
+  // Memory schedule.  Loads complete in issue order, so a load issued before
+  // the tables of row r+1 must be back when row r+1 starts.  The next row's
+  // tables come first in every row, then the costs two rows ahead (a ring of
+  // four rows, [search][row mod 4]) and, in the first row of a quad, the
+  // quad's checkpoint row: each has a whole row of compute to arrive.
+  uint32_t cr[2][4];
+  auto cload = [&](int row, int slot) __attribute__((always_inline)) {
+    const int r = min(row, ilast);
+    cr[0][slot] = (uint32_t)(cb0 + (size_t)r * K)[sl];
+    cr[1][slot] = (uint32_t)(cb1 + (size_t)r * K)[sl];
+  };
+  uint32_t ckv[2] = {0, 0};
+
+  // One row i (u = i mod 4) with the tables in w; the next row's tables go to wn.
+  auto row = [&](int i, auto Uc, u32x4(&w)[16], u32x4(&wn)[16]) __attribute__((always_inline)) {
+    constexpr int u = decltype(Uc)::value;
+    if (i < ilast) tload(wn, i + 1);
+    cload(i + 2, (u + 2) & 3);
+    if (u == 0) {
+      ckv[0] = (ck0 + (size_t)(i >> 2) * 64)[lane];
+      ckv[1] = (ck1 + (size_t)(i >> 2) * 64)[lane];
+    }
+    const bool act[2] = {conv[0] < 0, conv[1] < 0};
+    uint32_t c0[2], c1[2], c2[2], c3[2], acc[2];
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      if (!act[g]) continue;
+      const auto pp = __builtin_amdgcn_permlane16_swap(qv[g], qv[g], false, false);
+      const auto lo = __builtin_amdgcn_permlane32_swap(pp[0], pp[0], false, false);
+      const auto hi = __builtin_amdgcn_permlane32_swap(pp[1], pp[1], false, false);
+      c0[g] = lo[0];
+      c2[g] = lo[1];
+      c1[g] = hi[0];
+      c3[g] = hi[1];
+      acc[g] = kSat;
+    }
+#define CFP_CH2(C, cc_) cand4_g2<4 * ((cc_) & 3), ((cc_) & 3) == 0>(acc[0], acc[1], C[0], C[1], w[cc_]);
+#define CFP_CH1(X, C, cc_) cand4_g1<4 * ((cc_) & 3), ((cc_) & 3) == 0>(acc[X], C[X], w[cc_]);
+#define CFP_ROW(CH, ...)                                                                        \
+  {                                                                                             \
+    CH(__VA_ARGS__ c0, 0) CH(__VA_ARGS__ c0, 1) CH(__VA_ARGS__ c0, 2) CH(__VA_ARGS__ c0, 3)     \
+    CH(__VA_ARGS__ c1, 4) CH(__VA_ARGS__ c1, 5) CH(__VA_ARGS__ c1, 6) CH(__VA_ARGS__ c1, 7)     \
+    CH(__VA_ARGS__ c2, 8) CH(__VA_ARGS__ c2, 9) CH(__VA_ARGS__ c2, 10) CH(__VA_ARGS__ c2, 11)   \
+    CH(__VA_ARGS__ c3, 12) CH(__VA_ARGS__ c3, 13) CH(__VA_ARGS__ c3, 14) CH(__VA_ARGS__ c3, 15) \
+  }
+    if (act[0] && act[1]) CFP_ROW(CFP_CH2)
+    else if (act[0]) CFP_ROW(CFP_CH1, 0,)
+    else if (act[1]) CFP_ROW(CFP_CH1, 1,)
+#undef CFP_ROW
+#undef CFP_CH1
+#undef CFP_CH2
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      if (!act[g]) continue;
+      const uint32_t cv = cr[g][u];
+      const bool avail = lane < K && cv != (uint32_t)CFP_COST_INF;
+      const uint32_t x = avail ? (acc[g] >> kWBits) + cv : kWX;
+      const uint32_t d = wave_min64_s(x);
+      qv[g] = umin(x - d, kWQcap6 >> kWBits) << kWBits;
+      dsum[g] += d;
+      if (lane < K) ((g == 0 ? tb0 : tb1) + (size_t)i * K)[lane] = (uint8_t)acc[g];
+    }
+  };
+
+  tload(wA, i0);
+  cload(i0, 0);
+  cload(i0 + 1, 1);
+  using U0 = std::integral_constant<int, 0>;
+  using U1 = std::integral_constant<int, 1>;
+  using U2 = std::integral_constant<int, 2>;
+  using U3 = std::integral_constant<int, 3>;
+  for (int q0 = i0; q0 <= ilast; q0 += 4) {
+    row(q0, U0{}, wA, wB);
+    if (q0 + 1 <= ilast) row(q0 + 1, U1{}, wB, wA);
+    if (q0 + 2 <= ilast) row(q0 + 2, U2{}, wA, wB);
+    if (q0 + 3 <= ilast) row(q0 + 3, U3{}, wB, wA);
+    // Quad end: meet the speculative checkpoint of the same quad.
+    const int q = min(q0 + 3, ilast) >> 2;
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      if (conv[g] < 0 && __ballot(qv[g] != ckv[g]) == 0) {
+        conv[g] = q;
+        dconv[g] = dsum[g];
       }
+    }
+    if (conv[0] >= 0 && conv[1] >= 0) break;
+  }
+#pragma unroll
+  for (int g = 0; g < 2; ++g) {
+    if (g == 1 && !two) continue;
+    const int b = bw + g;
+    if (conv[g] < 0) a.endrow[((size_t)b * a.P + p) * 64 + lane] = qv[g];
+    if (lane == 0) {
+      WaveRec &r = a.rec[(size_t)b * a.P + p];
+      r.conv = conv[g];
+      r.dfix = (int64_t)(conv[g] >= 0 ? dconv[g] : dsum[g]);
     }
   }
 }
@@ -611,9 +704,10 @@ static void launch_wave_passes(const WaveArgs &a, const WsHeader *hdr, SearchRes
                                int32_t *status, hipStream_t st) {
   const int rows = (a.B + kWWaves * kWG - 1) / (kWWaves * kWG);
   timer_begin(st);
-  hipLaunchKernelGGL((chain_wave_kernel<kWSpec, EP>), dim3(rows, a.P), dim3(64 * kWWaves), 0, st, a);
+  hipLaunchKernelGGL((chain_wave_kernel<EP>), dim3(rows, a.P), dim3(64 * kWWaves), 0, st, a);
   timer_end(st);
-  hipLaunchKernelGGL((chain_wave_kernel<kWFix, EP>), dim3(rows, a.P - 1), dim3(64 * kWWaves), 0, st, a);
+  hipLaunchKernelGGL((chain_wave_fix_kernel<EP>), dim3((a.B + 2 * kWFixWaves - 1) / (2 * kWFixWaves), a.P - 1),
+                     dim3(64 * kWFixWaves), 0, st, a);
   hipLaunchKernelGGL((chain_wave_final_kernel<EP>), dim3(a.B), dim3(64 * kWFinalWaves), 0, st, a, hdr, res, opt,
                      status);
 }
