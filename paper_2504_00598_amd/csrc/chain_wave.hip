@@ -164,6 +164,20 @@ __device__ __forceinline__ void cand4_g1(uint32_t &a0, uint32_t c0, const u32x4 
       : [c0] "v"(c0), [wx] "v"(w.x), [wy] "v"(w.y), [wz] "v"(w.z), [ww] "v"(w.w),
         [j0] "i"(J0), [j1] "i"(J0 + 1), [j2] "i"(J0 + 2), [j3] "i"(J0 + 3), [nop] "i"(NOP ? 1 : 0));
 }
+// The first four candidates of a row: a0 is set, not updated.
+__device__ __forceinline__ void cand4_g1_first(uint32_t &a0, uint32_t c0, const u32x4 &w) {
+  uint32_t t0, t1;
+  asm(
+      "s_nop 2\n"
+      CFP_W_ADD("%[t0]", "%[c0]", "%[wx]", "0")
+      CFP_W_ADD("%[t1]", "%[c0]", "%[wy]", "1")
+      "v_min_u32 %[a0], %[t0], %[t1]\n"
+      CFP_W_ADD("%[t0]", "%[c0]", "%[wz]", "2")
+      CFP_W_ADD("%[t1]", "%[c0]", "%[ww]", "3")
+      "v_min3_u32 %[a0], %[a0], %[t0], %[t1]\n"
+      : [a0] "=&v"(a0), [t0] "=&v"(t0), [t1] "=&v"(t1)
+      : [c0] "v"(c0), [wx] "v"(w.x), [wy] "v"(w.y), [wz] "v"(w.z), [ww] "v"(w.w));
+}
 #undef CFP_W_ADD
 
 template <int NW>
@@ -316,6 +330,8 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
     }
   };
 
+  constexpr int NPRE = 4;  // table chunks of the next row read ahead
+  u32x4 wpre[NPRE];
   // One row; J = row mod 12.  GUARD: the block may end before its 12th row;
   // FIRST: the run's first block, whose rows before i0 are skipped and whose
   // first quad's loads were issued before the loop.
@@ -357,19 +373,28 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
       c3[g] = hi[1];
       acc[g] = kSat;
     }
-    // all sixteen table chunks of the row in flight at once
     const u32x4 *tb = sm.tb[(i >> 2) & 1][u];
-    // The fix-up pass holds the checkpoint row besides, so it loads the row's
-    // table chunks in two halves to stay within the register file.
+    // With two searches a wave has the registers for all sixteen table chunks
+    // of a row; with one (sixteen waves per workgroup) it loads them in two
+    // halves, and outside the first block the first half of rows 1..3 of a
+    // quad is read during the previous row's normalisation (PRE).
     constexpr int WH = (MODE == kWSpec && G == 2) ? 16 : 8;
+    constexpr bool PRE = WH < 16 && !FIRST && u != 0;
     u32x4 w[16];
     // Candidates of every predecessor for the searches X (and Y): two
     // searches share each table chunk read.
 #define CFP_CH2(C, cc_) cand4_g2<4 * ((cc_) & 3), ((cc_) & 3) == 0>(acc[0], acc[G - 1], C[0], C[G - 1], w[cc_]);
-#define CFP_CH1(X, C, cc_) cand4_g1<4 * ((cc_) & 3), ((cc_) & 3) == 0>(acc[X], C[X], w[cc_]);
+#define CFP_CH1(X, C, cc_)                                                  \
+  if constexpr ((cc_) == 0) cand4_g1_first(acc[X], C[X], w[0]);             \
+  else cand4_g1<4 * ((cc_) & 3), ((cc_) & 3) == 0>(acc[X], C[X], w[cc_]);
 #define CFP_ROW(CH, ...)                                                                   \
   {                                                                                        \
-    _Pragma("unroll") for (int cc_ = 0; cc_ < WH; ++cc_) w[cc_] = tb[cc_ * 64 + lane];     \
+    if constexpr (PRE) {                                                                   \
+      _Pragma("unroll") for (int cc_ = 0; cc_ < NPRE; ++cc_) w[cc_] = wpre[cc_];           \
+      _Pragma("unroll") for (int cc_ = NPRE; cc_ < WH; ++cc_) w[cc_] = tb[cc_ * 64 + lane]; \
+    } else {                                                                               \
+      _Pragma("unroll") for (int cc_ = 0; cc_ < WH; ++cc_) w[cc_] = tb[cc_ * 64 + lane];   \
+    }                                                                                      \
     CH(__VA_ARGS__ c0, 0) CH(__VA_ARGS__ c0, 1) CH(__VA_ARGS__ c0, 2) CH(__VA_ARGS__ c0, 3) \
     CH(__VA_ARGS__ c1, 4) CH(__VA_ARGS__ c1, 5) CH(__VA_ARGS__ c1, 6) CH(__VA_ARGS__ c1, 7) \
     if constexpr (WH < 16) {                                                               \
@@ -377,6 +402,9 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
     }                                                                                      \
     CH(__VA_ARGS__ c2, 8) CH(__VA_ARGS__ c2, 9) CH(__VA_ARGS__ c2, 10) CH(__VA_ARGS__ c2, 11) \
     CH(__VA_ARGS__ c3, 12) CH(__VA_ARGS__ c3, 13) CH(__VA_ARGS__ c3, 14) CH(__VA_ARGS__ c3, 15) \
+    if constexpr (WH < 16 && !FIRST && u != 3) {                                           \
+      _Pragma("unroll") for (int cc_ = 0; cc_ < NPRE; ++cc_) wpre[cc_] = tb[kWTable16 + cc_ * 64 + lane]; \
+    }                                                                                      \
   }
     if constexpr (G == 2) CFP_ROW(CFP_CH2)
     else CFP_ROW(CFP_CH1, 0,)
@@ -543,7 +571,9 @@ __global__ __launch_bounds__(64 * kWFixWaves) void chain_wave_fix_kernel(WaveArg
       acc[g] = kSat;
     }
 #define CFP_CH2(C, cc_) cand4_g2<4 * ((cc_) & 3), ((cc_) & 3) == 0>(acc[0], acc[1], C[0], C[1], w[cc_]);
-#define CFP_CH1(X, C, cc_) cand4_g1<4 * ((cc_) & 3), ((cc_) & 3) == 0>(acc[X], C[X], w[cc_]);
+#define CFP_CH1(X, C, cc_)                                                  \
+  if constexpr ((cc_) == 0) cand4_g1_first(acc[X], C[X], w[0]);             \
+  else cand4_g1<4 * ((cc_) & 3), ((cc_) & 3) == 0>(acc[X], C[X], w[cc_]);
 #define CFP_ROW(CH, ...)                                                                        \
   {                                                                                             \
     CH(__VA_ARGS__ c0, 0) CH(__VA_ARGS__ c0, 1) CH(__VA_ARGS__ c0, 2) CH(__VA_ARGS__ c0, 3)     \
