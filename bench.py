@@ -40,7 +40,7 @@ DEFAULT_CONFIG = "chain_gpt_n1152_k64"
 KERNELS = {
     "chain_gpt_n24_k16": ("chain_fwd_res_kernel<16,12>", ["chain_fwd_res.hip", "res_common.h"]),
     # speculative pass of the chunk-parallel search: it computes every step of every chain
-    "chain_gpt_n1152_k64": ("chain_wave_kernel<0, 12>", ["chain_wave.hip", "res_common.h"]),
+    "chain_gpt_n1152_k64": ("chain_wave_kernel<12>", ["chain_wave.hip", "res_common.h"]),
     "mem_llama_n288_k32": ("mem_fwd_kernel<32>", ["mem_fwd.hip", "res_common.h"]),
     "chain_wide_n512_k256": ("chain_fwd_splitw_kernel<256>", ["chain_fwd_split.hip", "chain_fwd_wide.hip"]),
     "scan_n4096_k512": ("scan_gemm_kernel", ["scan.hip"]),
@@ -51,21 +51,21 @@ COMMON_SOURCES = ["common.h", "cfp_internal.h", "../../include/cfp.h"]
 # HBM bytes per launch of the dominant kernel, from two rocprofv3 --pmc runs
 # of this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each scaled
 # by the factor that maps the counter onto the bytes of a plain 512 MiB copy
-# (bench.py --calibrate-copy: FETCH_SIZE reads 262159 KiB -> x2.000,
+# (bench.py --calibrate-copy: FETCH_SIZE reads 262167 KiB -> x2.000,
 # WRITE_SIZE reads 524288 KiB -> x1.000).  "sources" is sources_hash() of the
 # kernel when the counters were taken; a different hash means the kernel has
 # changed and the figure is withheld.
-FETCH_SCALE, WRITE_SCALE = 524288.0 / 262159.1, 524288.0 / 524288.0
+FETCH_SCALE, WRITE_SCALE = 524288.0 / 262166.6, 524288.0 / 524288.0
 TRAFFIC = {
-    "chain_gpt_n24_k16": {"fetch_kib": 18.4, "write_kib": 0.5, "sources": "8f49cac9c912f637"},
-    "chain_gpt_n1152_k64": {"fetch_kib": 37915.9, "write_kib": 18456.0, "sources": "5a97ee1ff90b424c"},
-    "mem_llama_n288_k32": {"fetch_kib": 60535.6, "write_kib": 239222.6, "sources": "d668d626f64cdbd7"},
-    "chain_wide_n512_k256": {"fetch_kib": 30233.4, "write_kib": 8182.0, "sources": "eb76c9ed03780d22"},
+    "chain_gpt_n24_k16": {"fetch_kib": 18.0, "write_kib": 0.5, "sources": "8f96d936c23286f2"},
+    "chain_gpt_n1152_k64": {"fetch_kib": 37981.2, "write_kib": 37514.8, "sources": "c32e87116e074150"},
+    "mem_llama_n288_k32": {"fetch_kib": 60508.5, "write_kib": 239152.8, "sources": "efe31c2ab53be227"},
+    "chain_wide_n512_k256": {"fetch_kib": 151586.5, "write_kib": 73587.7, "sources": "95027697bdce3992"},
     # mean over the 12 matrix-product launches of one forward call
-    "scan_n4096_k512": {"fetch_kib": 3038953.7, "write_kib": 1398442.5, "sources": "de7227e316558ba4"},
-    "seg_gpt_n96_k81": {"fetch_kib": 3922.7, "write_kib": 1936.0, "sources": "db3445394db6f79e"},
+    "scan_n4096_k512": {"fetch_kib": 3033234.8, "write_kib": 1398442.5, "sources": "c0b783da46bf748c"},
+    "seg_gpt_n96_k81": {"fetch_kib": 3922.7, "write_kib": 1936.0, "sources": "a910a0e94a0c4a1f"},
     # the memory workload run as a budget frontier (every chunk of every search active)
-    "mem_llama_n288_k32:frontier": {"fetch_kib": 78399.6, "write_kib": 307886.5, "sources": "30876301e6c50782"},
+    "mem_llama_n288_k32:frontier": {"fetch_kib": 78358.9, "write_kib": 307895.3, "sources": "efe31c2ab53be227"},
 }
 
 
