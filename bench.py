@@ -42,7 +42,8 @@ KERNELS = {
     # speculative pass of the chunk-parallel search: it computes every step of every chain
     "chain_gpt_n1152_k64": ("chain_wave_kernel<12>", ["chain_wave.hip", "res_common.h"]),
     "mem_llama_n288_k32": ("mem_fwd_kernel<32>", ["mem_fwd.hip", "res_common.h"]),
-    "chain_wide_n512_k256": ("chain_fwd_splitw_kernel<256>", ["chain_fwd_split.hip", "chain_fwd_wide.hip"]),
+    # speculative pass of the chunk-parallel search
+    "chain_wide_n512_k256": ("chain_cw_kernel<0>", ["chain_cw.hip", "chain_fwd_wide.hip"]),
     "scan_n4096_k512": ("scan_gemm_kernel", ["scan.hip"]),
     "seg_gpt_n96_k81": ("seg_fwd_kernel<2>", ["seg_fwd.hip"]),
 }

@@ -50,6 +50,10 @@ WsLayout layout(int variant, int n, int k, int batch, int n_mem, int n_tables) {
     L.wave = off;
     off = align_up(off + wave_region_bytes(n, k, n_tables, batch));
   }
+  if (variant == CFP_V_CHAIN && chain_cw_supported(n, k, batch)) {
+    L.cw = off;
+    off = align_up(off + cw_region_bytes(n, k, n_tables, batch));
+  }
   if (variant == CFP_V_SCAN) {
     L.scan = off;
     L.scan_bytes = scan_region_bytes(n, k, batch);
@@ -173,6 +177,9 @@ int cfp_dp_chain(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t *op
   if (chain_wave_supported(d->n_blocks, d->k, d->n_tables, d->batch))
     e = launch_chain_wave(*d, (const int32_t *)(w + L.redge), w + L.wave, w + L.table,
                           (SearchResult *)(w + L.result), hdr, opt, status, st);
+  else if (chain_cw_supported(d->n_blocks, d->k, d->batch))
+    e = launch_chain_cw(*d, (const int32_t *)(w + L.redge), w + L.cw, w + L.table, (SearchResult *)(w + L.result),
+                        hdr, opt, status, st);
   else if (chain_fwd_split_supported(d->k, d->n_tables, d->batch))
     e = launch_chain_fwd_split(*d, (const int32_t *)(w + L.redge), w + L.split, (uint32_t *)(w + L.wide),
                                w + L.table, (SearchResult *)(w + L.result), hdr, opt, status, st);

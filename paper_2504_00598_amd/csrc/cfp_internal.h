@@ -53,6 +53,7 @@ struct WsLayout {
   size_t wide = 0;     // chain variant, K > 64: packed tables and cost-row minima
   size_t split = 0;    // chain variant, K > 64: exchange slots and flags of the split kernel
   size_t wave = 0;     // chain variant, 32 < K <= 64 on long chains: packed tables, chunk records, checkpoints
+  size_t cw = 0;       // chain variant, 128 < K <= 256 on long chains: packed tables, chunk records, checkpoints
   size_t scan = 0;     // scan variant: start of its private region
   size_t scan_bytes = 0;
   size_t total = 0;
@@ -77,6 +78,10 @@ size_t wave_region_bytes(int n, int k, int n_tables, int batch);
 hipError_t launch_chain_wave(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *region, uint8_t *table,
                              SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
                              hipStream_t st);
+bool chain_cw_supported(int n, int k, int batch);
+size_t cw_region_bytes(int n, int k, int n_tables, int batch);
+hipError_t launch_chain_cw(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *region, uint8_t *table,
+                           SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st);
 bool chain_fwd_split_supported(int k, int n_tables, int batch);
 size_t split_region_bytes(int k, int batch);
 hipError_t launch_chain_fwd_split(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *region, uint32_t *rpk,

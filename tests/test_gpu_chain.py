@@ -239,3 +239,65 @@ def test_chunked_ties_and_statuses():
     opt, st, plan = run_chain(cost, rtab, redge)
     assert st[9] == CFP_ST_BADINPUT and opt[9] == np.iinfo(np.int64).max and (plan[9] == -1).all()
     assert st[5] != 0 and (st[np.r_[0:5, 6:9, 10:70]] == 0).all()
+
+
+# 128 < K <= 256 on long chains (at least 32 blocks) runs chunk-parallel as well, with two
+# chains per workgroup sharing each streamed table word.  Same requirement: the oracle's
+# answer whatever the rows do.
+
+@pytest.mark.parametrize("N,K,B", [(32, 256, 1), (33, 129, 2), (100, 200, 3), (513, 256, 64), (1000, 255, 5),
+                                   (257, 160, 64), (64, 256, 129), (81, 256, 2)])
+def test_chunked_wide_shapes(N, K, B):
+    """Ragged batches (an odd last search), ragged last chunks, K below 256, one-row chunks."""
+    need_gpu()
+    from paper_2504_00598_amd import cfp_r_limit
+    rhi = min(10_000_000, cfp_r_limit(0, K))
+    cost, rtab, redge = rand_case([44, N, K, B], B, N, K, 12, 10_000, 10_000_000, rlo=10_000, rhi=rhi)
+    if N % 2:
+        redge = (np.arange(N) % 12).astype(np.int32)
+    say("chunked wide shape", N, K, B)
+    assert_chain_parity(cost, rtab, redge, f"chunked wide N={N} K={K} B={B}")
+
+
+@pytest.mark.parametrize("K,B", [(256, 3), (200, 8)])
+def test_chunked_wide_rows_never_meet(K, B):
+    """Every chunk misses its checkpoints: the final pass reruns the chains."""
+    need_gpu()
+    from paper_2504_00598_amd import cfp_r_limit
+    rs = np.random.default_rng([45, K, B])
+    N = 300
+    cost = rs.integers(0, 50, size=(B, N, K)).astype(np.int32)
+    rtab = _no_switch_tables(rs, 12, K, cfp_r_limit(0, K))
+    redge = (np.arange(N) % 12).astype(np.int32)
+    say("chunked wide, no convergence", K, B)
+    assert_chain_parity(cost, rtab, redge, f"wide never meet K={K} B={B}")
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_chunked_wide_some_chunks_meet(seed):
+    """Zero tables on a few edges make some chunks meet and others not, in a seeded pattern."""
+    need_gpu()
+    from paper_2504_00598_amd import cfp_r_limit
+    rs = np.random.default_rng([46, seed])
+    K, B, N = 256, 6, 600
+    cost = rs.integers(0, 1000, size=(B, N, K)).astype(np.int32)
+    rtab = _no_switch_tables(rs, 3, K, cfp_r_limit(0, K))
+    rtab[2] = 0
+    redge = rs.integers(0, 2, size=N).astype(np.int32)
+    resets = rs.choice(np.arange(1, N), size=int(rs.integers(1, 6)), replace=False)
+    redge[resets] = 2
+    say("chunked wide, partial convergence", seed, sorted(resets.tolist()))
+    assert_chain_parity(cost, rtab, redge, f"wide partial seed={seed}")
+
+
+def test_chunked_wide_ties_and_statuses():
+    """Tie-heavy values, unavailable strategies, an infeasible search and a negative cost."""
+    need_gpu()
+    from paper_2504_00598_amd import CFP_ST_BADINPUT
+    cost, rtab, redge = rand_case([47], 9, 200, 256, 5, 0, 3, inf_frac=0.1)
+    cost[4, 150, :] = INF   # infeasible search, in a late chunk
+    assert_chain_parity(cost, rtab, redge, "chunked wide ties")
+    cost[7, 60, 3] = -7     # a negative cost is rejected by the library
+    opt, st, plan = run_chain(cost, rtab, redge)
+    assert st[7] == CFP_ST_BADINPUT and opt[7] == np.iinfo(np.int64).max and (plan[7] == -1).all()
+    assert st[4] != 0 and st[6] == 0 and st[8] == 0 and (st[np.r_[0:4, 5:7]] == 0).all()
