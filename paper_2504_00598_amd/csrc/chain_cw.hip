@@ -15,19 +15,25 @@
 //      checkpoint has its true end row, and the rest of the chain is rerun from
 //      it.  The result is the sequential recurrence's bit for bit.
 //
-// One workgroup of 512 threads carries two chains (two searches of the same
-// chunk: every chain of a launch is at the same row, so both use the same
+// One workgroup of 512 threads carries four chains (four searches of the same
+// chunk: every chain of a launch is at the same row, so all use the same
 // table) and all KP = 256 states.  Thread tid = 8 q + g works for the states
-// 4q .. 4q+3 of both chains over the predecessors t = 32 g .. 32 g + 31.  Per
+// 4q .. 4q+3 of every chain over the predecessors t = 32 g .. 32 g + 31.  Per
 // step it reads its 32 x 4 packed words (R_e[t][s] << 8) | t of the edge's
-// table from the cache-resident array (each word serves both chains), in four
-// pieces of eight rows, each loaded one step ahead into its own registers, and
-// the predecessors' values from the previous row in LDS (broadcast reads).  A
-// candidate is a saturating add, and one unsigned minimum keeps the value and
-// the lowest predecessor.  The eight group minima of a state are combined by a
-// reduce-scatter over the eight lanes of the state quad (two quad_perm steps and
-// a half-mirror step, lanes of the upper half holding the complementary
-// indices), after which lane g holds chain g / 4, state 4q + ((g ^ 3 (g / 4)) % 4).
+// table from the cache-resident array (each word serves the four chains), in
+// four pieces of eight rows, each loaded one step ahead into its own registers,
+// and the predecessors' values from the previous rows in LDS (broadcast
+// reads).  A candidate is a saturating add, and one unsigned minimum keeps the
+// value and the lowest predecessor.  The eight group minima of a state are
+// combined by a reduce-scatter over the eight lanes of the state quad (two
+// quad_perm steps and a half-mirror step, lanes of the upper half holding the
+// complementary indices), after which lane g holds state
+// 4q + ((g ^ 3 (g / 4)) % 4) of chains g / 4 and 2 + g / 4.
+//
+// The table stream is what bounds a step: 256 KiB per workgroup and step,
+// which one CU takes in from L2 at about 14 bytes per clock (measured: the
+// step time does not change with the number of workgroups), hence four chains
+// per workgroup rather than two.
 //
 // Normalisation: x[s] = (m >> 8) + c[i][s]; the row is divided into the part
 // d = min_s x[s] (summed exactly, per chain) and Q[s] = min(x[s] - d, cap) << 8,
@@ -57,6 +63,8 @@ constexpr uint32_t kCX = 0xFFFFFFFFu;   // x of an unavailable or padding state
 constexpr int kCMaxChunks = 64;
 constexpr int kCMinRows = 16;           // least rows per chunk
 
+constexpr int kCG = 4;                  // chains per workgroup (searches of the same chunk)
+constexpr int kCH = kCG / 2;            // chains per thread after the reduce-scatter
 constexpr int kCSpec = 0, kCFix = 1, kCRepair = 2;
 
 struct CwRec {
@@ -78,15 +86,15 @@ struct CwArgs {
 };
 
 struct CwSmem {
-  uint32_t q[2][2][kCQS];  // rows [buffer][chain][state, padded]
-  uint32_t wm[kCWaves][2];  // wave minima of the new row, per chain
-  int32_t wd[kCWaves][2];   // fix-up: the wave found a state off the checkpoint, per chain
+  uint32_t q[2][kCG][kCQS];   // rows [buffer][chain][state, padded]
+  uint32_t wm[kCWaves][kCG];  // wave minima of the new row, per chain
+  int32_t wd[kCWaves][kCG];   // fix-up: the wave found a state off the checkpoint, per chain
 };
 
 __device__ __forceinline__ int qpad(int t) { return t + (t >> 5) * 4; }
 
-// min(keep, lane ^ 1's send) and min(keep, lane ^ 2's send) by quad_perm; the
-// half mirror pairs lane i with lane 7 - i of its eight.
+// min(keep, the partner lane's send): quad_perm partners lane ^ 1 and lane ^ 2;
+// the half mirror pairs lane i with lane 7 - i of its eight.
 template <int CTRL>
 __device__ __forceinline__ uint32_t min_dpp(uint32_t keep, uint32_t send) {
   return umin(keep, (uint32_t)__builtin_amdgcn_mov_dpp((int)send, CTRL, 0xF, 0xF, true));
@@ -105,35 +113,47 @@ __device__ __forceinline__ uint32_t cw_wave_min(uint32_t x) {
   return umin(r[0], r[1]);
 }
 
-// Runs rows [r0 (+1 in the speculative pass), r1] of the two chains b0, b1 of
-// the workgroup (real: valid0, valid1).  Speculative: the start row is row r0
-// from its costs; checkpoints are written.  Fix-up: the start row (row r0 - 1)
-// is start[c]; stops at the first quad end where both chains meet their
-// checkpoints.  Repair: like fix-up without checkpoints.
+// State of the workgroup's chains as seen by one thread.  After the
+// reduce-scatter a thread holds, for its state s, the chains 2h + f2,
+// h = 0 .. kCG/2 - 1 (f2 = bit 2 of its group).
 template <int MODE>
 struct CwChains {
-  uint32_t x;          // the lane's (chain, state) value of the current row, normalised and shifted
-  uint64_t dsum[2];    // offset sums since the start row
-  int conv[2];         // fix-up: quad of the meeting checkpoint, -1 before
-  uint64_t dconv[2];   // fix-up: dsum at that checkpoint
-  uint32_t flags[2];   // speculative, per chain: bit 0 a negative cost, bit 1 a row with no available strategy
+  uint32_t x[kCH];      // the thread's values of the current row, normalised and shifted
+  uint64_t dsum[kCG];   // offset sums since the start row (uniform)
+  int conv[kCG];        // fix-up: quad of the meeting checkpoint, -1 before
+  uint64_t dconv[kCG];  // fix-up: dsum at that checkpoint
+  uint32_t flags[kCG];  // speculative: bit 0 a negative cost, bit 1 a row with no available strategy
 };
 
+// Runs rows [r0 (+1 in the speculative pass), r1] of the workgroup's chains
+// (searches bs[c], real where valid[c]).  Speculative: the start row is row r0
+// from its costs; checkpoints are written.  Fix-up: the start row (row r0 - 1)
+// is start[c]; stops at the first quad end where every real chain has met its
+// checkpoint.  Repair: like fix-up without checkpoints.
 template <int MODE>
-__device__ __forceinline__ void cw_run(const CwArgs &a, int b0, int b1, bool valid0, bool valid1, int r0, int r1,
-                                       const uint32_t *start0, const uint32_t *start1, CwSmem &sm,
-                                       CwChains<MODE> &ch) {
+__device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const bool *valid, int r0, int r1,
+                                       const uint32_t *const *start, CwSmem &sm, CwChains<MODE> &ch) {
   const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int qd = tid >> 3, g = tid & 7;  // state quad, predecessor group
   const int N = a.N, K = a.K;
-  // the lane's (chain, state) after the reduce-scatter
-  const int mc = g >> 2;
-  const int ms = 4 * qd + ((g ^ (mc ? 3 : 0)) & 3);
-  const int mb = mc ? b1 : b0;
-  const bool mvalid = mc ? valid1 : valid0;
+  // the thread's state and chains after the reduce-scatter
+  const bool f0 = ((g ^ (g >> 2)) & 1) != 0, f1 = (((g >> 1) ^ (g >> 2)) & 1) != 0, f2 = (g >> 2) != 0;
+  const int ms = 4 * qd + (f1 ? 2 : 0) + (f0 ? 1 : 0);
   const bool sin = ms < K;
-  const int32_t *cbase = a.cost + (size_t)mb * N * K + min(ms, K - 1);
-  uint8_t *tbase = a.table + (size_t)mb * N * K + ms;
+  int hc[kCH];  // chain of pair h
+  bool hv[kCH];
+  const int32_t *cbase[kCH];
+  uint8_t *tbase[kCH];
+  uint32_t *ckb[kCH];
+#pragma unroll
+  for (int h = 0; h < kCH; ++h) {
+    hc[h] = 2 * h + (f2 ? 1 : 0);
+    const int b = f2 ? bs[2 * h + 1] : bs[2 * h];
+    hv[h] = f2 ? valid[2 * h + 1] : valid[2 * h];
+    cbase[h] = a.cost + (size_t)b * N * K + min(ms, K - 1);
+    tbase[h] = a.table + (size_t)b * N * K + ms;
+    ckb[h] = a.ckrow + (size_t)b * a.nq * kCKP + ms;
+  }
   auto edge = [&](int row) __attribute__((always_inline)) {
     return __builtin_amdgcn_readfirstlane(a.redge[row]);
   };
@@ -148,207 +168,249 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, int b0, int b1, bool val
 #pragma unroll
     for (int j = 0; j < kCRows; ++j) tb[piece][j] = *(const u32x4 *)(tab + j * kCKP);
   };
-
-  // Start row.
-  ch.flags[0] = ch.flags[1] = 0;
-  ch.conv[0] = ch.conv[1] = -1;
-  ch.dconv[0] = ch.dconv[1] = 0;
-  uint32_t cor = 0;
-  int cur = 0;
-  if (MODE == kCSpec) {
-    const uint32_t cv = (uint32_t)cbase[(size_t)r0 * K];
-    cor = cv;
-    const uint32_t x = (sin && cv != (uint32_t)CFP_COST_INF) ? cv : kCX;
-    const uint32_t w0 = cw_wave_min(mc == 0 ? x : kCX), w1 = cw_wave_min(mc == 1 ? x : kCX);
-    if (lane == 0) {
-      sm.wm[wid][0] = w0;
-      sm.wm[wid][1] = w1;
+  // Row minima of every chain from the threads' values: wave minima to LDS,
+  // one barrier, then the minimum over the waves (uniform).
+  auto row_min = [&](const uint32_t(&x)[kCH], uint32_t(&d)[kCG]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int c = 0; c < kCG; ++c) {
+      const uint32_t w = cw_wave_min(((c & 1) == (f2 ? 1 : 0)) ? x[c >> 1] : kCX);
+      if (lane == 0) sm.wm[wid][c] = w;
     }
     __syncthreads();
-    uint32_t d0 = sm.wm[0][0], d1 = sm.wm[0][1];
 #pragma unroll
-    for (int w = 1; w < kCWaves; ++w) {
-      d0 = umin(d0, sm.wm[w][0]);
-      d1 = umin(d1, sm.wm[w][1]);
+    for (int c = 0; c < kCG; ++c) {
+      uint32_t m = sm.wm[0][c];
+#pragma unroll
+      for (int w = 1; w < kCWaves; ++w) m = umin(m, sm.wm[w][c]);
+      d[c] = __builtin_amdgcn_readfirstlane(m);
     }
-    const uint32_t d = mc ? d1 : d0;
-    if (d0 == kCX) ch.flags[0] |= 2;
-    if (d1 == kCX) ch.flags[1] |= 2;
-    ch.x = umin(x - d, kCCap) << kCBits;
-    ch.dsum[0] = d0;
-    ch.dsum[1] = d1;
-    sm.q[0][mc][qpad(ms)] = ch.x;
-    if (i0 > r1 && mvalid) {  // a run of one row: the start row is its checkpoint
-      (a.ckrow + ((size_t)mb * a.nq + r0 / 4) * kCKP)[ms] = ch.x;
-      if (tid == 0 && valid0) a.dck[(size_t)b0 * a.nq + r0 / 4] = (int64_t)ch.dsum[0];
-      if (tid == 4 && valid1) a.dck[(size_t)b1 * a.nq + r0 / 4] = (int64_t)ch.dsum[1];
+  };
+
+  // Start row.
+#pragma unroll
+  for (int c = 0; c < kCG; ++c) {
+    ch.flags[c] = 0;
+    ch.conv[c] = -1;
+    ch.dconv[c] = 0;
+    ch.dsum[c] = 0;
+  }
+  uint32_t cor[kCH];
+  int cur = 0;
+  if (MODE == kCSpec) {
+    uint32_t x[kCH], d[kCG];
+#pragma unroll
+    for (int h = 0; h < kCH; ++h) {
+      const uint32_t cv = (uint32_t)cbase[h][(size_t)r0 * K];
+      cor[h] = cv;
+      x[h] = (sin && cv != (uint32_t)CFP_COST_INF) ? cv : kCX;
+    }
+    row_min(x, d);
+#pragma unroll
+    for (int c = 0; c < kCG; ++c) {
+      if (d[c] == kCX) ch.flags[c] |= 2;
+      ch.dsum[c] = d[c];
+    }
+#pragma unroll
+    for (int h = 0; h < kCH; ++h) {
+      ch.x[h] = umin(x[h] - (f2 ? d[2 * h + 1] : d[2 * h]), kCCap) << kCBits;
+      sm.q[0][hc[h]][qpad(ms)] = ch.x[h];
+    }
+    if (i0 > r1) {  // a run of one row: the start row is its checkpoint
+#pragma unroll
+      for (int h = 0; h < kCH; ++h)
+        if (hv[h]) ckb[h][(size_t)(r0 / 4) * kCKP] = ch.x[h];
+#pragma unroll
+      for (int c = 0; c < kCG; ++c)
+        if (tid == c && valid[c]) a.dck[(size_t)bs[c] * a.nq + r0 / 4] = (int64_t)ch.dsum[c];
     }
   } else {
-    ch.x = (mc ? start1 : start0)[ms];
-    ch.dsum[0] = ch.dsum[1] = 0;
-    sm.q[0][mc][qpad(ms)] = ch.x;
+#pragma unroll
+    for (int h = 0; h < kCH; ++h) {
+      ch.x[h] = (f2 ? start[2 * h + 1] : start[2 * h])[ms];
+      sm.q[0][hc[h]][qpad(ms)] = ch.x[h];
+      cor[h] = 0;
+    }
   }
   auto negative_costs = [&]() __attribute__((always_inline)) {
-    if (__syncthreads_or(mc == 0 && (cor >> 31))) ch.flags[0] |= 1;
-    if (__syncthreads_or(mc == 1 && (cor >> 31))) ch.flags[1] |= 1;
+#pragma unroll
+    for (int c = 0; c < kCG; ++c)
+      if (__syncthreads_or(((c & 1) == (f2 ? 1 : 0)) && (cor[c >> 1] >> 31))) ch.flags[c] |= 1;
   };
-  if (i0 > r1) {  // nothing to compute (a run of one row)
+  if (i0 > r1) {
     if (MODE == kCSpec) negative_costs();
     return;
   }
 #pragma unroll
   for (int k = 0; k < kCPieces; ++k) tload(k, i0);
-  uint32_t c1 = (uint32_t)cbase[(size_t)i0 * K];                 // cost of the next row
-  uint32_t c2 = (uint32_t)cbase[(size_t)min(i0 + 1, r1) * K];    // and of the one after
-  uint32_t ckv = 0;
-  if (MODE == kCFix) ckv = (mc ? a.ckrow + (size_t)b1 * a.nq * kCKP : a.ckrow + (size_t)b0 * a.nq * kCKP)[(size_t)(i0 >> 2) * kCKP + ms];
+  uint32_t c1[kCH], c2[kCH], ckv[kCH];  // costs of the next row and of the one after; checkpoint
+#pragma unroll
+  for (int h = 0; h < kCH; ++h) {
+    c1[h] = (uint32_t)cbase[h][(size_t)i0 * K];
+    c2[h] = (uint32_t)cbase[h][(size_t)min(i0 + 1, r1) * K];
+    ckv[h] = 0;
+    if (MODE == kCFix) ckv[h] = ckb[h][(size_t)(i0 >> 2) * kCKP];
+  }
   __syncthreads();
 
   for (int i = i0; i <= r1; ++i) {
     const int nxt = cur ^ 1;
-    const uint32_t *q0 = &sm.q[cur][0][qpad(32 * g)];
-    const uint32_t *q1 = &sm.q[cur][1][qpad(32 * g)];
-    uint32_t acc[2][4];
+    uint32_t acc[kCG][4];
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+    for (int c = 0; c < kCG; ++c)
 #pragma unroll
       for (int u = 0; u < 4; ++u) acc[c][u] = kSat;
     const int inext = min(i + 1, r1);
 #pragma unroll
     for (int k = 0; k < kCPieces; ++k) {
-      const u32x4 qa0 = *(const u32x4 *)(q0 + 8 * k), qb0 = *(const u32x4 *)(q0 + 8 * k + 4);
-      const u32x4 qa1 = *(const u32x4 *)(q1 + 8 * k), qb1 = *(const u32x4 *)(q1 + 8 * k + 4);
-      const uint32_t v0[8] = {qa0.x, qa0.y, qa0.z, qa0.w, qb0.x, qb0.y, qb0.z, qb0.w};
-      const uint32_t v1[8] = {qa1.x, qa1.y, qa1.z, qa1.w, qb1.x, qb1.y, qb1.z, qb1.w};
+      uint32_t v[kCG][kCRows];  // the predecessors' values of this piece, per chain
+#pragma unroll
+      for (int c = 0; c < kCG; ++c) {
+        const uint32_t *qc = &sm.q[cur][c][qpad(32 * g) + 8 * k];
+        const u32x4 lo = *(const u32x4 *)qc, hi = *(const u32x4 *)(qc + 4);
+        v[c][0] = lo.x; v[c][1] = lo.y; v[c][2] = lo.z; v[c][3] = lo.w;
+        v[c][4] = hi.x; v[c][5] = hi.y; v[c][6] = hi.z; v[c][7] = hi.w;
+      }
 #pragma unroll
       for (int j = 0; j < kCRows; j += 2) {
         const u32x4 w = tb[k][j], y = tb[k][j + 1];
-        acc[0][0] = umin(umin(acc[0][0], sat_add(v0[j], w.x)), sat_add(v0[j + 1], y.x));
-        acc[0][1] = umin(umin(acc[0][1], sat_add(v0[j], w.y)), sat_add(v0[j + 1], y.y));
-        acc[0][2] = umin(umin(acc[0][2], sat_add(v0[j], w.z)), sat_add(v0[j + 1], y.z));
-        acc[0][3] = umin(umin(acc[0][3], sat_add(v0[j], w.w)), sat_add(v0[j + 1], y.w));
-        acc[1][0] = umin(umin(acc[1][0], sat_add(v1[j], w.x)), sat_add(v1[j + 1], y.x));
-        acc[1][1] = umin(umin(acc[1][1], sat_add(v1[j], w.y)), sat_add(v1[j + 1], y.y));
-        acc[1][2] = umin(umin(acc[1][2], sat_add(v1[j], w.z)), sat_add(v1[j + 1], y.z));
-        acc[1][3] = umin(umin(acc[1][3], sat_add(v1[j], w.w)), sat_add(v1[j + 1], y.w));
+#pragma unroll
+        for (int c = 0; c < kCG; ++c) {
+          acc[c][0] = umin(umin(acc[c][0], sat_add(v[c][j], w.x)), sat_add(v[c][j + 1], y.x));
+          acc[c][1] = umin(umin(acc[c][1], sat_add(v[c][j], w.y)), sat_add(v[c][j + 1], y.y));
+          acc[c][2] = umin(umin(acc[c][2], sat_add(v[c][j], w.z)), sat_add(v[c][j + 1], y.z));
+          acc[c][3] = umin(umin(acc[c][3], sat_add(v[c][j], w.w)), sat_add(v[c][j + 1], y.w));
+        }
       }
       tload(k, inext);  // this piece of the next row into the registers just consumed
     }
     // Reduce-scatter over the eight groups of the state quad.  Value index
     // k = 4 c + u; lane bits (b2 b1 b0) = g.  Step 1 keeps k0 = b0 ^ b2, step 2
     // k1 = b1 ^ b2 (quad_perm partners), step 3 k2 = b2 (half mirror: lane
-    // 7 - g, whose kept k0, k1 equal this lane's).
-    const bool f0 = ((g ^ (g >> 2)) & 1) != 0, f1 = (((g >> 1) ^ (g >> 2)) & 1) != 0, f2 = (g >> 2) != 0;
-    uint32_t r1v[4];
+    // 7 - g, whose kept k0, k1 equal this lane's); k3 .. remain (pairs h).
+    uint32_t r1v[2 * kCG];
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {  // pairs (k, k + 1) with k = 2p: k0 = 0 / 1
+    for (int p = 0; p < 2 * kCG; ++p) {
       const uint32_t lo = acc[p >> 1][(p & 1) * 2], hi = acc[p >> 1][(p & 1) * 2 + 1];
       r1v[p] = min_dpp<kDppXor1>(f0 ? hi : lo, f0 ? lo : hi);
     }
-    uint32_t r2v[2];
+    uint32_t r2v[kCG];
 #pragma unroll
-    for (int p = 0; p < 2; ++p) r2v[p] = min_dpp<kDppXor2>(f1 ? r1v[2 * p + 1] : r1v[2 * p], f1 ? r1v[2 * p] : r1v[2 * p + 1]);
-    const uint32_t m = min_dpp<kDppHalfMirror>(f2 ? r2v[1] : r2v[0], f2 ? r2v[0] : r2v[1]);
+    for (int p = 0; p < kCG; ++p)
+      r2v[p] = min_dpp<kDppXor2>(f1 ? r1v[2 * p + 1] : r1v[2 * p], f1 ? r1v[2 * p] : r1v[2 * p + 1]);
+    uint32_t m[kCH];
+#pragma unroll
+    for (int h = 0; h < kCH; ++h)
+      m[h] = min_dpp<kDppHalfMirror>(f2 ? r2v[2 * h + 1] : r2v[2 * h], f2 ? r2v[2 * h] : r2v[2 * h + 1]);
 
-    // New row: the lane's (chain, state).
-    const uint32_t cv = c1;
-    c1 = c2;
-    c2 = (uint32_t)cbase[(size_t)min(i + 2, r1) * K];
-    if (MODE == kCSpec) cor |= cv;
-    const bool avail = sin && cv != (uint32_t)CFP_COST_INF;
-    const uint32_t x = avail ? (m >> kCBits) + cv : kCX;
-    if (sin && mvalid) tbase[(size_t)i * K] = (uint8_t)(m & (kCKP - 1));
-    const uint32_t w0 = cw_wave_min(mc == 0 ? x : kCX), w1 = cw_wave_min(mc == 1 ? x : kCX);
-    if (lane == 0) {
-      sm.wm[wid][0] = w0;
-      sm.wm[wid][1] = w1;
-    }
-    __syncthreads();
-    uint32_t d0 = sm.wm[0][0], d1 = sm.wm[0][1];
+    // New row: the thread's pairs.
+    uint32_t x[kCH];
 #pragma unroll
-    for (int w = 1; w < kCWaves; ++w) {
-      d0 = umin(d0, sm.wm[w][0]);
-      d1 = umin(d1, sm.wm[w][1]);
+    for (int h = 0; h < kCH; ++h) {
+      const uint32_t cv = c1[h];
+      c1[h] = c2[h];
+      c2[h] = (uint32_t)cbase[h][(size_t)min(i + 2, r1) * K];
+      if (MODE == kCSpec) cor[h] |= cv;
+      x[h] = (sin && cv != (uint32_t)CFP_COST_INF) ? (m[h] >> kCBits) + cv : kCX;
+      if (sin && hv[h]) tbase[h][(size_t)i * K] = (uint8_t)(m[h] & (kCKP - 1));
     }
-    d0 = __builtin_amdgcn_readfirstlane(d0);
-    d1 = __builtin_amdgcn_readfirstlane(d1);
-    if (MODE == kCSpec && d0 == kCX) ch.flags[0] |= 2;
-    if (MODE == kCSpec && d1 == kCX) ch.flags[1] |= 2;
-    const uint32_t d = mc ? d1 : d0;
-    ch.x = umin(x - d, kCCap) << kCBits;
-    ch.dsum[0] += d0;
-    ch.dsum[1] += d1;
-    sm.q[nxt][mc][qpad(ms)] = ch.x;
+    uint32_t d[kCG];
+    row_min(x, d);
+#pragma unroll
+    for (int c = 0; c < kCG; ++c) {
+      if (MODE == kCSpec && d[c] == kCX) ch.flags[c] |= 2;
+      ch.dsum[c] += d[c];
+    }
+#pragma unroll
+    for (int h = 0; h < kCH; ++h) {
+      ch.x[h] = umin(x[h] - (f2 ? d[2 * h + 1] : d[2 * h]), kCCap) << kCBits;
+      sm.q[nxt][hc[h]][qpad(ms)] = ch.x[h];
+    }
     const bool qend = (i & 3) == 3 || i == r1;
     if (qend) {
       const int q = i >> 2;
       if (MODE == kCSpec) {
-        if (mvalid) {
-          (a.ckrow + ((size_t)mb * a.nq + q) * kCKP)[ms] = ch.x;
-          if (tid == 0 && valid0) a.dck[(size_t)b0 * a.nq + q] = (int64_t)ch.dsum[0];
-          if (tid == 4 && valid1) a.dck[(size_t)b1 * a.nq + q] = (int64_t)ch.dsum[1];
-        }
+#pragma unroll
+        for (int h = 0; h < kCH; ++h)
+          if (hv[h]) ckb[h][(size_t)q * kCKP] = ch.x[h];
+#pragma unroll
+        for (int c = 0; c < kCG; ++c)
+          if (tid == c && valid[c]) a.dck[(size_t)bs[c] * a.nq + q] = (int64_t)ch.dsum[c];
       }
       if (MODE == kCFix) {
-        const uint64_t off0 = __ballot(mc == 0 && ch.x != ckv), off1 = __ballot(mc == 1 && ch.x != ckv);
-        if (lane == 0) {
-          sm.wd[wid][0] = off0 != 0;
-          sm.wd[wid][1] = off1 != 0;
+#pragma unroll
+        for (int c = 0; c < kCG; ++c) {
+          const uint64_t off = __ballot(((c & 1) == (f2 ? 1 : 0)) && ch.x[c >> 1] != ckv[c >> 1]);
+          if (lane == 0) sm.wd[wid][c] = off != 0;
         }
-        if (i < r1) ckv = (mc ? a.ckrow + (size_t)b1 * a.nq * kCKP : a.ckrow + (size_t)b0 * a.nq * kCKP)[(size_t)(q + 1) * kCKP + ms];
+        if (i < r1) {
+#pragma unroll
+          for (int h = 0; h < kCH; ++h) ckv[h] = ckb[h][(size_t)(q + 1) * kCKP];
+        }
       }
     }
     __syncthreads();
     cur = nxt;
     if (MODE == kCFix && qend) {
-      bool same0 = true, same1 = true;
-#pragma unroll
-      for (int w = 0; w < kCWaves; ++w) {
-        same0 = same0 && !sm.wd[w][0];
-        same1 = same1 && !sm.wd[w][1];
-      }
       const int q = i >> 2;
-      if (ch.conv[0] < 0 && same0) {
-        ch.conv[0] = q;
-        ch.dconv[0] = ch.dsum[0];
+      bool all = true;
+#pragma unroll
+      for (int c = 0; c < kCG; ++c) {
+        bool same = true;
+#pragma unroll
+        for (int w = 0; w < kCWaves; ++w) same = same && !sm.wd[w][c];
+        if (ch.conv[c] < 0 && same) {
+          ch.conv[c] = q;
+          ch.dconv[c] = ch.dsum[c];
+        }
+        all = all && (ch.conv[c] >= 0 || !valid[c]);
       }
-      if (ch.conv[1] < 0 && same1) {
-        ch.conv[1] = q;
-        ch.dconv[1] = ch.dsum[1];
-      }
-      if ((ch.conv[0] >= 0 || !valid0) && (ch.conv[1] >= 0 || !valid1)) break;
+      if (all) break;
     }
   }
   if (MODE == kCSpec) negative_costs();
 }
 
-// Speculative (MODE kCSpec, grid (ceil(B/2), P)) and fix-up (kCFix, grid
-// (ceil(B/2), P-1)) passes.
+// Speculative (MODE kCSpec, grid (ceil(B/kCG), P)) and fix-up (kCFix, grid
+// (ceil(B/kCG), P-1)) passes.
 template <int MODE>
 __global__ __launch_bounds__(kCThreads, 1) void chain_cw_kernel(CwArgs a) {
   __shared__ __align__(16) CwSmem sm;
-  const int b0 = 2 * blockIdx.x, b1 = min(b0 + 1, a.B - 1);
-  const bool valid1 = b0 + 1 < a.B;
+  int bs[kCG];
+  bool valid[kCG];
+#pragma unroll
+  for (int c = 0; c < kCG; ++c) {
+    const int b = kCG * blockIdx.x + c;
+    valid[c] = b < a.B;
+    bs[c] = min(b, a.B - 1);
+  }
   const int p = MODE == kCFix ? blockIdx.y + 1 : blockIdx.y;
   const int r0 = p * a.CL, r1 = min(r0 + a.CL, a.N) - 1;
-  const uint32_t *s0 = nullptr, *s1 = nullptr;
-  if (MODE == kCFix) {
-    s0 = a.ckrow + ((size_t)b0 * a.nq + r0 / 4 - 1) * kCKP;
-    s1 = a.ckrow + ((size_t)b1 * a.nq + r0 / 4 - 1) * kCKP;
-  }
+  const uint32_t *start[kCG];
+#pragma unroll
+  for (int c = 0; c < kCG; ++c) start[c] = a.ckrow + ((size_t)bs[c] * a.nq + (r0 > 0 ? r0 / 4 - 1 : 0)) * kCKP;
   CwChains<MODE> ch;
-  cw_run<MODE>(a, b0, b1, true, valid1, r0, r1, s0, s1, sm, ch);
-  const int tid = threadIdx.x;
-  const int mc = (tid & 7) >> 2, ms = 4 * (tid >> 3) + (((tid & 7) ^ (mc ? 3 : 0)) & 3);
+  cw_run<MODE>(a, bs, valid, r0, r1, start, sm, ch);
+  const int tid = threadIdx.x, g = tid & 7;
+  const bool f0 = ((g ^ (g >> 2)) & 1) != 0, f1 = (((g >> 1) ^ (g >> 2)) & 1) != 0, f2 = (g >> 2) != 0;
+  const int ms = 4 * (tid >> 3) + (f1 ? 2 : 0) + (f0 ? 1 : 0);
   if (MODE == kCSpec) {
-    if (tid == 0) a.rec[(size_t)b0 * a.P + p].flags = (int32_t)ch.flags[0];
-    if (tid == 0 && valid1) a.rec[(size_t)b1 * a.P + p].flags = (int32_t)ch.flags[1];
+#pragma unroll
+    for (int c = 0; c < kCG; ++c)
+      if (tid == 0 && valid[c]) a.rec[(size_t)bs[c] * a.P + p].flags = (int32_t)ch.flags[c];
   } else {
-    const int mb = mc ? b1 : b0;
-    if ((mc == 0 || valid1) && ch.conv[mc] < 0) a.endrow[((size_t)mb * a.P + p) * kCKP + ms] = ch.x;
-    for (int c = 0; c < 2; ++c) {
-      if (tid != 4 * c || (c == 1 && !valid1)) continue;
-      CwRec &r = a.rec[(size_t)(c ? b1 : b0) * a.P + p];
+#pragma unroll
+    for (int h = 0; h < kCH; ++h) {
+      const int c = 2 * h + (f2 ? 1 : 0);
+      const bool v = f2 ? valid[2 * h + 1] : valid[2 * h];
+      const int b = f2 ? bs[2 * h + 1] : bs[2 * h];
+      const int cv = f2 ? ch.conv[2 * h + 1] : ch.conv[2 * h];
+      (void)c;
+      if (v && cv < 0) a.endrow[((size_t)b * a.P + p) * kCKP + ms] = ch.x[h];
+    }
+#pragma unroll
+    for (int c = 0; c < kCG; ++c) {
+      if (tid != c || !valid[c]) continue;
+      CwRec &r = a.rec[(size_t)bs[c] * a.P + p];
       r.conv = ch.conv[c];
       r.dfix = (int64_t)(ch.conv[c] >= 0 ? ch.dconv[c] : ch.dsum[c]);
     }
@@ -397,24 +459,36 @@ __global__ __launch_bounds__(kCThreads, 1) void chain_cw_final_kernel(CwArgs a, 
   __syncthreads();
   const int q = s_q;
   uint64_t drep = 0;
-  // the final row: state s of chain 0 is held by lane (tid & 7) < 4 of its quad
-  const int mc = (tid & 7) >> 2, ms = 4 * (tid >> 3) + (((tid & 7) ^ (mc ? 3 : 0)) & 3);
+  // the final row: chain 0 of state s is held by the threads with bit 2 of
+  // their group clear, as pair 0
+  const int g = tid & 7;
+  const bool f0 = ((g ^ (g >> 2)) & 1) != 0, f1 = (((g >> 1) ^ (g >> 2)) & 1) != 0, f2 = (g >> 2) != 0;
+  const int ms = 4 * (tid >> 3) + (f1 ? 2 : 0) + (f0 ? 1 : 0);
   uint32_t xv;
   if (q < P - 1) {
-    // Rerun the chain after chunk q from its true end row (the second chain
-    // duplicates the first and is discarded).
+    // Rerun the chain after chunk q from its true end row (the other chains
+    // duplicate it and are discarded).
     const uint32_t *st = a.endrow + ((size_t)b * P + q) * kCKP;
+    int bs[kCG];
+    bool valid[kCG];
+    const uint32_t *start[kCG];
+#pragma unroll
+    for (int c = 0; c < kCG; ++c) {
+      bs[c] = b;
+      valid[c] = c == 0;
+      start[c] = st;
+    }
     CwChains<kCRepair> ch;
-    cw_run<kCRepair>(a, b, b, true, false, (q + 1) * a.CL, a.N - 1, st, st, sm, ch);
-    xv = ch.x;
+    cw_run<kCRepair>(a, bs, valid, (q + 1) * a.CL, a.N - 1, start, sm, ch);
+    xv = ch.x[0];
     drep = ch.dsum[0];
   } else if (q == P - 1) {
     xv = a.endrow[((size_t)b * P + q) * kCKP + ms];
   } else {
     xv = a.ckrow[((size_t)b * a.nq + a.nq - 1) * kCKP + ms];
   }
-  // The final row has minimum 0: the lowest state at the minimum (chain 0 lanes).
-  const uint32_t pk = cw_wave_min((mc == 0 && ms < a.K) ? (xv | (uint32_t)ms) : kSat);
+  // The final row has minimum 0: the lowest state at the minimum.
+  const uint32_t pk = cw_wave_min((!f2 && ms < a.K) ? (xv | (uint32_t)ms) : kSat);
   if (lane == 0) s_fin[wid] = pk;
   __syncthreads();
   if (tid == 0) {
@@ -440,8 +514,8 @@ struct CwPlan {
 CwPlan cw_plan(int n, int k, int batch) {
   CwPlan c{0, 0, 0};
   if (k <= 128 || k > kCKP || n < 2 * kCMinRows) return c;
-  const int pairs = (batch + 1) / 2;
-  int P = std::max(2, (256 + pairs - 1) / pairs);  // about one workgroup per compute unit
+  const int groups = (batch + kCG - 1) / kCG;
+  int P = std::max(2, (256 + groups - 1) / groups);  // about one workgroup per compute unit
   P = std::min(P, std::min(kCMaxChunks, n / kCMinRows));
   int CL = ((n + P - 1) / P + 3) & ~3;
   P = (n + CL - 1) / CL;
@@ -492,11 +566,11 @@ hipError_t launch_chain_cw(const cfp_chain_desc &d, const int32_t *redge_dev, ui
   off += align_up((size_t)d.batch * c.nq * kCKP * 4);
   a.endrow = (uint32_t *)(region + off);
   launch_pack_rtab(d.rtab, d.n_tables, d.k, kCKP, kCBits, rpk, st);
-  const int pairs = (d.batch + 1) / 2;
+  const int groups = (d.batch + kCG - 1) / kCG;
   timer_begin(st);
-  hipLaunchKernelGGL(chain_cw_kernel<kCSpec>, dim3(pairs, c.P), dim3(kCThreads), 0, st, a);
+  hipLaunchKernelGGL(chain_cw_kernel<kCSpec>, dim3(groups, c.P), dim3(kCThreads), 0, st, a);
   timer_end(st);
-  hipLaunchKernelGGL(chain_cw_kernel<kCFix>, dim3(pairs, c.P - 1), dim3(kCThreads), 0, st, a);
+  hipLaunchKernelGGL(chain_cw_kernel<kCFix>, dim3(groups, c.P - 1), dim3(kCThreads), 0, st, a);
   hipLaunchKernelGGL(chain_cw_final_kernel, dim3(d.batch), dim3(kCThreads), 0, st, a, hdr, res, opt, status);
   return hipGetLastError();
 }
