@@ -61,7 +61,7 @@ TRAFFIC = {
     "chain_gpt_n24_k16": {"fetch_kib": 18.0, "write_kib": 0.5, "sources": "8f96d936c23286f2"},
     "chain_gpt_n1152_k64": {"fetch_kib": 37981.2, "write_kib": 37514.8, "sources": "c32e87116e074150"},
     "mem_llama_n288_k32": {"fetch_kib": 60508.5, "write_kib": 239152.8, "sources": "efe31c2ab53be227"},
-    "chain_wide_n512_k256": {"fetch_kib": 151586.5, "write_kib": 73587.7, "sources": "95027697bdce3992"},
+    "chain_wide_n512_k256": {"fetch_kib": 44549.3, "write_kib": 16423.8, "sources": "1a7191b805032226"},
     # mean over the 12 matrix-product launches of one forward call
     "scan_n4096_k512": {"fetch_kib": 3033234.8, "write_kib": 1398442.5, "sources": "c0b783da46bf748c"},
     "seg_gpt_n96_k81": {"fetch_kib": 3922.7, "write_kib": 1936.0, "sources": "a910a0e94a0c4a1f"},

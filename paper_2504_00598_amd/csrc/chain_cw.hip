@@ -5,9 +5,9 @@
 // P chunks that run at once, made exact by rank convergence (Maleki,
 // Musuvathi and Mytkowicz, PPoPP 2014): a recurrence started from an
 // arbitrary row becomes parallel to the true one after a few steps.
-//   1. speculative pass: chunk p starts at its first row from that row's costs
-//      alone, writes its argmin rows and, at every quad end, its normalised row
-//      and running offset (a checkpoint);
+//   1. speculative pass: chunk p starts at its first row (or kCWarm rows
+//      before it) from that row's costs alone, writes its argmin rows and, at
+//      every quad end, its normalised row and running offset (a checkpoint);
 //   2. fix-up pass, chunks p >= 1: start again from the last checkpoint row of
 //      chunk p-1 and recompute until the row equals chunk p's checkpoint of the
 //      same quad (from there on the speculative rows are the true ones);
@@ -17,18 +17,17 @@
 //
 // One workgroup of 512 threads carries four chains (four searches of the same
 // chunk: every chain of a launch is at the same row, so all use the same
-// table) and all KP = 256 states.  Thread tid = 8 q + g works for the states
-// 4q .. 4q+3 of every chain over the predecessors t = 32 g .. 32 g + 31.  Per
+// table) and all KP = 256 states.  Thread tid = 64 g + q (wave g) works for the
+// states 4q .. 4q+3 of every chain over the predecessors t = 32 g .. 32 g + 31,
+// so every table load of a wave reads 1 KiB of one row contiguously.  Per
 // step it reads its 32 x 4 packed words (R_e[t][s] << 8) | t of the edge's
 // table from the cache-resident array (each word serves the four chains), in
 // four pieces of eight rows, each loaded one step ahead into its own registers,
 // and the predecessors' values from the previous rows in LDS (broadcast
 // reads).  A candidate is a saturating add, and one unsigned minimum keeps the
 // value and the lowest predecessor.  The eight group minima of a state are
-// combined by a reduce-scatter over the eight lanes of the state quad (two
-// quad_perm steps and a half-mirror step, lanes of the upper half holding the
-// complementary indices), after which lane g holds state
-// 4q + ((g ^ 3 (g / 4)) % 4) of chains g / 4 and 2 + g / 4.
+// combined through LDS, after which thread tid holds state tid % 256 of chains
+// tid / 256 and 2 + tid / 256.
 //
 // The table stream is what bounds a step: 256 KiB per workgroup and step,
 // which one CU takes in from L2 at about 14 bytes per clock (measured: the
@@ -62,6 +61,10 @@ constexpr uint32_t kCCap = (1u << (32 - kCBits)) - 1u;
 constexpr uint32_t kCX = 0xFFFFFFFFu;   // x of an unavailable or padding state
 constexpr int kCMaxChunks = 64;
 constexpr int kCMinRows = 16;           // least rows per chunk
+// Rows a speculative run starts before its chunk.  Starting early makes the
+// run parallel to the true one sooner, so the fix-up pass stops earlier, but
+// at K = 256 the rows saved there equal the rows added here (measured), so 0.
+constexpr int kCWarm = 0;
 
 constexpr int kCG = 4;                  // chains per workgroup (searches of the same chunk)
 constexpr int kCH = kCG / 2;            // chains per thread after the reduce-scatter
@@ -86,6 +89,7 @@ struct CwArgs {
 };
 
 struct CwSmem {
+  uint32_t part[kCG][kCWaves][kCKP];  // partial minima [chain][predecessor group][state]
   uint32_t q[2][kCG][kCQS];   // rows [buffer][chain][state, padded]
   uint32_t wm[kCWaves][kCG];  // wave minima of the new row, per chain
   int32_t wd[kCWaves][kCG];   // fix-up: the wave found a state off the checkpoint, per chain
@@ -114,8 +118,8 @@ __device__ __forceinline__ uint32_t cw_wave_min(uint32_t x) {
 }
 
 // State of the workgroup's chains as seen by one thread.  After the
-// reduce-scatter a thread holds, for its state s, the chains 2h + f2,
-// h = 0 .. kCG/2 - 1 (f2 = bit 2 of its group).
+// reduction a thread holds, for its state s = tid % 256, the chains 2h + f2,
+// h = 0 .. kCG/2 - 1 (f2 = tid / 256).
 template <int MODE>
 struct CwChains {
   uint32_t x[kCH];      // the thread's values of the current row, normalised and shifted
@@ -125,20 +129,21 @@ struct CwChains {
   uint32_t flags[kCG];  // speculative: bit 0 a negative cost, bit 1 a row with no available strategy
 };
 
-// Runs rows [r0 (+1 in the speculative pass), r1] of the workgroup's chains
-// (searches bs[c], real where valid[c]).  Speculative: the start row is row r0
-// from its costs; checkpoints are written.  Fix-up: the start row (row r0 - 1)
+// Runs rows [r0, r1] of the workgroup's chains (searches bs[c], real where
+// valid[c]).  Speculative: the start row is row rs <= r0 from its costs alone
+// (rows before r0 warm the run up and write nothing); argmins from row r0 and
+// checkpoints are written.  Fix-up: the start row (row r0 - 1)
 // is start[c]; stops at the first quad end where every real chain has met its
 // checkpoint.  Repair: like fix-up without checkpoints.
 template <int MODE>
-__device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const bool *valid, int r0, int r1,
+__device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const bool *valid, int rs, int r0, int r1,
                                        const uint32_t *const *start, CwSmem &sm, CwChains<MODE> &ch) {
   const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int qd = tid >> 3, g = tid & 7;  // state quad, predecessor group
+  const int qd = lane, g = wid;  // state quad, predecessor group (one wave each)
   const int N = a.N, K = a.K;
-  // the thread's state and chains after the reduce-scatter
-  const bool f0 = ((g ^ (g >> 2)) & 1) != 0, f1 = (((g >> 1) ^ (g >> 2)) & 1) != 0, f2 = (g >> 2) != 0;
-  const int ms = 4 * qd + (f1 ? 2 : 0) + (f0 ? 1 : 0);
+  // the thread's state and chains after the reduction
+  const bool f2 = tid >= kCKP;
+  const int ms = tid & (kCKP - 1);
   const bool sin = ms < K;
   int hc[kCH];  // chain of pair h
   bool hv[kCH];
@@ -154,10 +159,12 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
     tbase[h] = a.table + (size_t)b * N * K + ms;
     ckb[h] = a.ckrow + (size_t)b * a.nq * kCKP + ms;
   }
-  auto edge = [&](int row) __attribute__((always_inline)) {
-    return __builtin_amdgcn_readfirstlane(a.redge[row]);
-  };
-  const int i0 = MODE == kCSpec ? r0 + 1 : r0;
+  // redge is read-only for the kernel's lifetime: read through the constant
+  // address space, so a row's table index is one scalar load.
+  const __attribute__((address_space(4))) int32_t *redge_c =
+      (const __attribute__((address_space(4))) int32_t *)a.redge;
+  auto edge = [&](int row) __attribute__((always_inline)) { return redge_c[row]; };
+  const int i0 = MODE == kCSpec ? rs + 1 : r0;
 
   // Table pieces of the next row, [piece][row in piece]; word offset of the
   // thread's first word within a table.
@@ -195,12 +202,11 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
     ch.dsum[c] = 0;
   }
   uint32_t cor[kCH];
-  int cur = 0;
   if (MODE == kCSpec) {
     uint32_t x[kCH], d[kCG];
 #pragma unroll
     for (int h = 0; h < kCH; ++h) {
-      const uint32_t cv = (uint32_t)cbase[h][(size_t)r0 * K];
+      const uint32_t cv = (uint32_t)cbase[h][(size_t)rs * K];
       cor[h] = cv;
       x[h] = (sin && cv != (uint32_t)CFP_COST_INF) ? cv : kCX;
     }
@@ -215,7 +221,7 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
       ch.x[h] = umin(x[h] - (f2 ? d[2 * h + 1] : d[2 * h]), kCCap) << kCBits;
       sm.q[0][hc[h]][qpad(ms)] = ch.x[h];
     }
-    if (i0 > r1) {  // a run of one row: the start row is its checkpoint
+    if (i0 > r1) {  // a run of one row (rs = r0): the start row is its checkpoint
 #pragma unroll
       for (int h = 0; h < kCH; ++h)
         if (hv[h]) ckb[h][(size_t)(r0 / 4) * kCKP] = ch.x[h];
@@ -242,18 +248,23 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
   }
 #pragma unroll
   for (int k = 0; k < kCPieces; ++k) tload(k, i0);
-  uint32_t c1[kCH], c2[kCH], ckv[kCH];  // costs of the next row and of the one after; checkpoint
+  // Costs of the next two rows, [row parity][pair]: step i uses set i - i0 mod 2
+  // and reloads it with row i + 2 (the loop runs two rows per turn, so every
+  // index is a constant and no register is copied from a load in flight).
+  uint32_t cq[2][kCH], ckv[kCH];
 #pragma unroll
   for (int h = 0; h < kCH; ++h) {
-    c1[h] = (uint32_t)cbase[h][(size_t)i0 * K];
-    c2[h] = (uint32_t)cbase[h][(size_t)min(i0 + 1, r1) * K];
+    cq[0][h] = (uint32_t)cbase[h][(size_t)i0 * K];
+    cq[1][h] = (uint32_t)cbase[h][(size_t)min(i0 + 1, r1) * K];
     ckv[h] = 0;
     if (MODE == kCFix) ckv[h] = ckb[h][(size_t)(i0 >> 2) * kCKP];
   }
   __syncthreads();
 
-  for (int i = i0; i <= r1; ++i) {
-    const int nxt = cur ^ 1;
+  // One row i with the previous rows in LDS buffer CUR; returns true when the
+  // fix-up pass is done.
+  auto step = [&](int i, auto Pc) __attribute__((always_inline)) -> bool {
+    constexpr int cur = decltype(Pc)::value, nxt = cur ^ 1;
     uint32_t acc[kCG][4];
 #pragma unroll
     for (int c = 0; c < kCG; ++c)
@@ -283,35 +294,36 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
       }
       tload(k, inext);  // this piece of the next row into the registers just consumed
     }
-    // Reduce-scatter over the eight groups of the state quad.  Value index
-    // k = 4 c + u; lane bits (b2 b1 b0) = g.  Step 1 keeps k0 = b0 ^ b2, step 2
-    // k1 = b1 ^ b2 (quad_perm partners), step 3 k2 = b2 (half mirror: lane
-    // 7 - g, whose kept k0, k1 equal this lane's); k3 .. remain (pairs h).
-    uint32_t r1v[2 * kCG];
+    // Minima over the eight predecessor groups (one wave each) through LDS.
 #pragma unroll
-    for (int p = 0; p < 2 * kCG; ++p) {
-      const uint32_t lo = acc[p >> 1][(p & 1) * 2], hi = acc[p >> 1][(p & 1) * 2 + 1];
-      r1v[p] = min_dpp<kDppXor1>(f0 ? hi : lo, f0 ? lo : hi);
+    for (int c = 0; c < kCG; ++c) {
+      u32x4 pv;
+      pv.x = acc[c][0];
+      pv.y = acc[c][1];
+      pv.z = acc[c][2];
+      pv.w = acc[c][3];
+      *(u32x4 *)&sm.part[c][g][4 * qd] = pv;
     }
-    uint32_t r2v[kCG];
-#pragma unroll
-    for (int p = 0; p < kCG; ++p)
-      r2v[p] = min_dpp<kDppXor2>(f1 ? r1v[2 * p + 1] : r1v[2 * p], f1 ? r1v[2 * p] : r1v[2 * p + 1]);
+    __syncthreads();
     uint32_t m[kCH];
 #pragma unroll
-    for (int h = 0; h < kCH; ++h)
-      m[h] = min_dpp<kDppHalfMirror>(f2 ? r2v[2 * h + 1] : r2v[2 * h], f2 ? r2v[2 * h] : r2v[2 * h + 1]);
+    for (int h = 0; h < kCH; ++h) {
+      const int c = 2 * h + (f2 ? 1 : 0);
+      uint32_t v = sm.part[c][0][ms];
+#pragma unroll
+      for (int w = 1; w < kCWaves; ++w) v = umin(v, sm.part[c][w][ms]);
+      m[h] = v;
+    }
 
     // New row: the thread's pairs.
     uint32_t x[kCH];
 #pragma unroll
     for (int h = 0; h < kCH; ++h) {
-      const uint32_t cv = c1[h];
-      c1[h] = c2[h];
-      c2[h] = (uint32_t)cbase[h][(size_t)min(i + 2, r1) * K];
+      const uint32_t cv = cq[cur][h];
+      cq[cur][h] = (uint32_t)cbase[h][(size_t)min(i + 2, r1) * K];
       if (MODE == kCSpec) cor[h] |= cv;
       x[h] = (sin && cv != (uint32_t)CFP_COST_INF) ? (m[h] >> kCBits) + cv : kCX;
-      if (sin && hv[h]) tbase[h][(size_t)i * K] = (uint8_t)(m[h] & (kCKP - 1));
+      if (sin && hv[h] && i >= r0) tbase[h][(size_t)i * K] = (uint8_t)(m[h] & (kCKP - 1));
     }
     uint32_t d[kCG];
     row_min(x, d);
@@ -328,7 +340,7 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
     const bool qend = (i & 3) == 3 || i == r1;
     if (qend) {
       const int q = i >> 2;
-      if (MODE == kCSpec) {
+      if (MODE == kCSpec && i >= r0) {
 #pragma unroll
         for (int h = 0; h < kCH; ++h)
           if (hv[h]) ckb[h][(size_t)q * kCKP] = ch.x[h];
@@ -349,7 +361,6 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
       }
     }
     __syncthreads();
-    cur = nxt;
     if (MODE == kCFix && qend) {
       const int q = i >> 2;
       bool all = true;
@@ -364,8 +375,13 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
         }
         all = all && (ch.conv[c] >= 0 || !valid[c]);
       }
-      if (all) break;
+      if (all) return true;
     }
+    return false;
+  };
+  for (int i = i0; i <= r1; i += 2) {
+    if (step(i, std::integral_constant<int, 0>{})) break;
+    if (i + 1 > r1 || step(i + 1, std::integral_constant<int, 1>{})) break;
   }
   if (MODE == kCSpec) negative_costs();
 }
@@ -385,14 +401,16 @@ __global__ __launch_bounds__(kCThreads, 1) void chain_cw_kernel(CwArgs a) {
   }
   const int p = MODE == kCFix ? blockIdx.y + 1 : blockIdx.y;
   const int r0 = p * a.CL, r1 = min(r0 + a.CL, a.N) - 1;
+  // the speculative run of a chunk after the first starts kCWarm rows early
+  const int rs = (MODE == kCSpec && p > 0) ? max(r0 - kCWarm, 0) : r0;
   const uint32_t *start[kCG];
 #pragma unroll
   for (int c = 0; c < kCG; ++c) start[c] = a.ckrow + ((size_t)bs[c] * a.nq + (r0 > 0 ? r0 / 4 - 1 : 0)) * kCKP;
   CwChains<MODE> ch;
-  cw_run<MODE>(a, bs, valid, r0, r1, start, sm, ch);
-  const int tid = threadIdx.x, g = tid & 7;
-  const bool f0 = ((g ^ (g >> 2)) & 1) != 0, f1 = (((g >> 1) ^ (g >> 2)) & 1) != 0, f2 = (g >> 2) != 0;
-  const int ms = 4 * (tid >> 3) + (f1 ? 2 : 0) + (f0 ? 1 : 0);
+  cw_run<MODE>(a, bs, valid, rs, r0, r1, start, sm, ch);
+  const int tid = threadIdx.x;
+  const bool f2 = tid >= kCKP;
+  const int ms = tid & (kCKP - 1);
   if (MODE == kCSpec) {
 #pragma unroll
     for (int c = 0; c < kCG; ++c)
@@ -459,11 +477,9 @@ __global__ __launch_bounds__(kCThreads, 1) void chain_cw_final_kernel(CwArgs a, 
   __syncthreads();
   const int q = s_q;
   uint64_t drep = 0;
-  // the final row: chain 0 of state s is held by the threads with bit 2 of
-  // their group clear, as pair 0
-  const int g = tid & 7;
-  const bool f0 = ((g ^ (g >> 2)) & 1) != 0, f1 = (((g >> 1) ^ (g >> 2)) & 1) != 0, f2 = (g >> 2) != 0;
-  const int ms = 4 * (tid >> 3) + (f1 ? 2 : 0) + (f0 ? 1 : 0);
+  // the final row: chain 0 of state s is held by thread s, as pair 0
+  const bool f2 = tid >= kCKP;
+  const int ms = tid & (kCKP - 1);
   uint32_t xv;
   if (q < P - 1) {
     // Rerun the chain after chunk q from its true end row (the other chains
@@ -479,7 +495,7 @@ __global__ __launch_bounds__(kCThreads, 1) void chain_cw_final_kernel(CwArgs a, 
       start[c] = st;
     }
     CwChains<kCRepair> ch;
-    cw_run<kCRepair>(a, bs, valid, (q + 1) * a.CL, a.N - 1, start, sm, ch);
+    cw_run<kCRepair>(a, bs, valid, (q + 1) * a.CL, (q + 1) * a.CL, a.N - 1, start, sm, ch);
     xv = ch.x[0];
     drep = ch.dsum[0];
   } else if (q == P - 1) {
