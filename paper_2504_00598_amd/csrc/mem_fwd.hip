@@ -332,7 +332,10 @@ __device__ __forceinline__ int mem_index_bits(int k) {
   return b;
 }
 
-__global__ __launch_bounds__(kThreads) void mem_tb_kernel(int N, int K, int M, const uint8_t *__restrict__ table,
+constexpr int kMemTbThreads = 1024;  // every 16-byte piece of a window in flight at once
+constexpr int kMemTbLoads = 8;       // pieces per thread and pass
+
+__global__ __launch_bounds__(kMemTbThreads) void mem_tb_kernel(int N, int K, int M, const uint8_t *__restrict__ table,
                                                           const uint8_t *__restrict__ mem_copy,
                                                           const SearchResult *__restrict__ res,
                                                           int32_t *__restrict__ plan) {
@@ -362,37 +365,40 @@ __global__ __launch_bounds__(kThreads) void mem_tb_kernel(int N, int K, int M, c
     const int lo16 = lo & ~15;
     const int n16 = (mtop - lo16) / 16 + 1;  // 16-byte pieces covering [lo16, mtop]
     if (vec) {
+      // all pieces of a pass are loaded before any is stored, so the window
+      // costs about one memory latency
       const int total = steps * K * n16;
-      for (int x0 = 0; x0 < total; x0 += 4 * kThreads) {
-        uint4 v[4];
+      for (int x0 = 0; x0 < total; x0 += kMemTbLoads * kMemTbThreads) {
+        typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));  // copies stay in registers
+        u32x4 v[kMemTbLoads];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int x = x0 + u * kThreads + tid;
+        for (int u = 0; u < kMemTbLoads; ++u) {
+          const int x = x0 + u * kMemTbThreads + tid;
           const int k = x / (K * n16), t = (x / n16) % K, c = x % n16;
           if (x < total)
-            v[u] = *(const uint4 *)&table[(((size_t)b * N + (i - k)) * K + t) * M + lo16 + 16 * c];
+            v[u] = *(const u32x4 *)&table[(((size_t)b * N + (i - k)) * K + t) * M + lo16 + 16 * c];
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int x = x0 + u * kThreads + tid;
+        for (int u = 0; u < kMemTbLoads; ++u) {
+          const int x = x0 + u * kMemTbThreads + tid;
           const int k = x / (K * n16), t = (x / n16) % K, c = x % n16;
-          if (x < total) *(uint4 *)&win[((size_t)k * K + t) * width + 16 * c] = v[u];
+          if (x < total) *(u32x4 *)&win[((size_t)k * K + t) * width + 16 * c] = v[u];
         }
       }
     } else {
       const int wd = mtop - lo16 + 1;
       const int total = steps * K * wd;
-      for (int x0 = 0; x0 < total; x0 += 16 * kThreads) {
+      for (int x0 = 0; x0 < total; x0 += 16 * kMemTbThreads) {
         uint8_t v[16];
 #pragma unroll
         for (int u = 0; u < 16; ++u) {
-          const int x = x0 + u * kThreads + tid;
+          const int x = x0 + u * kMemTbThreads + tid;
           const int k = x / (K * wd), t = (x / wd) % K, c = x % wd;
           v[u] = x < total ? table[(((size_t)b * N + (i - k)) * K + t) * M + lo16 + c] : 0;
         }
 #pragma unroll
         for (int u = 0; u < 16; ++u) {
-          const int x = x0 + u * kThreads + tid;
+          const int x = x0 + u * kMemTbThreads + tid;
           const int k = x / (K * wd), t = (x / wd) % K, c = x % wd;
           if (x < total) win[((size_t)k * K + t) * width + c] = v[u];
         }
@@ -422,7 +428,7 @@ __global__ __launch_bounds__(kThreads) void mem_tb_kernel(int N, int K, int M, c
 hipError_t launch_traceback_mem(int n, int k, int batch, int n_mem, const uint8_t *table, const uint8_t *mem,
                                 const SearchResult *res, int32_t *plan, hipStream_t st) {
   const size_t lds = (size_t)kMemWin * k * kMemWinWidth + (size_t)kMemWin * k;
-  hipLaunchKernelGGL(mem_tb_kernel, dim3(batch), dim3(kThreads), lds, st, n, k, n_mem, table, mem, res, plan);
+  hipLaunchKernelGGL(mem_tb_kernel, dim3(batch), dim3(kMemTbThreads), lds, st, n, k, n_mem, table, mem, res, plan);
   return hipGetLastError();
 }
 
