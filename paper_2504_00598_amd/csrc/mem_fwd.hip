@@ -117,10 +117,12 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
   constexpr int COLS = H + C;
 
   __shared__ uint32_t Q[KP][COLS];
-  __shared__ int64_t off[COLS];
+  __shared__ int64_t off[2][COLS];   // column offsets, [step parity]
   __shared__ uint32_t part[NW][C];
   __shared__ uint32_t reach[NW][C];
+  __shared__ uint8_t argb[KP][C];    // argmin bytes of the step, written back after it
   __shared__ int abort_flag;
+  __shared__ int halo_ready;         // wave 0 has the next halo in registers
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave: per-state data comes by scalar loads
@@ -147,7 +149,8 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
 
   // Halo of chunk 0: buckets below 0 are infeasible.
   for (int x = tid; x < KP * H; x += kMemThreads) Q[x / H][x % H] = CAP << BITS;
-  if (tid < H) off[tid] = kOffInf;
+  if (tid < H) off[0][tid] = off[1][tid] = kOffInf;
+  if (tid == 0) abort_flag = 0;
   __syncthreads();
 
   const size_t chunk_id = (size_t)b * w.nchunk + j;
@@ -155,14 +158,54 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
   int64_t *my_roff = w.ring_off + chunk_id * N * H;
   const uint32_t *lo_ring = w.ring + (chunk_id - 1) * N * KP * H;
   const int64_t *lo_roff = w.ring_off + (chunk_id - 1) * N * H;
+  const bool consumer = j > 0;
 
   // y[k]: value of the wave's k-th state at bucket m relative to the previous
   // offset of column m; rk: the state is reachable.
   uint32_t y[SW];
   bool rk[SW];
 
+  // Halo prefetch of wave 0: the producer's published step, read at the start
+  // of a step, and its halo, read after the wave's part of the step once the
+  // producer has published it.
+  constexpr int HW = KP * H / 64;
+  uint32_t hq[HW];
+  int64_t ho = kOffInf;
+  int pubv = -1;
+  auto pub_prefetch = [&](int i) __attribute__((always_inline)) {
+    if (consumer && wid == 0 && i + 1 < N)
+      pubv = __hip_atomic_load(&w.pub[chunk_id - 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  };
+  auto halo_prefetch = [&](int i) __attribute__((always_inline)) {
+    if (wid != 0) return;
+    const bool ok = consumer && i + 1 < N && pubv >= i;
+    if (ok) {
+#pragma unroll
+      for (int k = 0; k < HW; ++k)
+        hq[k] = __hip_atomic_load(&lo_ring[(size_t)i * KP * H + lane + 64 * k], __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_AGENT);
+      if (lane < H) ho = __hip_atomic_load(&lo_roff[(size_t)i * H + lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (lane == 0) halo_ready = ok;
+  };
+
+  // Argmin bytes of step i from LDS to the table, buckets m0 .. min(m0 + C, Bb + 1, M) - 1.
+  constexpr int BPT = KP * C / kMemThreads;  // bytes per thread
+  auto flush = [&](int i) __attribute__((always_inline)) {
+    const int s = tid / (C / BPT), c0 = (tid % (C / BPT)) * BPT;
+    if (s >= K) return;
+    uint8_t *dst = table + ((rowbase + i) * K + s) * (size_t)M + m0 + c0;
+    const int lim = min(Bb + 1, M) - (m0 + c0);  // bytes of this thread's piece within the budget
+#pragma unroll
+    for (int q = 0; q < BPT; ++q)
+      if (q < lim) dst[q] = argb[s][c0 + q];
+  };
+
+  // End of step i: offsets, the own rows and their halo publication, the
+  // producer's halo for step i+1.  The publication of step i-1 happens here,
+  // one step late, when its ring stores have long completed.
   auto finish_step = [&](int i) __attribute__((always_inline)) {
-    // column minimum over all states
+    const int cur = i & 1, nxt = cur ^ 1;
     uint32_t pm = kSat, pr = 0;
 #pragma unroll
     for (int k = 0; k < SW; ++k) {
@@ -171,7 +214,9 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
     }
     part[wid][lane] = pm;
     reach[wid][lane] = pr;
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's stores of step i-1 are complete
     __syncthreads();
+    if (tid == 0 && i > 0) __hip_atomic_store(&w.pub[chunk_id], i - 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     uint32_t cm = part[0][lane], rr = reach[0][lane];
 #pragma unroll
     for (int x = 1; x < NW; ++x) {
@@ -180,7 +225,7 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
     }
     const bool feas = rr != 0;
     if (feas && cm >= 0x80000000u) flags |= MEMF_OVERFLOW;
-    const int64_t onew = (feas && cm < kSat) ? off[H + lane] + (int64_t)cm : kOffInf;
+    const int64_t onew = (feas && cm < kSat) ? off[cur][H + lane] + (int64_t)cm : kOffInf;
     const uint2 *rec = srec + (rowbase + i) * KP + wid * SW;
 #pragma unroll
     for (int k = 0; k < SW; ++k) {
@@ -191,44 +236,50 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
         __hip_atomic_store(&my_ring[((size_t)i * KP + s) * H + (lane - (C - H))], q, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
     }
-    __syncthreads();  // every wave has read the old offsets
     if (wid == 0) {
-      off[H + lane] = onew;
+      off[nxt][H + lane] = onew;
       if (lane >= C - H)
         __hip_atomic_store(&my_roff[(size_t)i * H + (lane - (C - H))], onew, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
     }
-    // Publish: the ring entries are device-scope stores; once every wave has
-    // seen them complete (vmcnt 0), one device-scope store raises the flag.
-    // Only device-scope accesses touch the ring and the flags, so no cache
-    // write-back is needed.
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (tid == 0) __hip_atomic_store(&w.pub[chunk_id], i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (i > 0) flush(i);
     // Halo for step i+1: the top buckets of the chunk below, at step i.
-    if (j > 0 && i + 1 < N) {
-      if (tid == 0) {
-        int spins = 0;
-        while (__hip_atomic_load(&w.pub[chunk_id - 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < i) {
-          if (++spins > kSpinLimit) {
-            abort_flag = 1;
-            atomicOr(&w.mflags[b], MEMF_TIMEOUT);
-            break;
+    if (consumer && i + 1 < N) {
+      if (halo_ready) {
+        if (wid == 0) {
+#pragma unroll
+          for (int k = 0; k < HW; ++k) {
+            const int x = lane + 64 * k;
+            Q[x / H][x % H] = hq[k];
           }
-          __builtin_amdgcn_s_sleep(1);
+          if (lane < H) off[nxt][lane] = ho;
         }
+      } else {
+        if (tid == 0) {
+          int spins = 0;
+          while (__hip_atomic_load(&w.pub[chunk_id - 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < i) {
+            if (++spins > kSpinLimit) {
+              abort_flag = 1;
+              atomicOr(&w.mflags[b], MEMF_TIMEOUT);
+              break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+          }
+        }
+        __syncthreads();
+        for (int x = tid; x < KP * H; x += kMemThreads)
+          Q[x / H][x % H] =
+              __hip_atomic_load(&lo_ring[(size_t)i * KP * H + x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (tid < H)
+          off[nxt][tid] = __hip_atomic_load(&lo_roff[(size_t)i * H + tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
-      __syncthreads();
-      for (int x = tid; x < KP * H; x += kMemThreads)
-        Q[x / H][x % H] = __hip_atomic_load(&lo_ring[(size_t)i * KP * H + x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (tid < H) off[tid] = __hip_atomic_load(&lo_roff[(size_t)i * H + tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __syncthreads();
     }
+    __syncthreads();
   };
 
-  if (tid == 0) abort_flag = 0;
   // Block 0.
   {
+    pub_prefetch(0);
     const uint2 *rec = srec + rowbase * KP + wid * SW;
 #pragma unroll
     for (int k = 0; k < SW; ++k) {
@@ -237,12 +288,15 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
       rk[k] = active && m >= d && c != CFP_COST_INF;
       y[k] = rk[k] ? (uint32_t)c : kSat;
     }
-    if (wid == 0) off[H + lane] = 0;  // block 0 values are absolute
+    if (wid == 0) off[0][H + lane] = 0;  // block 0 values are absolute
+    halo_prefetch(0);
     __syncthreads();
     finish_step(0);
   }
 
   for (int i = 1; i < N; ++i) {
+    const int cur = i & 1;
+    pub_prefetch(i);
     const int e = redge[i];
     const uint2 *rec = srec + (rowbase + i) * KP + wid * SW;
     uint32_t A[KP];
@@ -272,7 +326,7 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
         dprev = d;
 #pragma unroll
         for (int t = 0; t < KP; ++t) A[t] = Q[t][H + lane - d];
-        const int64_t os = off[H + lane - d], od = off[H + lane];
+        const int64_t os = off[cur][H + lane - d], od = off[cur][H + lane];
         srcok = os < kOffInf;
         const int64_t g = srcok ? os - od : 0;
         goff = g > 0x7FFFFFFF ? 0x80000000u : (uint32_t)g;
@@ -280,18 +334,25 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
       uint32_t acc = sat_add(A[0], colc[0]);
 #pragma unroll
       for (int t = 1; t < KP; ++t) acc = umin(acc, sat_add(A[t], colc[t]));
-      if (active && s < K) table[((rowbase + i) * K + s) * (size_t)M + m] = (uint8_t)acc;
+      argb[s][lane] = (uint8_t)acc;
       const uint32_t v = acc >> BITS;
       rk[k] = active && srcok && v < CAP && c != CFP_COST_INF;
       y[k] = rk[k] ? sat_add(sat_add(v, (uint32_t)c), goff) : kSat;
     }
+    halo_prefetch(i);
     finish_step(i);
   }
+  // Publication of the last step (a consumer needs at most step N-2), then
+  // the state of the final offsets.
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (tid == 0) __hip_atomic_store(&w.pub[chunk_id], N - 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const int fin = N & 1;  // off buffer holding the last step's offsets
 
   // Budget frontier: the exact offset of column m is min_s D[N-1][s][m], the
   // least cost with memory total at most m.
   if (frontier && wid == 0 && m < M)
-    frontier[(size_t)b * M + m] = (active && off[H + lane] < kOffInf) ? off[H + lane] : INT64_MAX;
+    frontier[(size_t)b * M + m] = (active && off[fin][H + lane] < kOffInf) ? off[fin][H + lane] : INT64_MAX;
 
   // The chunk holding the budget bucket reports the search.
   if (abort_flag) flags |= MEMF_TIMEOUT;
@@ -300,7 +361,7 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
     if (tid == 0) {
       uint32_t f = kSat;
       for (int s = 0; s < K; ++s) f = umin(f, Q[s][col] | (uint32_t)s);
-      const int64_t o = off[col];
+      const int64_t o = off[fin][col];
       const int sf = __hip_atomic_load(&w.mflags[b], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) | flags;
       int st = CFP_ST_OK;
       if (abort_flag || (sf & MEMF_TIMEOUT)) st = CFP_ST_TIMEOUT;
