@@ -33,12 +33,21 @@ __device__ __forceinline__ ChunkSpan chunk_span(int c, int n) {
   return sp;
 }
 
-// Copy the rows of steps lo+1 .. hi of one search into LDS (contiguous).
+// Copy the rows of steps lo+1 .. hi of one search into LDS (contiguous), in
+// 16-byte pieces when the rows are so aligned.
 template <typename T>
 __device__ void load_chunk(const T *__restrict__ tab, int b, int n, int k, ChunkSpan sp, T *lds) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
   const size_t base = ((size_t)b * n + sp.lo + 1) * k;
   const int count = (sp.hi - sp.lo) * k;
-  for (int x = threadIdx.x; x < count; x += blockDim.x) lds[x] = tab[base + x];
+  constexpr int PER = 16 / sizeof(T);
+  if ((base % PER) == 0 && (count % PER) == 0) {
+    const u32x4 *src = (const u32x4 *)(tab + base);
+    u32x4 *dst = (u32x4 *)lds;
+    for (int x = threadIdx.x; x < count / PER; x += blockDim.x) dst[x] = src[x];
+  } else {
+    for (int x = threadIdx.x; x < count; x += blockDim.x) lds[x] = tab[base + x];
+  }
   __syncthreads();
 }
 
@@ -63,20 +72,33 @@ __global__ __launch_bounds__(kThreads) void tb_maps_kernel(int n, int k, const T
   }
 }
 
-__global__ void tb_bounds_kernel(int n, int k, int batch, const SearchResult *__restrict__ res,
-                                 const uint16_t *__restrict__ maps, int32_t *__restrict__ bounds, int nchunks,
-                                 int32_t *__restrict__ plan) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= batch) return;
+// One search per workgroup: its chunk maps are staged in LDS (when they fit)
+// so the composition is a chain of LDS reads rather than of memory loads.
+constexpr int kBoundsThreads = 256;
+constexpr size_t kBoundsLds = 48 * 1024;
+
+__global__ __launch_bounds__(kBoundsThreads) void tb_bounds_kernel(int n, int k, int batch,
+                                                                   const SearchResult *__restrict__ res,
+                                                                   const uint16_t *__restrict__ maps,
+                                                                   int32_t *__restrict__ bounds, int nchunks,
+                                                                   int32_t *__restrict__ plan, int staged) {
+  extern __shared__ __align__(16) uint16_t smaps[];
+  const int b = blockIdx.x;
   if (res[b].status != CFP_ST_OK) {
-    plan[(size_t)b * n + n - 1] = -1;
+    if (threadIdx.x == 0) plan[(size_t)b * n + n - 1] = -1;
     return;
   }
+  const uint16_t *mb = maps + (size_t)b * nchunks * k;
+  if (staged) {
+    for (int x = threadIdx.x; x < nchunks * k; x += blockDim.x) smaps[x] = mb[x];
+    __syncthreads();
+  }
+  if (threadIdx.x != 0) return;
   int s = res[b].final_state;
   plan[(size_t)b * n + n - 1] = s;
   for (int c = 0; c < nchunks; ++c) {
     bounds[(size_t)b * nchunks + c] = s;
-    s = maps[((size_t)b * nchunks + c) * k + s];
+    s = staged ? smaps[c * k + s] : mb[(size_t)c * k + s];
   }
 }
 
@@ -121,8 +143,10 @@ hipError_t launch_traceback_chain(int n, int k, int batch, int elem, const uint8
       hipLaunchKernelGGL(tb_maps_kernel<uint16_t>, dim3(nchunks, batch), dim3(kThreads), lds, st, n, k,
                          (const uint16_t *)table, res, maps, nchunks);
   }
-  hipLaunchKernelGGL(tb_bounds_kernel, dim3((batch + 63) / 64), dim3(64), 0, st, n, k, batch, res, maps, bounds,
-                     nchunks, plan);
+  const size_t mbytes = (size_t)nchunks * k * 2;
+  const int staged = mbytes <= kBoundsLds ? 1 : 0;
+  hipLaunchKernelGGL(tb_bounds_kernel, dim3(batch), dim3(kBoundsThreads), staged ? mbytes : 0, st, n, k, batch, res,
+                     maps, bounds, nchunks, plan, staged);
   if (nchunks > 0) {
     if (elem == 1)
       hipLaunchKernelGGL(tb_fill_kernel<uint8_t>, dim3(nchunks, batch), dim3(kThreads), lds, st, n, k, table, res,
