@@ -201,9 +201,26 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
       if (q < lim) dst[q] = argb[s][c0 + q];
   };
 
-  // End of step i: offsets, the own rows and their halo publication, the
-  // producer's halo for step i+1.  The publication of step i-1 happens here,
-  // one step late, when its ring stores have long completed.
+  // Ring stores of step i (the top kMemShift buckets of every state and their
+  // offsets, read back from LDS), by the last wave at the start of step i+1;
+  // that wave waits for them at the end of step i+1, before the barrier after
+  // which step i is published.
+  auto ring_store = [&](int i) __attribute__((always_inline)) {
+    if (wid != NW - 1 || i + 1 >= N) return;
+    const int cur = (i + 1) & 1;  // offsets of step i
+#pragma unroll
+    for (int k = 0; k < HW; ++k) {
+      const int x = lane + 64 * k, st = x / H, h = x % H;
+      __hip_atomic_store(&my_ring[(size_t)i * KP * H + x], Q[st][C + h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (lane < H)
+      __hip_atomic_store(&my_roff[(size_t)i * H + lane], off[cur][C + lane], __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+  };
+
+  // End of step i: offsets, the own rows, the producer's halo for step i+1.
+  // The publication of step i-1 happens here, one step late, when its ring
+  // stores have long completed.
   auto finish_step = [&](int i) __attribute__((always_inline)) {
     const int cur = i & 1, nxt = cur ^ 1;
     uint32_t pm = kSat, pr = 0;
@@ -214,7 +231,7 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
     }
     part[wid][lane] = pm;
     reach[wid][lane] = pr;
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's stores of step i-1 are complete
+    if (wid == NW - 1) __builtin_amdgcn_s_waitcnt(0);  // the ring stores of step i-1 are complete
     __syncthreads();
     if (tid == 0 && i > 0) __hip_atomic_store(&w.pub[chunk_id], i - 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     uint32_t cm = part[0][lane], rr = reach[0][lane];
@@ -232,16 +249,8 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
       const int s = rec[k].x & 0xFF;
       const uint32_t q = ((onew < kOffInf && y[k] < kSat) ? umin(y[k] - cm, CAP) : CAP) << BITS;
       Q[s][H + lane] = q;
-      if (lane >= C - H)
-        __hip_atomic_store(&my_ring[((size_t)i * KP + s) * H + (lane - (C - H))], q, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
     }
-    if (wid == 0) {
-      off[nxt][H + lane] = onew;
-      if (lane >= C - H)
-        __hip_atomic_store(&my_roff[(size_t)i * H + (lane - (C - H))], onew, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-    }
+    if (wid == 0) off[nxt][H + lane] = onew;
     if (i > 0) flush(i);
     // Halo for step i+1: the top buckets of the chunk below, at step i.
     if (consumer && i + 1 < N) {
@@ -296,6 +305,7 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
 
   for (int i = 1; i < N; ++i) {
     const int cur = i & 1;
+    ring_store(i - 1);
     pub_prefetch(i);
     const int e = redge[i];
     const uint2 *rec = srec + (rowbase + i) * KP + wid * SW;
