@@ -39,6 +39,7 @@ constexpr int kMemChunk = 64;  // buckets per workgroup
 constexpr int kMemShift = 16;  // largest supported mem entry (halo width)
 constexpr int64_t kOffInf = (int64_t)1 << 62;
 constexpr int kSpinLimit = 1 << 22;
+constexpr int kMemTables = 12;  // resharding tables supported (kept in LDS)
 constexpr int kMemThreads = 512;  // 8 waves: two per SIMD, so one wave's waits overlap the other's work
 
 enum { MEMF_BAD = 1, MEMF_TIMEOUT = 2, MEMF_OVERFLOW = 4 };
@@ -123,6 +124,8 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
   __shared__ uint8_t argb[KP][C];    // argmin bytes of the step, written back after it
   __shared__ int abort_flag;
   __shared__ int halo_ready;         // wave 0 has the next halo in registers
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  __shared__ __align__(16) uint32_t rT[kMemTables][KP][KP];  // packed tables, read by broadcast
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave: per-state data comes by scalar loads
@@ -147,6 +150,9 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
   const size_t rowbase = (size_t)b * N;
   int flags = 0;
 
+  // The packed tables (all slots; only those below E are ever read).
+  for (int x = tid; x < kMemTables * KP * KP / 4; x += kMemThreads)
+    ((u32x4 *)&rT[0][0][0])[x] = ((const u32x4 *)rpT)[x];
   // Halo of chunk 0: buckets below 0 are infeasible.
   for (int x = tid; x < KP * H; x += kMemThreads) Q[x / H][x % H] = CAP << BITS;
   if (tid < H) off[0][tid] = off[1][tid] = kOffInf;
@@ -313,24 +319,20 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
     int dprev = -1;
     uint32_t goff = 0;
     bool srcok = false;
-    // resharding column of the next state, loaded one state ahead (SGPRs)
-    uint32_t colc[KP], coln[KP];
-    {
-      const uint32_t *col0 = rpT + ((size_t)e * KP + (rec[0].x & 0xFF)) * KP;
-#pragma unroll
-      for (int t = 0; t < KP; ++t) coln[t] = col0[t];
-    }
 #pragma unroll
     for (int k = 0; k < SW; ++k) {
       const int s = rec[k].x & 0xFF;
       const int d = (rec[k].x >> 8) & 0xFF;
       const int32_t c = (int32_t)rec[k].y;
+      // resharding column of state s (every lane reads the same words)
+      uint32_t colc[KP];
 #pragma unroll
-      for (int t = 0; t < KP; ++t) colc[t] = coln[t];
-      if (k + 1 < SW) {
-        const uint32_t *col1 = rpT + ((size_t)e * KP + (rec[k + 1].x & 0xFF)) * KP;
-#pragma unroll
-        for (int t = 0; t < KP; ++t) coln[t] = col1[t];
+      for (int q = 0; q < KP / 4; ++q) {
+        const u32x4 v = ((const u32x4 *)&rT[e][s][0])[q];
+        colc[4 * q] = v.x;
+        colc[4 * q + 1] = v.y;
+        colc[4 * q + 2] = v.z;
+        colc[4 * q + 3] = v.w;
       }
       if (d != dprev) {
         dprev = d;
