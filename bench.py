@@ -60,13 +60,13 @@ FETCH_SCALE, WRITE_SCALE = 524288.0 / 262167.1, 524288.0 / 524288.0
 TRAFFIC = {
     "chain_gpt_n24_k16": {"fetch_kib": 18.0, "write_kib": 0.5, "sources": "0e8d13c27d216b99"},
     "chain_gpt_n1152_k64": {"fetch_kib": 37977.6, "write_kib": 37514.9, "sources": "80481ca70025b261"},
-    "mem_llama_n288_k32": {"fetch_kib": 59528.0, "write_kib": 236285.7, "sources": "d812307e898c8cab"},
+    "mem_llama_n288_k32": {"fetch_kib": 59583.6, "write_kib": 236706.7, "sources": "a54c35be35daeb3e"},
     "chain_wide_n512_k256": {"fetch_kib": 44575.4, "write_kib": 16423.8, "sources": "1a7191b805032226"},
     # mean over the 12 matrix-product launches of one forward call
     "scan_n4096_k512": {"fetch_kib": 3035428.6, "write_kib": 1398442.5, "sources": "baf520c71302e876"},
     "seg_gpt_n96_k81": {"fetch_kib": 3922.7, "write_kib": 1936.0, "sources": "9f3604356fb3c132"},
     # the memory workload run as a budget frontier (every chunk of every search active)
-    "mem_llama_n288_k32:frontier": {"fetch_kib": 77096.4, "write_kib": 306244.9, "sources": "d812307e898c8cab"},
+    "mem_llama_n288_k32:frontier": {"fetch_kib": 77501.4, "write_kib": 307839.8, "sources": "a54c35be35daeb3e"},
 }
 
 
