@@ -124,6 +124,19 @@ def test_periodic_layers(K):
     assert_chain_parity(cost, rtab, redge, f"periodic K={K}")
 
 
+# The traceback follows the argmin table in one launch from LDS when a search's
+# table fits there (about 150 KiB: N K bytes, 2 N K for K > 256) and in three
+# launches from memory otherwise; shapes on both sides of that boundary, with
+# ties so that many chains of the traceback merge.
+@pytest.mark.parametrize("N,K,B", [(512, 256, 2), (1152, 64, 2), (129, 512, 1), (300, 129, 2),
+                                   (600, 256, 2), (2600, 64, 2), (160, 512, 1), (300, 257, 1)])
+def test_traceback_lds_and_memory_paths(N, K, B):
+    need_gpu()
+    say("traceback path", N, K, B)
+    cost, rtab, redge = rand_case([7, N, K], B, N, K, 4, 0, 50)
+    assert_chain_parity(cost, rtab, redge, f"traceback N={N} K={K}")
+
+
 # K > 64 runs on one of two kernels: the split kernel (each search over P = K_P^2 / 4096
 # workgroups, K_P the padded K, tables in registers) when all B * P workgroups fit the
 # device's 256 compute units and there are at most 12 tables, else the wide kernel (one
