@@ -109,24 +109,78 @@ int check_desc(const cfp_chain_desc *d) {
   return CFP_OK;
 }
 
+// Host-to-device copies of the per-call header go through a ring of pinned
+// host slots per device, so that the copy is asynchronous: a copy from pageable
+// memory holds the calling thread until the stream has drained, which leaves
+// the GPU idle while the next call's launches are issued.  A slot is reused
+// only once the event recorded behind its previous copy has completed.
+constexpr int kUpSlots = 32;
+constexpr size_t kUpSlotBytes = 64 * 1024;
+constexpr int kUpDevices = 64;
+
+struct UploadRing {
+  uint8_t *host = nullptr;
+  hipEvent_t ev[kUpSlots] = {};
+  bool pending[kUpSlots] = {};
+  int next = 0;
+  bool init = false, ok = false;
+};
+std::mutex g_up_mu;
+UploadRing g_up[kUpDevices];
+
+// Copy `bytes` bytes produced by fill(host_ptr) to dst on stream st.
+template <typename F>
+int upload(void *dst, size_t bytes, hipStream_t st, F fill) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return CFP_ERR_HIP;
+  if (bytes <= kUpSlotBytes && dev >= 0 && dev < kUpDevices) {
+    std::lock_guard<std::mutex> lk(g_up_mu);
+    UploadRing &r = g_up[dev];
+    if (!r.init) {
+      r.init = true;
+      r.ok = hipHostMalloc((void **)&r.host, kUpSlots * kUpSlotBytes, hipHostMallocDefault) == hipSuccess;
+      for (int i = 0; r.ok && i < kUpSlots; ++i)
+        r.ok = hipEventCreateWithFlags(&r.ev[i], hipEventDisableTiming) == hipSuccess;
+    }
+    if (r.ok) {
+      const int slot = r.next;
+      r.next = (r.next + 1) % kUpSlots;
+      if (r.pending[slot] && hipEventSynchronize(r.ev[slot]) != hipSuccess) return CFP_ERR_HIP;
+      r.pending[slot] = false;
+      uint8_t *h = r.host + (size_t)slot * kUpSlotBytes;
+      fill(h);
+      if (hipMemcpyAsync(dst, h, bytes, hipMemcpyHostToDevice, st) != hipSuccess) return CFP_ERR_HIP;
+      if (hipEventRecord(r.ev[slot], st) != hipSuccess) return CFP_ERR_HIP;
+      r.pending[slot] = true;
+      return CFP_OK;
+    }
+  }
+  // Too large for a slot (or no pinned memory): a copy from pageable memory.
+  std::vector<uint8_t> buf(bytes);
+  fill(buf.data());
+  if (hipMemcpyAsync(dst, buf.data(), bytes, hipMemcpyHostToDevice, st) != hipSuccess) return CFP_ERR_HIP;
+  return CFP_OK;
+}
+
 // Header + device copy of redge, enqueued as one host-to-device copy.
 int upload_header(const cfp_chain_desc *d, int variant, int n_mem, const WsLayout &L, void *ws, hipStream_t st) {
-  std::vector<uint8_t> buf(L.redge + (size_t)d->n_blocks * 4, 0);
-  WsHeader h;
-  memset(&h, 0, sizeof h);
-  h.magic = kMagic;
-  h.variant = variant;
-  h.n = d->n_blocks;
-  h.k = d->k;
-  h.batch = d->batch;
-  h.n_mem = n_mem;
-  h.elem = L.elem;
-  h.rflag = 0;
-  memcpy(buf.data(), &h, sizeof h);
-  memcpy(buf.data() + L.redge, d->redge, (size_t)d->n_blocks * 4);
-  memset(buf.data() + L.redge, 0, 4);  // redge[0] is ignored; keep it a valid table index
-  if (hipMemcpyAsync(ws, buf.data(), buf.size(), hipMemcpyHostToDevice, st) != hipSuccess) return CFP_ERR_HIP;
-  return CFP_OK;
+  const size_t bytes = L.redge + (size_t)d->n_blocks * 4;
+  return upload(ws, bytes, st, [&](uint8_t *buf) {
+    memset(buf, 0, L.redge);
+    WsHeader h;
+    memset(&h, 0, sizeof h);
+    h.magic = kMagic;
+    h.variant = variant;
+    h.n = d->n_blocks;
+    h.k = d->k;
+    h.batch = d->batch;
+    h.n_mem = n_mem;
+    h.elem = L.elem;
+    h.rflag = 0;
+    memcpy(buf, &h, sizeof h);
+    memcpy(buf + L.redge, d->redge, (size_t)d->n_blocks * 4);
+    memset(buf + L.redge, 0, 4);  // redge[0] is ignored; keep it a valid table index
+  });
 }
 
 }  // namespace
@@ -171,13 +225,17 @@ int cfp_dp_chain(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t *op
   uint8_t *w = (uint8_t *)ws;
   if ((rc = upload_header(d, CFP_V_CHAIN, 0, L, ws, st)) != CFP_OK) return rc;
   WsHeader *hdr = (WsHeader *)w;
-  if (launch_validate_rtab(d->rtab, d->n_tables, d->k, cfp_r_limit(CFP_V_CHAIN, d->k), hdr, st) != hipSuccess)
+  // The chunk-parallel paths check the range of R while packing it.
+  const bool wave = chain_wave_supported(d->n_blocks, d->k, d->n_tables, d->batch);
+  const bool cw = !wave && chain_cw_supported(d->n_blocks, d->k, d->batch);
+  if (!wave && !cw &&
+      launch_validate_rtab(d->rtab, d->n_tables, d->k, cfp_r_limit(CFP_V_CHAIN, d->k), hdr, st) != hipSuccess)
     return CFP_ERR_HIP;
   hipError_t e;
-  if (chain_wave_supported(d->n_blocks, d->k, d->n_tables, d->batch))
+  if (wave)
     e = launch_chain_wave(*d, (const int32_t *)(w + L.redge), w + L.wave, w + L.table,
                           (SearchResult *)(w + L.result), hdr, opt, status, st);
-  else if (chain_cw_supported(d->n_blocks, d->k, d->batch))
+  else if (cw)
     e = launch_chain_cw(*d, (const int32_t *)(w + L.redge), w + L.cw, w + L.table, (SearchResult *)(w + L.result),
                         hdr, opt, status, st);
   else if (chain_fwd_split_supported(d->k, d->n_tables, d->batch))
@@ -204,8 +262,7 @@ int cfp_dp_chain_mem(const cfp_chain_desc *d, const uint8_t *mem, int32_t n_mem,
   uint8_t *w = (uint8_t *)ws;
   if ((rc = upload_header(d, CFP_V_MEM, n_mem, L, ws, st)) != CFP_OK) return rc;
   WsHeader *hdr = (WsHeader *)w;
-  if (launch_validate_rtab(d->rtab, d->n_tables, d->k, cfp_r_limit(CFP_V_MEM, d->k), hdr, st) != hipSuccess)
-    return CFP_ERR_HIP;
+  // the memory forward checks the range of R while packing it
   if (launch_chain_mem_fwd(*d, mem, n_mem, budget, (const int32_t *)(w + L.redge), w + L.table, w + L.mem,
                            w + L.memreg, (SearchResult *)(w + L.result), hdr, opt, status, nullptr, st) != hipSuccess)
     return CFP_ERR_HIP;
@@ -227,8 +284,7 @@ int cfp_mem_frontier(const cfp_chain_desc *d, const uint8_t *mem, int32_t n_mem,
   WsHeader *hdr = (WsHeader *)w;
   int32_t *budget = (int32_t *)(w + L.fbudget);
   if (launch_fill_i32(budget, d->batch, n_mem - 1, st) != hipSuccess) return CFP_ERR_HIP;
-  if (launch_validate_rtab(d->rtab, d->n_tables, d->k, cfp_r_limit(CFP_V_MEM, d->k), hdr, st) != hipSuccess)
-    return CFP_ERR_HIP;
+  // the memory forward checks the range of R while packing it
   if (launch_chain_mem_fwd(*d, mem, n_mem, budget, (const int32_t *)(w + L.redge), w + L.table, w + L.mem,
                            w + L.memreg, (SearchResult *)(w + L.result), hdr, (int64_t *)(w + L.fopt), status,
                            frontier, st) != hipSuccess)

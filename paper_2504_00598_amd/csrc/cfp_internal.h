@@ -87,7 +87,9 @@ size_t split_region_bytes(int k, int batch);
 hipError_t launch_chain_fwd_split(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *region, uint32_t *rpk,
                                   uint8_t *table, SearchResult *res, const WsHeader *hdr, int64_t *opt,
                                   int32_t *status, hipStream_t st);
-void launch_pack_rtab(const int32_t *rtab, int E, int K, int KP, int lb, uint32_t *rpk, hipStream_t st);
+// Packs R as (R << lb) | t; with hdr set it also flags an R entry outside [0, limit).
+void launch_pack_rtab(const int32_t *rtab, int E, int K, int KP, int lb, uint32_t *rpk, hipStream_t st,
+                      int32_t limit = 0, WsHeader *hdr = nullptr);
 bool chain_fwd_wide_supported(int k);
 size_t wide_region_bytes(int n, int k, int batch, int n_tables);
 hipError_t launch_chain_fwd_wide(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *region, uint8_t *table,

@@ -581,7 +581,8 @@ hipError_t launch_chain_cw(const cfp_chain_desc &d, const int32_t *redge_dev, ui
   a.ckrow = (uint32_t *)(region + off);
   off += align_up((size_t)d.batch * c.nq * kCKP * 4);
   a.endrow = (uint32_t *)(region + off);
-  launch_pack_rtab(d.rtab, d.n_tables, d.k, kCKP, kCBits, rpk, st);
+  launch_pack_rtab(d.rtab, d.n_tables, d.k, kCKP, kCBits, rpk, st, cfp_r_limit(CFP_V_CHAIN, d.k),
+                   const_cast<WsHeader *>(hdr));
   const int groups = (d.batch + kCG - 1) / kCG;
   timer_begin(st);
   hipLaunchKernelGGL(chain_cw_kernel<kCSpec>, dim3(groups, c.P), dim3(kCThreads), 0, st, a);

@@ -54,15 +54,21 @@ struct WideShape {
   static constexpr int LB = Pow2Bits<TPG>::value;  // index bits within a group
 };
 
+// With hdr set, the range check of R (entries in [0, limit)) is made on the
+// way and flagged in the header.
 __global__ void pack_rtab_kernel(const int32_t *__restrict__ rtab, int E, int K, int KP, int lb,
-                                 uint32_t *__restrict__ rpk) {
+                                 uint32_t *__restrict__ rpk, int32_t limit, WsHeader *__restrict__ hdr) {
   const size_t total = (size_t)E * KP * KP;
   for (size_t x = (size_t)blockIdx.x * blockDim.x + threadIdx.x; x < total; x += (size_t)gridDim.x * blockDim.x) {
     const int s = (int)(x % KP);
     const int t = (int)((x / KP) % KP);
     const int e = (int)(x / ((size_t)KP * KP));
     uint32_t v = kSat;
-    if (t < K && s < K) v = ((uint32_t)rtab[((size_t)e * K + t) * K + s] << lb) | (uint32_t)(t & ((1 << lb) - 1));
+    if (t < K && s < K) {
+      const int32_t r = rtab[((size_t)e * K + t) * K + s];
+      if (hdr && (r < 0 || r >= limit)) hdr->rflag = 1;
+      v = ((uint32_t)r << lb) | (uint32_t)(t & ((1 << lb) - 1));
+    }
     rpk[x] = v;
   }
 }
@@ -253,10 +259,11 @@ __global__ __launch_bounds__(kWideThreads, 1) void chain_fwd_wide_kernel(
 
 bool chain_fwd_wide_supported(int k) { return k > 64 && k <= 512; }
 
-void launch_pack_rtab(const int32_t *rtab, int E, int K, int KP, int lb, uint32_t *rpk, hipStream_t st) {
+void launch_pack_rtab(const int32_t *rtab, int E, int K, int KP, int lb, uint32_t *rpk, hipStream_t st, int32_t limit,
+                      WsHeader *hdr) {
   const size_t total = (size_t)E * KP * KP;
   const int grid = (int)((total + 255) / 256 < 4096 ? (total + 255) / 256 : 4096);
-  hipLaunchKernelGGL(pack_rtab_kernel, dim3(grid), dim3(256), 0, st, rtab, E, K, KP, lb, rpk);
+  hipLaunchKernelGGL(pack_rtab_kernel, dim3(grid), dim3(256), 0, st, rtab, E, K, KP, lb, rpk, limit, hdr);
 }
 
 // Workspace region of the kernel: packed tables [E][KP][KP] u32, then the
@@ -279,7 +286,7 @@ static void launch_wide_kp(const cfp_chain_desc &d, const int32_t *redge_dev, ui
   const size_t total = (size_t)d.n_tables * KP * KP;
   const int grid = (int)((total + 255) / 256 < 4096 ? (total + 255) / 256 : 4096);
   hipLaunchKernelGGL(pack_rtab_kernel, dim3(grid), dim3(256), 0, st, d.rtab, d.n_tables, d.k, KP,
-                     WideShape<KP>::LB, rpk);
+                     WideShape<KP>::LB, rpk, 0, (WsHeader *)nullptr);
   const int rows = d.batch * d.n_blocks;
   hipLaunchKernelGGL(row_cmin_kernel, dim3((rows + 3) / 4), dim3(256), 0, st, d.cost, rows, d.k, rowcmin);
   timer_begin(st);

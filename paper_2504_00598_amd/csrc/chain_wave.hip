@@ -61,7 +61,7 @@ namespace {
 // copy of the HIP vector type goes through a private-memory temporary).
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kWSpec = 0, kWRepair = 2;
+constexpr int kWSpec = 0, kWFix = 1, kWRepair = 2;
 constexpr int kWU = 12;                 // rows per block (checkpoint spacing)
 constexpr int kWWaves = 16;             // waves per workgroup of the speculative pass
 constexpr int kWG = 1;                  // searches per wave
@@ -94,13 +94,17 @@ struct WaveArgs {
 // with t = 4c + u.  Rows t >= K and columns s >= K take row or column K-1: a
 // predecessor t >= K holds a capped word, so its candidate exceeds every exact
 // one without wrapping, and a state s >= K is padding.
-__global__ void wave_pack_kernel(const int32_t *__restrict__ rtab, int E, int K, uint32_t *__restrict__ rpk) {
+// Every R entry is read here, so the range check of R (entries in [0, limit))
+// is made on the way and flagged in the header.
+__global__ void wave_pack_kernel(const int32_t *__restrict__ rtab, int E, int K, uint32_t *__restrict__ rpk,
+                                 int32_t limit, WsHeader *__restrict__ hdr) {
   const size_t words = (size_t)E * 64 * 64;
   for (size_t w = blockIdx.x * (size_t)blockDim.x + threadIdx.x; w < words; w += (size_t)gridDim.x * blockDim.x) {
     const int u = (int)(w & 3), s = (int)((w >> 2) & 63), c = (int)((w >> 8) & 15), e = (int)(w >> 12);
     const int t = 4 * c + u;
-    const uint32_t r = (uint32_t)rtab[((size_t)e * K + min(t, K - 1)) * K + min(s, K - 1)];
-    rpk[w] = (r << kWBits) | (uint32_t)t;
+    const int32_t r = rtab[((size_t)e * K + min(t, K - 1)) * K + min(s, K - 1)];
+    if (r < 0 || r >= limit) hdr->rflag = 1;
+    rpk[w] = ((uint32_t)r << kWBits) | (uint32_t)t;
   }
 }
 
@@ -185,6 +189,7 @@ struct WaveSmem {
   static constexpr int CPT = kWTable16 / (64 * NW);  // 16-byte chunks per thread and table
   u32x4 tb[2][4][kWTable16];                          // packed tables of two quads of rows
   uint8_t argb[NW][kWG][kWU][64];                     // argmin bytes of the block's rows, per wave and search
+  uint32_t wact[2][NW];                               // fix-up: wave still has an unmet search, by quad parity
 };
 
 // State of a wave's searches.
@@ -194,6 +199,8 @@ struct WaveChains {
   uint64_t dsum[G];    // offset sum since the start row
   uint32_t flags[G];   // bit 0 a negative cost, bit 1 a row with no available strategy
   uint32_t cor[G];     // speculative pass: OR of the lane's costs (bit 31 = a negative cost)
+  int conv[G];         // fix-up: quad where the row met the checkpoint, -1 if never
+  uint64_t dconv[G];   // fix-up: offset sum at that quad
 };
 
 // Runs rows [12*blk0 (+1 for kSpec), min(12*blk1, N)) of the wave's G searches
@@ -202,11 +209,16 @@ struct WaveChains {
 //   kSpec:   the start row is row 12*blk0 from its costs alone; checkpoints are
 //            written.
 //   kRepair: the start row (row 12*blk0 - 1) is start[g].
+//   kFix:    as kRepair; at every quad end the row is compared with the
+//            speculative checkpoint of the same quad.  A search that has met
+//            it stops computing (its later speculative rows are the true ones)
+//            and the workgroup stops once all of its searches have met.
 template <int NW, int G, int MODE, int EP>
 __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, int blk0, int blk1,
                                          const uint32_t *const *start, WaveSmem<NW> &sm, WaveChains<G> &ch) {
   constexpr int U = kWU, CPT = WaveSmem<NW>::CPT;
   static_assert(G == 1 || G == 2, "one or two searches per wave");
+  static_assert(MODE != kWFix || G == 1, "the fix-up carries one search per wave");
   static_assert(CPT == 1 || CPT == 2 || CPT == 4, "1, 2 or 4 chunks per thread and table");
   const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int N = a.N, K = a.K;
@@ -306,7 +318,14 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
       ch.qv[g] = start[g][lane];
       ch.dsum[g] = 0;
     }
+    ch.conv[g] = valid(g) ? -1 : 0;  // a missing search counts as met
+    ch.dconv[g] = 0;
   }
+  int endr[G];  // last row whose argmin bytes are written back
+  uint32_t ckv[G] = {};  // fix-up: checkpoint of the current quad
+#pragma unroll
+  for (int g = 0; g < G; ++g) endr[g] = ilast;
+  bool stop = false;
   __syncthreads();  // the first quad's tables
 
   // Argmin bytes of rows [12 blk + r0, 12 blk + nr) of the wave's searches from
@@ -317,7 +336,8 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
     for (int g = 0; g < G; ++g) {
       if (!valid(g)) continue;
       uint8_t *dst = (g == 0 ? tb0 : tb1) + (size_t)blk * U * K;
-      for (int x = lane + 4 * r0; x < 4 * nr; x += 64) {  // piece x: row x / 4, bytes 16 (x % 4) ..
+      const int nrg = MODE == kWFix ? min(nr, endr[g] - blk * U + 1) : nr;
+      for (int x = lane + 4 * r0; x < 4 * nrg; x += 64) {  // piece x: row x / 4, bytes 16 (x % 4) ..
         const int r = x >> 2, c = (x & 3) * 16;
         const u32x4 v = *(const u32x4 *)&sm.argb[wid][g][r][c];
         if (K == 64) {
@@ -339,6 +359,7 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
     constexpr int J = decltype(Jc)::value, u = J & 3;
     constexpr bool GUARD = decltype(Gd)::value, FIRST = decltype(Fd)::value;
     const int i = blk * U + J;
+    if (MODE == kWFix && stop) return;
     if (GUARD && i > ilast) return;
     if (FIRST && i < i0) return;
     if (!FIRST || i >= (i0 & ~3) + 4) {  // the next quad's loads (the first quad's: prologue)
@@ -351,6 +372,10 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
       }
       if constexpr (u == 1) CFP_QLOAD(2)
       if constexpr (u == 2) CFP_QLOAD(3)
+    }
+    if (MODE == kWFix && u == 0) {  // this quad's checkpoint (runs start at a quad)
+#pragma unroll
+      for (int g = 0; g < G; ++g) ckv[g] = (a.ckrow + ((size_t)srch(g) * a.nq + (i >> 2)) * 64)[lane];
     }
     if (u == 3 && (!FIRST || i >= (i0 & ~3) + 4)) {  // costs two quads ahead, after this quad's table loads
       const int cbase = (i & ~3) + 8;
@@ -406,8 +431,9 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
       _Pragma("unroll") for (int cc_ = 0; cc_ < NPRE; ++cc_) wpre[cc_] = tb[kWTable16 + cc_ * 64 + lane]; \
     }                                                                                      \
   }
+    const bool live = MODE != kWFix || ch.conv[0] < 0;  // (one search per wave in the fix-up)
     if constexpr (G == 2) CFP_ROW(CFP_CH2)
-    else CFP_ROW(CFP_CH1, 0,)
+    else if (live) CFP_ROW(CFP_CH1, 0,)
 #undef CFP_ROW
 #undef CFP_CH1
 #undef CFP_CH2
@@ -415,6 +441,7 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
     // New row: add the cost, normalise by the row minimum, record the argmin.
 #pragma unroll
     for (int g = 0; g < G; ++g) {
+      if (MODE == kWFix && !live) continue;
       const uint32_t cv = cs[(J / 4) % 3][u][g];
       const bool avail = lane < K && cv != (uint32_t)CFP_COST_INF;
       if (MODE == kWSpec) ch.cor[g] |= cv;
@@ -437,7 +464,23 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
         const int qbase = (i & ~3) + 4;
         CFP_Q4(CFP_QSTORE)
       }
+      if (MODE == kWFix) {
+        if (ch.conv[0] < 0 && __ballot(ch.qv[0] != ckv[0]) == 0) {
+          ch.conv[0] = i >> 2;
+          ch.dconv[0] = ch.dsum[0];
+          endr[0] = i;
+        }
+        if (lane == 0) sm.wact[(i >> 2) & 1][wid] = ch.conv[0] < 0 ? 1u : 0u;
+      }
       __syncthreads();
+      if (MODE == kWFix) {  // every wave reads the same flags: a uniform decision
+        const uint32_t f = lane < NW ? sm.wact[(i >> 2) & 1][lane] : 0u;
+        stop = __ballot(f != 0) == 0;
+        if (stop) {
+          flush(blk, J + 1);
+          return;
+        }
+      }
       if (MODE == kWSpec) {
         const int q = i >> 2;
 #pragma unroll
@@ -472,8 +515,8 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
   }
   block(std::false_type{}, std::true_type{}, blk0);
   int blk = blk0 + 1;
-  for (; blk < full_end; ++blk) block(std::false_type{}, std::false_type{}, blk);
-  if (blk < blk1) block(std::true_type{}, std::false_type{}, blk);
+  for (; blk < full_end && !(MODE == kWFix && stop); ++blk) block(std::false_type{}, std::false_type{}, blk);
+  if (blk < blk1 && !(MODE == kWFix && stop)) block(std::true_type{}, std::false_type{}, blk);
 }
 
 // Speculative pass, grid (ceil(B/16), P).
@@ -494,145 +537,29 @@ __global__ __launch_bounds__(64 * kWWaves) void chain_wave_kernel(WaveArgs a) {
   }
 }
 
-// Fix-up pass with independent waves.  Each wave carries two searches of one
-// chunk p >= 1, starting from the last checkpoint row of chunk p-1, and reads
-// the packed tables of every row straight from the table array (a few hundred
-// KiB that stays in the caches; every chunk starts at a multiple of 12 rows, so
-// all waves walk the same table sequence), one row ahead.  A wave stops at the
-// first quad end where both of its searches have met a checkpoint, so a slowly
-// converging search runs on alone instead of holding a workgroup of others.
-// Grid (ceil(B / (2 kWFixWaves)), P - 1); no barriers.
-constexpr int kWFixWaves = 4;
-
+// Fix-up pass, grid (ceil(B/16), P-1): the sixteen searches of a workgroup
+// rerun chunk p >= 1 from the last checkpoint row of chunk p-1 (their true row
+// once chunk p-1 has met) until each row equals chunk p's checkpoint at a quad
+// end; the tables are staged once per quad for all sixteen, a search that has
+// met stops computing, and the workgroup stops when all have met.
 template <int EP>
-__global__ __launch_bounds__(64 * kWFixWaves) void chain_wave_fix_kernel(WaveArgs a) {
+__global__ __launch_bounds__(64 * kWWaves) void chain_wave_fix_kernel(WaveArgs a) {
+  __shared__ __align__(16) WaveSmem<kWWaves> sm;
   const int lane = threadIdx.x & 63, wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int bw = (blockIdx.x * kWFixWaves + wid) * 2;
-  if (bw >= a.B) return;  // the whole wave
-  const bool two = bw + 1 < a.B;
-  const int b1 = two ? bw + 1 : bw;
+  const int bw = blockIdx.x * kWWaves + wid;  // one search per wave
   const int p = blockIdx.y + 1;
   const int blk0 = p * a.CB, blk1 = min(blk0 + a.CB, a.nblk);
-  const int N = a.N, K = a.K;
-  const int i0 = blk0 * kWU, ilast = min(blk1 * kWU, N) - 1;  // i0 is a multiple of 4
-  const int sl = min(lane, K - 1);
-  auto edge = [&](int row) __attribute__((always_inline)) { return EP ? row % (EP ? EP : 1) : a.redge[row]; };
-  const int32_t *cb0 = a.cost + (size_t)bw * N * K;  // wave-uniform bases
-  const int32_t *cb1 = a.cost + (size_t)b1 * N * K;
-  uint8_t *tb0 = a.table + (size_t)bw * N * K;
-  uint8_t *tb1 = a.table + (size_t)b1 * N * K;
-  const uint32_t *ck0 = a.ckrow + (size_t)bw * a.nq * 64;
-  const uint32_t *ck1 = a.ckrow + (size_t)b1 * a.nq * 64;
-
-  uint32_t qv[2] = {(ck0 + (size_t)(i0 / 4 - 1) * 64)[lane], (ck1 + (size_t)(i0 / 4 - 1) * 64)[lane]};
-  uint64_t dsum[2] = {0, 0}, dconv[2] = {0, 0};
-  int conv[2] = {-1, two ? -1 : 0};  // a missing second search counts as met
-
-  u32x4 wA[16], wB[16];
-  auto tload = [&](u32x4(&w)[16], int row) __attribute__((always_inline)) {
-    const u32x4 *src = a.rpk + (size_t)edge(row) * kWTable16;
-#pragma unroll
-    for (int c = 0; c < 16; ++c) w[c] = src[lane + c * 64];
-  };
-  // Memory schedule.  Loads complete in issue order, so a load issued before
-  // the tables of row r+1 must be back when row r+1 starts.  The next row's
-  // tables come first in every row, then the costs two rows ahead (a ring of
-  // four rows, [search][row mod 4]) and, in the first row of a quad, the
-  // quad's checkpoint row: each has a whole row of compute to arrive.
-  uint32_t cr[2][4];
-  auto cload = [&](int row, int slot) __attribute__((always_inline)) {
-    const int r = min(row, ilast);
-    cr[0][slot] = (uint32_t)(cb0 + (size_t)r * K)[sl];
-    cr[1][slot] = (uint32_t)(cb1 + (size_t)r * K)[sl];
-  };
-  uint32_t ckv[2] = {0, 0};
-
-  // One row i (u = i mod 4) with the tables in w; the next row's tables go to wn.
-  auto row = [&](int i, auto Uc, u32x4(&w)[16], u32x4(&wn)[16]) __attribute__((always_inline)) {
-    constexpr int u = decltype(Uc)::value;
-    if (i < ilast) tload(wn, i + 1);
-    cload(i + 2, (u + 2) & 3);
-    if (u == 0) {
-      ckv[0] = (ck0 + (size_t)(i >> 2) * 64)[lane];
-      ckv[1] = (ck1 + (size_t)(i >> 2) * 64)[lane];
-    }
-    const bool act[2] = {conv[0] < 0, conv[1] < 0};
-    uint32_t c0[2], c1[2], c2[2], c3[2], acc[2];
-#pragma unroll
-    for (int g = 0; g < 2; ++g) {
-      if (!act[g]) continue;
-      const auto pp = __builtin_amdgcn_permlane16_swap(qv[g], qv[g], false, false);
-      const auto lo = __builtin_amdgcn_permlane32_swap(pp[0], pp[0], false, false);
-      const auto hi = __builtin_amdgcn_permlane32_swap(pp[1], pp[1], false, false);
-      c0[g] = lo[0];
-      c2[g] = lo[1];
-      c1[g] = hi[0];
-      c3[g] = hi[1];
-      acc[g] = kSat;
-    }
-#define CFP_CH2(C, cc_) cand4_g2<4 * ((cc_) & 3), ((cc_) & 3) == 0>(acc[0], acc[1], C[0], C[1], w[cc_]);
-#define CFP_CH1(X, C, cc_)                                                  \
-  if constexpr ((cc_) == 0) cand4_g1_first(acc[X], C[X], w[0]);             \
-  else cand4_g1<4 * ((cc_) & 3), ((cc_) & 3) == 0>(acc[X], C[X], w[cc_]);
-#define CFP_ROW(CH, ...)                                                                        \
-  {                                                                                             \
-    CH(__VA_ARGS__ c0, 0) CH(__VA_ARGS__ c0, 1) CH(__VA_ARGS__ c0, 2) CH(__VA_ARGS__ c0, 3)     \
-    CH(__VA_ARGS__ c1, 4) CH(__VA_ARGS__ c1, 5) CH(__VA_ARGS__ c1, 6) CH(__VA_ARGS__ c1, 7)     \
-    CH(__VA_ARGS__ c2, 8) CH(__VA_ARGS__ c2, 9) CH(__VA_ARGS__ c2, 10) CH(__VA_ARGS__ c2, 11)   \
-    CH(__VA_ARGS__ c3, 12) CH(__VA_ARGS__ c3, 13) CH(__VA_ARGS__ c3, 14) CH(__VA_ARGS__ c3, 15) \
-  }
-    if (act[0] && act[1]) CFP_ROW(CFP_CH2)
-    else if (act[0]) CFP_ROW(CFP_CH1, 0,)
-    else if (act[1]) CFP_ROW(CFP_CH1, 1,)
-#undef CFP_ROW
-#undef CFP_CH1
-#undef CFP_CH2
-#pragma unroll
-    for (int g = 0; g < 2; ++g) {
-      if (!act[g]) continue;
-      const uint32_t cv = cr[g][u];
-      const bool avail = lane < K && cv != (uint32_t)CFP_COST_INF;
-      const uint32_t x = avail ? (acc[g] >> kWBits) + cv : kWX;
-      const uint32_t d = wave_min64_s(x);
-      qv[g] = umin(x - d, kWQcap6 >> kWBits) << kWBits;
-      dsum[g] += d;
-      if (lane < K) ((g == 0 ? tb0 : tb1) + (size_t)i * K)[lane] = (uint8_t)acc[g];
-    }
-  };
-
-  tload(wA, i0);
-  cload(i0, 0);
-  cload(i0 + 1, 1);
-  using U0 = std::integral_constant<int, 0>;
-  using U1 = std::integral_constant<int, 1>;
-  using U2 = std::integral_constant<int, 2>;
-  using U3 = std::integral_constant<int, 3>;
-  for (int q0 = i0; q0 <= ilast; q0 += 4) {
-    row(q0, U0{}, wA, wB);
-    if (q0 + 1 <= ilast) row(q0 + 1, U1{}, wB, wA);
-    if (q0 + 2 <= ilast) row(q0 + 2, U2{}, wA, wB);
-    if (q0 + 3 <= ilast) row(q0 + 3, U3{}, wB, wA);
-    // Quad end: meet the speculative checkpoint of the same quad.
-    const int q = min(q0 + 3, ilast) >> 2;
-#pragma unroll
-    for (int g = 0; g < 2; ++g) {
-      if (conv[g] < 0 && __ballot(qv[g] != ckv[g]) == 0) {
-        conv[g] = q;
-        dconv[g] = dsum[g];
-      }
-    }
-    if (conv[0] >= 0 && conv[1] >= 0) break;
-  }
-#pragma unroll
-  for (int g = 0; g < 2; ++g) {
-    if (g == 1 && !two) continue;
-    const int b = bw + g;
-    if (conv[g] < 0) a.endrow[((size_t)b * a.P + p) * 64 + lane] = qv[g];
-    if (lane == 0) {
-      WaveRec &r = a.rec[(size_t)b * a.P + p];
-      r.conv = conv[g];
-      r.dfix = (int64_t)(conv[g] >= 0 ? dconv[g] : dsum[g]);
-    }
+  const int i0 = blk0 * kWU;  // a multiple of 4
+  const int b = min(bw, a.B - 1);
+  const uint32_t *start[1] = {a.ckrow + ((size_t)b * a.nq + (i0 / 4 - 1)) * 64};
+  WaveChains<1> ch;
+  wave_run<kWWaves, 1, kWFix, EP>(a, bw, 1, blk0, blk1, start, sm, ch);
+  if (bw >= a.B) return;
+  if (ch.conv[0] < 0) a.endrow[((size_t)bw * a.P + p) * 64 + lane] = ch.qv[0];
+  if (lane == 0) {
+    WaveRec &r = a.rec[(size_t)bw * a.P + p];
+    r.conv = ch.conv[0];
+    r.dfix = (int64_t)(ch.conv[0] >= 0 ? ch.dconv[0] : ch.dsum[0]);
   }
 }
 
@@ -736,8 +663,8 @@ static void launch_wave_passes(const WaveArgs &a, const WsHeader *hdr, SearchRes
   timer_begin(st);
   hipLaunchKernelGGL((chain_wave_kernel<EP>), dim3(rows, a.P), dim3(64 * kWWaves), 0, st, a);
   timer_end(st);
-  hipLaunchKernelGGL((chain_wave_fix_kernel<EP>), dim3((a.B + 2 * kWFixWaves - 1) / (2 * kWFixWaves), a.P - 1),
-                     dim3(64 * kWFixWaves), 0, st, a);
+  hipLaunchKernelGGL((chain_wave_fix_kernel<EP>), dim3((a.B + kWWaves - 1) / kWWaves, a.P - 1), dim3(64 * kWWaves), 0,
+                     st, a);
   hipLaunchKernelGGL((chain_wave_final_kernel<EP>), dim3(a.B), dim3(64 * kWFinalWaves), 0, st, a, hdr, res, opt,
                      status);
 }
@@ -794,7 +721,7 @@ hipError_t launch_chain_wave(const cfp_chain_desc &d, const int32_t *redge_dev, 
   off += align_up((size_t)d.batch * c.nq * 64 * 4);
   a.endrow = (uint32_t *)(region + off);
   hipLaunchKernelGGL(wave_pack_kernel, dim3(std::min(1024, d.n_tables * 16)), dim3(256), 0, st, d.rtab, d.n_tables,
-                     d.k, rpk);
+                     d.k, rpk, cfp_r_limit(CFP_V_CHAIN, d.k), const_cast<WsHeader *>(hdr));
   if (wave_edge_period(d.redge, d.n_blocks, d.n_tables) == 12) launch_wave_passes<12>(a, hdr, res, opt, status, st);
   else launch_wave_passes<0>(a, hdr, res, opt, status, st);
   return hipGetLastError();

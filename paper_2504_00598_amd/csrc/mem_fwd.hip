@@ -84,13 +84,22 @@ __global__ __launch_bounds__(256) void mem_prep_kernel(const int32_t *__restrict
 }
 
 // Resharding tables transposed and packed: rpT[e][s][t] = (R[e][t][s] << b) | t.
+// Every R entry is read here, so the range check of R (entries in [0, limit))
+// is made on the way and flagged in the header.
 template <int KP>
-__global__ void mem_pack_rtab_kernel(const int32_t *__restrict__ rtab, int E, int K, uint32_t *__restrict__ rpT) {
+__global__ void mem_pack_rtab_kernel(const int32_t *__restrict__ rtab, int E, int K, uint32_t *__restrict__ rpT,
+                                     int32_t limit, WsHeader *__restrict__ hdr) {
   constexpr int BITS = Pow2Bits<KP>::value;
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= E * KP * KP) return;
   const int e = idx / (KP * KP), s = (idx / KP) % KP, t = idx % KP;
-  rpT[idx] = (s < K && t < K) ? (((uint32_t)rtab[((size_t)e * K + t) * K + s] << BITS) | (uint32_t)t) : kSat;
+  uint32_t v = kSat;
+  if (s < K && t < K) {
+    const int32_t r = rtab[((size_t)e * K + t) * K + s];
+    if (r < 0 || r >= limit) hdr->rflag = 1;
+    v = ((uint32_t)r << BITS) | (uint32_t)t;
+  }
+  rpT[idx] = v;
 }
 
 struct MemWs {
@@ -547,7 +556,8 @@ static void launch_mem(const cfp_chain_desc &d, const uint8_t *mem, int n_mem, c
   const int N = d.n_blocks, K = d.k, B = d.batch, E = d.n_tables;
   MemWs w = carve(region, N, K, B, n_mem);
   hipLaunchKernelGGL(mem_init_kernel, dim3(64), dim3(256), 0, st, w.mflags, B, w.pub, B * w.nchunk);
-  hipLaunchKernelGGL(mem_pack_rtab_kernel<KP>, dim3((E * KP * KP + 255) / 256), dim3(256), 0, st, d.rtab, E, K, w.rpT);
+  hipLaunchKernelGGL(mem_pack_rtab_kernel<KP>, dim3((E * KP * KP + 255) / 256), dim3(256), 0, st, d.rtab, E, K, w.rpT,
+                     cfp_r_limit(CFP_V_MEM, K), const_cast<WsHeader *>(hdr));
   hipLaunchKernelGGL(mem_prep_kernel<KP>, dim3((B * N + 3) / 4), dim3(256), 0, st, d.cost, mem, budget, N, K, n_mem, B,
                      w.srec, mem_copy, w.mflags);
   timer_begin(st);

@@ -137,6 +137,25 @@ def test_traceback_lds_and_memory_paths(N, K, B):
     assert_chain_parity(cost, rtab, redge, f"traceback N={N} K={K}")
 
 
+# The chunk-parallel paths check the range of R while packing it (the other
+# paths in a separate pass): an entry at cfp_r_limit or below 0 marks every
+# search of the call as bad input.
+@pytest.mark.parametrize("N,K,B,bad", [(400, 64, 70, "limit"), (400, 64, 70, "negative"),
+                                       (200, 256, 9, "limit"), (200, 256, 9, "negative"),
+                                       (20, 16, 3, "limit")])
+def test_resharding_range_checked_on_every_path(N, K, B, bad):
+    need_gpu()
+    from paper_2504_00598_amd import CFP_ST_BADINPUT, cfp_r_limit
+    say("R range", N, K, B, bad)
+    cost, rtab, redge = rand_case([48, N, K], B, N, K, 12, 0, 1000)
+    redge = (np.arange(N) % 12).astype(np.int32)
+    opt, st, plan = run_chain(cost, rtab, redge)
+    assert (st == 0).all()
+    rtab[7, K - 1, K // 2] = cfp_r_limit(0, K) if bad == "limit" else -1
+    opt, st, plan = run_chain(cost, rtab, redge)
+    assert (st == CFP_ST_BADINPUT).all() and (opt == np.iinfo(np.int64).max).all() and (plan == -1).all()
+
+
 # K > 64 runs on one of two kernels: the split kernel (each search over P = K_P^2 / 4096
 # workgroups, K_P the padded K, tables in registers) when all B * P workgroups fit the
 # device's 256 compute units and there are at most 12 tables, else the wide kernel (one

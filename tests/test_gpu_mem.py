@@ -88,6 +88,17 @@ def test_budget_out_of_range_is_bad_input():
     assert st[0] == 0 and st[1] == CFP_ST_BADINPUT
 
 
+@pytest.mark.parametrize("bad", ["limit", "negative"])
+def test_resharding_out_of_range_is_bad_input(bad):
+    """The memory forward checks the range of R while packing it."""
+    need_gpu()
+    from paper_2504_00598_amd import CFP_ST_BADINPUT, cfp_r_limit
+    cost, rtab, redge, mem = mem_case(14, 3, 30, 32, 3, 0, 100, 0, 4, 64)
+    rtab[2, 31, 5] = cfp_r_limit(1, 32) if bad == "limit" else -1
+    opt, st, plan = run_mem(cost, rtab, redge, mem, 64, np.array([63, 40, 20], np.int32))
+    assert (st == CFP_ST_BADINPUT).all() and (plan == -1).all()
+
+
 def test_periodic_layers():
     """Repeated layers (the same costs and memory every 12 blocks): many tied
     plans at every budget."""
