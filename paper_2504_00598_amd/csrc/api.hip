@@ -64,27 +64,36 @@ WsLayout layout(int variant, int n, int k, int batch, int n_mem, int n_tables) {
 }
 
 // Benchmarking timer (cfp_timer_start / cfp_timer_stop).  Slot 2j and 2j+1
-// hold the events around the j-th recorded launch.
+// hold the start and stop events of the j-th timed launch.
 namespace {
 std::mutex g_timer_mu;
 std::atomic<bool> g_timer_on{false};
 std::vector<hipEvent_t> g_timer_ev;
 size_t g_timer_used = 0;
-bool g_timer_open = false;
+bool g_timer_open = false;  // armed for the next timed_launch
 }  // namespace
 
-void timer_begin(hipStream_t st) {
+void timer_begin(hipStream_t) {
   if (!g_timer_on.load(std::memory_order_acquire)) return;
   std::lock_guard<std::mutex> lk(g_timer_mu);
-  g_timer_open = 2 * g_timer_used + 1 < g_timer_ev.size() &&
-                 hipEventRecord(g_timer_ev[2 * g_timer_used], st) == hipSuccess;
+  g_timer_open = true;
 }
 
-void timer_end(hipStream_t st) {
+void timer_end(hipStream_t) {
   if (!g_timer_on.load(std::memory_order_acquire)) return;
   std::lock_guard<std::mutex> lk(g_timer_mu);
-  if (g_timer_open && hipEventRecord(g_timer_ev[2 * g_timer_used + 1], st) == hipSuccess) ++g_timer_used;
   g_timer_open = false;
+}
+
+bool timer_take(hipEvent_t *e0, hipEvent_t *e1) {
+  if (!g_timer_on.load(std::memory_order_acquire)) return false;
+  std::lock_guard<std::mutex> lk(g_timer_mu);
+  if (!g_timer_open || 2 * g_timer_used + 1 >= g_timer_ev.size()) return false;
+  *e0 = g_timer_ev[2 * g_timer_used];
+  *e1 = g_timer_ev[2 * g_timer_used + 1];
+  ++g_timer_used;
+  g_timer_open = false;
+  return true;
 }
 
 }  // namespace cfp
@@ -223,10 +232,13 @@ int cfp_dp_chain(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t *op
   if (!ws || ws_bytes < L.total) return CFP_ERR_WORKSPACE;
   hipStream_t st = (hipStream_t)stream;
   uint8_t *w = (uint8_t *)ws;
-  if ((rc = upload_header(d, CFP_V_CHAIN, 0, L, ws, st)) != CFP_OK) return rc;
   WsHeader *hdr = (WsHeader *)w;
-  // The chunk-parallel paths check the range of R while packing it.
+  // The chunk-parallel paths check the range of R while packing it; the K <= 64
+  // one with a periodic edge map reads nothing of the header, which is then not
+  // uploaded (a host-to-device copy costs several microseconds of GPU time).
   const bool wave = chain_wave_supported(d->n_blocks, d->k, d->n_tables, d->batch);
+  if (!(wave && chain_wave_headerless(*d)) && (rc = upload_header(d, CFP_V_CHAIN, 0, L, ws, st)) != CFP_OK)
+    return rc;
   const bool cw = !wave && chain_cw_supported(d->n_blocks, d->k, d->batch);
   if (!wave && !cw &&
       launch_validate_rtab(d->rtab, d->n_tables, d->k, cfp_r_limit(CFP_V_CHAIN, d->k), hdr, st) != hipSuccess)

@@ -1,6 +1,7 @@
 // Internal layout and launcher declarations of libcfp (not installed).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -25,7 +26,10 @@ struct WsHeader {
   uint32_t magic;
   int32_t variant, n, k, batch, n_mem, elem;  // elem: bytes per argmin entry
   int32_t rflag;                               // set to 1 by the device if rtab breaks its range
-  int32_t pad[56];
+  // Paths that do not upload the header flag a range error with the number of
+  // the call instead (no reset needed: a stale value never equals a new number).
+  uint64_t rseq;
+  int32_t pad[54];
 };
 static_assert(sizeof(WsHeader) == 256, "header is 256 bytes");
 
@@ -75,6 +79,9 @@ hipError_t launch_chain_fwd(const cfp_chain_desc &d, const int32_t *redge_dev, u
                             int32_t *status, hipStream_t st);
 bool chain_wave_supported(int n, int k, int n_tables, int batch);
 size_t wave_region_bytes(int n, int k, int n_tables, int batch);
+// True when the chunk-parallel K <= 64 path reads nothing of the uploaded
+// header (periodic edge map, range errors flagged by call number).
+bool chain_wave_headerless(const cfp_chain_desc &d);
 hipError_t launch_chain_wave(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *region, uint8_t *table,
                              SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
                              hipStream_t st);
@@ -120,7 +127,20 @@ size_t scan_region_bytes(int n, int k, int batch);
 
 // Benchmarking timer: when armed, brackets each launch of a forward call's
 // main kernel with a pair of HIP events on that launch's stream.
+// Benchmarking timer: between timer_begin and timer_end the next timed_launch
+// is timed by events attached to its dispatch (hipExtLaunchKernel), so the
+// measured span is the kernel's own, without the gaps that separate event
+// records add to a stream.
 void timer_begin(hipStream_t st);
 void timer_end(hipStream_t st);
+bool timer_take(hipEvent_t *e0, hipEvent_t *e1);
+
+template <typename... Args, typename... Params>
+inline void timed_launch(void (*kernel)(Params...), dim3 grid, dim3 block, uint32_t shmem, hipStream_t st,
+                         Args... args) {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  timer_take(&e0, &e1);
+  hipExtLaunchKernelGGL(kernel, grid, block, shmem, st, e0, e1, 0u, args...);
+}
 
 }  // namespace cfp

@@ -585,7 +585,7 @@ hipError_t launch_chain_cw(const cfp_chain_desc &d, const int32_t *redge_dev, ui
                    const_cast<WsHeader *>(hdr));
   const int groups = (d.batch + kCG - 1) / kCG;
   timer_begin(st);
-  hipLaunchKernelGGL(chain_cw_kernel<kCSpec>, dim3(groups, c.P), dim3(kCThreads), 0, st, a);
+  timed_launch(chain_cw_kernel<kCSpec>, dim3(groups, c.P), dim3(kCThreads), 0, st, a);
   timer_end(st);
   hipLaunchKernelGGL(chain_cw_kernel<kCFix>, dim3(groups, c.P - 1), dim3(kCThreads), 0, st, a);
   hipLaunchKernelGGL(chain_cw_final_kernel, dim3(d.batch), dim3(kCThreads), 0, st, a, hdr, res, opt, status);

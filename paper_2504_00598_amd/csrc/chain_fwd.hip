@@ -176,7 +176,7 @@ __global__ __launch_bounds__(kThreads) void chain_fwd_kernel(
 template <int KP>
 static void launch_kp(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *table, SearchResult *res,
                       const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st) {
-  hipLaunchKernelGGL(chain_fwd_kernel<KP>, dim3(d.batch), dim3(kThreads), 0, st, d.cost, d.rtab, redge_dev,
+  timed_launch(chain_fwd_kernel<KP>, dim3(d.batch), dim3(kThreads), 0, st, d.cost, d.rtab, redge_dev,
                      d.n_blocks, d.k, table, res, hdr, opt, status);
 }
 

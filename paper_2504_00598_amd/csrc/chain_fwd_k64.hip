@@ -172,7 +172,7 @@ __global__ __launch_bounds__(kThreads, 1) void chain_fwd_k64_kernel(
 template <int EP>
 static void launch_k64_ep(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *table, SearchResult *res,
                           const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st) {
-  hipLaunchKernelGGL((chain_fwd_k64_kernel<EP>), dim3(d.batch), dim3(kThreads), 0, st, d.cost, d.rtab, redge_dev,
+  timed_launch(chain_fwd_k64_kernel<EP>, dim3(d.batch), dim3(kThreads), 0, st, d.cost, d.rtab, redge_dev,
                      d.n_blocks, d.k, d.n_tables, table, res, hdr, opt, status);
 }
 

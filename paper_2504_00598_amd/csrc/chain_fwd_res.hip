@@ -223,7 +223,7 @@ template <int KP>
 static void launch_res(const cfp_chain_desc &d, int period, const int32_t *redge_dev, uint8_t *table,
                        SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st) {
 #define CFP_LAUNCH(EP)                                                                                      \
-  hipLaunchKernelGGL((chain_fwd_res_kernel<KP, EP>), dim3(d.batch), dim3(kThreads), 0, st, d.cost, d.rtab, \
+  timed_launch(chain_fwd_res_kernel<KP, EP>, dim3(d.batch), dim3(kThreads), 0, st, d.cost, d.rtab, \
                      redge_dev, d.n_blocks, d.k, d.n_tables, table, res, hdr, opt, status)
   switch (period) {
     case 1: CFP_LAUNCH(1); break;

@@ -448,14 +448,14 @@ static void launch_split_kp(const cfp_chain_desc &d, const int32_t *redge_dev, u
   hipLaunchKernelGGL(split_init_kernel, dim3(64), dim3(256), 0, st, xb, nxb, sflags, d.batch);
   if (split_form(d.k, d.n_tables, d.batch) == 1) {
     timer_begin(st);
-    hipLaunchKernelGGL(chain_fwd_split_kernel<KP>, dim3(d.batch * SplitShape<KP>::P), dim3(kSplitThreads), 0, st,
+    timed_launch(chain_fwd_split_kernel<KP>, dim3(d.batch * SplitShape<KP>::P), dim3(kSplitThreads), 0, st,
                        d.cost, d.rtab, redge_dev, d.n_blocks, d.k, d.n_tables, table, xb, sflags, res, hdr, opt,
                        status);
     timer_end(st);
   } else {
     launch_pack_rtab(d.rtab, d.n_tables, d.k, KP, Pow2Bits<KP>::value, rpk, st);
     timer_begin(st);
-    hipLaunchKernelGGL(chain_fwd_splitw_kernel<KP>, dim3(d.batch * SplitWShape<KP>::P), dim3(kSplitWThreads), 0,
+    timed_launch(chain_fwd_splitw_kernel<KP>, dim3(d.batch * SplitWShape<KP>::P), dim3(kSplitWThreads), 0,
                        st, d.cost, rpk, redge_dev, d.n_blocks, d.k, table, xb, sflags, res, hdr, opt, status);
     timer_end(st);
   }

@@ -290,8 +290,8 @@ static void launch_wide_kp(const cfp_chain_desc &d, const int32_t *redge_dev, ui
   const int rows = d.batch * d.n_blocks;
   hipLaunchKernelGGL(row_cmin_kernel, dim3((rows + 3) / 4), dim3(256), 0, st, d.cost, rows, d.k, rowcmin);
   timer_begin(st);
-  hipLaunchKernelGGL(chain_fwd_wide_kernel<KP>, dim3(d.batch), dim3(kWideThreads), 0, st, d.cost, rowcmin, rpk,
-                     redge_dev, d.n_blocks, d.k, table, res, hdr, opt, status);
+  timed_launch(chain_fwd_wide_kernel<KP>, dim3(d.batch), dim3(kWideThreads), 0, st, d.cost, (const int32_t *)rowcmin,
+               (const uint32_t *)rpk, redge_dev, d.n_blocks, d.k, table, res, hdr, opt, status);
   timer_end(st);
 }
 

@@ -50,6 +50,7 @@
 // four are staged while these are used (double buffer, one barrier per four
 // rows); a wave's two searches share every table read.
 #include <algorithm>
+#include <atomic>
 
 #include "res_common.h"
 
@@ -88,6 +89,7 @@ struct WaveArgs {
   int64_t *dck;         // speculative offset sum (from the chunk's start row) at every checkpoint [B][nq]
   uint32_t *ckrow;      // speculative row at every checkpoint (end of a quad of rows) [B][nq][64]
   uint32_t *endrow;     // fix-up end row of chunks that met no checkpoint [B][P][64]
+  uint64_t seq;         // number of this call: a range error in R is flagged as hdr->rseq = seq
 };
 
 // Packed tables: word u of chunk c of lane s of table e is (R_e[t][s] << 6) | t
@@ -95,15 +97,15 @@ struct WaveArgs {
 // predecessor t >= K holds a capped word, so its candidate exceeds every exact
 // one without wrapping, and a state s >= K is padding.
 // Every R entry is read here, so the range check of R (entries in [0, limit))
-// is made on the way and flagged in the header.
+// is made on the way and flagged in the header as the call's number.
 __global__ void wave_pack_kernel(const int32_t *__restrict__ rtab, int E, int K, uint32_t *__restrict__ rpk,
-                                 int32_t limit, WsHeader *__restrict__ hdr) {
+                                 int32_t limit, WsHeader *__restrict__ hdr, uint64_t seq) {
   const size_t words = (size_t)E * 64 * 64;
   for (size_t w = blockIdx.x * (size_t)blockDim.x + threadIdx.x; w < words; w += (size_t)gridDim.x * blockDim.x) {
     const int u = (int)(w & 3), s = (int)((w >> 2) & 63), c = (int)((w >> 8) & 15), e = (int)(w >> 12);
     const int t = 4 * c + u;
     const int32_t r = rtab[((size_t)e * K + min(t, K - 1)) * K + min(s, K - 1)];
-    if (r < 0 || r >= limit) hdr->rflag = 1;
+    if (r < 0 || r >= limit) hdr->rseq = seq;
     rpk[w] = ((uint32_t)r << kWBits) | (uint32_t)t;
   }
 }
@@ -627,7 +629,7 @@ __global__ __launch_bounds__(64 * kWFinalWaves, 1) void chain_wave_final_kernel(
   if (lane == 0) {
     const int fl = s_flags;
     int st = CFP_ST_OK;
-    if ((fl & 1) || hdr->rflag) st = CFP_ST_BADINPUT;
+    if ((fl & 1) || hdr->rseq == a.seq) st = CFP_ST_BADINPUT;
     else if (fl & 2) st = CFP_ST_INFEASIBLE;
     else if ((pk >> kWBits) != 0) st = CFP_ST_OVERFLOW;
     status[b] = st;
@@ -661,7 +663,7 @@ static void launch_wave_passes(const WaveArgs &a, const WsHeader *hdr, SearchRes
                                int32_t *status, hipStream_t st) {
   const int rows = (a.B + kWWaves * kWG - 1) / (kWWaves * kWG);
   timer_begin(st);
-  hipLaunchKernelGGL((chain_wave_kernel<EP>), dim3(rows, a.P), dim3(64 * kWWaves), 0, st, a);
+  timed_launch(chain_wave_kernel<EP>, dim3(rows, a.P), dim3(64 * kWWaves), 0, st, a);
   timer_end(st);
   hipLaunchKernelGGL((chain_wave_fix_kernel<EP>), dim3((a.B + kWWaves - 1) / kWWaves, a.P - 1), dim3(64 * kWWaves), 0,
                      st, a);
@@ -679,6 +681,10 @@ static int wave_edge_period(const int32_t *redge, int n, int e) {
 }
 
 }  // namespace
+
+bool chain_wave_headerless(const cfp_chain_desc &d) {
+  return wave_edge_period(d.redge, d.n_blocks, d.n_tables) == 12;
+}
 
 bool chain_wave_supported(int n, int k, int e, int batch) { return wave_plan(n, k, e, batch).P >= 2; }
 
@@ -720,8 +726,10 @@ hipError_t launch_chain_wave(const cfp_chain_desc &d, const int32_t *redge_dev, 
   a.ckrow = (uint32_t *)(region + off);
   off += align_up((size_t)d.batch * c.nq * 64 * 4);
   a.endrow = (uint32_t *)(region + off);
+  static std::atomic<uint64_t> call_seq{0};
+  a.seq = call_seq.fetch_add(1, std::memory_order_relaxed) + 1;  // never 0, which an upload writes
   hipLaunchKernelGGL(wave_pack_kernel, dim3(std::min(1024, d.n_tables * 16)), dim3(256), 0, st, d.rtab, d.n_tables,
-                     d.k, rpk, cfp_r_limit(CFP_V_CHAIN, d.k), const_cast<WsHeader *>(hdr));
+                     d.k, rpk, cfp_r_limit(CFP_V_CHAIN, d.k), const_cast<WsHeader *>(hdr), a.seq);
   if (wave_edge_period(d.redge, d.n_blocks, d.n_tables) == 12) launch_wave_passes<12>(a, hdr, res, opt, status, st);
   else launch_wave_passes<0>(a, hdr, res, opt, status, st);
   return hipGetLastError();

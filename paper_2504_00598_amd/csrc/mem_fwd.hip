@@ -561,8 +561,8 @@ static void launch_mem(const cfp_chain_desc &d, const uint8_t *mem, int n_mem, c
   hipLaunchKernelGGL(mem_prep_kernel<KP>, dim3((B * N + 3) / 4), dim3(256), 0, st, d.cost, mem, budget, N, K, n_mem, B,
                      w.srec, mem_copy, w.mflags);
   timer_begin(st);
-  hipLaunchKernelGGL(mem_fwd_kernel<KP>, dim3(B * w.nchunk), dim3(kMemThreads), 0, st, redge_dev, budget, w.srec, w.rpT, N, K,
-                     n_mem, B, w, table, res, hdr, opt, status, frontier);
+  timed_launch(mem_fwd_kernel<KP>, dim3(B * w.nchunk), dim3(kMemThreads), 0, st, redge_dev, budget,
+               (const uint2 *)w.srec, (const uint32_t *)w.rpT, N, K, n_mem, B, w, table, res, hdr, opt, status, frontier);
   timer_end(st);
 }
 

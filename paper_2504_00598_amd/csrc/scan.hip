@@ -528,11 +528,11 @@ hipError_t launch_scan(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_
       const bool full = K == KP && ((uintptr_t)d.cost % 16) == 0 && ((uintptr_t)d.rtab % 16) == 0;
       timer_begin(st);
       if (l == 1) {
-        if (full) hipLaunchKernelGGL((scan_gemm_kernel<true, true>), grid, dim3(256), 0, st, a);
-        else hipLaunchKernelGGL((scan_gemm_kernel<true, false>), grid, dim3(256), 0, st, a);
+        if (full) timed_launch(scan_gemm_kernel<true, true>, grid, dim3(256), 0, st, a);
+        else timed_launch(scan_gemm_kernel<true, false>, grid, dim3(256), 0, st, a);
       } else {
-        if (full) hipLaunchKernelGGL((scan_gemm_kernel<false, true>), grid, dim3(256), 0, st, a);
-        else hipLaunchKernelGGL((scan_gemm_kernel<false, false>), grid, dim3(256), 0, st, a);
+        if (full) timed_launch(scan_gemm_kernel<false, true>, grid, dim3(256), 0, st, a);
+        else timed_launch(scan_gemm_kernel<false, false>, grid, dim3(256), 0, st, a);
       }
       timer_end(st);
     }

@@ -163,7 +163,7 @@ template <int SPL>
 static void launch_seg_spl(const cfp_segment_desc &d, const int32_t *redge_dev, uint8_t *table, SearchResult *res,
                            const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st) {
   const int grid = (d.batch + kSegWaves - 1) / kSegWaves;
-  hipLaunchKernelGGL(seg_fwd_kernel<SPL>, dim3(grid), dim3(kSegWaves * 64), 0, st, d.cost, d.rbound, d.last,
+  timed_launch(seg_fwd_kernel<SPL>, dim3(grid), dim3(kSegWaves * 64), 0, st, d.cost, d.rbound, d.last,
                      d.first, redge_dev, d.n_segments, d.k, d.batch, d.n_last, d.n_first, index_bits(d.k), table,
                      res, hdr, opt, status);
 }
