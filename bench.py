@@ -58,15 +58,15 @@ COMMON_SOURCES = ["common.h", "cfp_internal.h", "../../include/cfp.h"]
 # changed and the figure is withheld.
 FETCH_SCALE, WRITE_SCALE = 524288.0 / 262167.1, 524288.0 / 524288.0
 TRAFFIC = {
-    "chain_gpt_n24_k16": {"fetch_kib": 18.0, "write_kib": 0.5, "sources": "0e8d13c27d216b99"},
-    "chain_gpt_n1152_k64": {"fetch_kib": 37977.6, "write_kib": 37514.9, "sources": "80481ca70025b261"},
-    "mem_llama_n288_k32": {"fetch_kib": 59583.6, "write_kib": 236706.7, "sources": "a54c35be35daeb3e"},
-    "chain_wide_n512_k256": {"fetch_kib": 44575.4, "write_kib": 16423.8, "sources": "1a7191b805032226"},
+    "chain_gpt_n24_k16": {"fetch_kib": 18.0, "write_kib": 0.5, "sources": "4a59102f0d13e6c1"},
+    "chain_gpt_n1152_k64": {"fetch_kib": 37970.3, "write_kib": 37516.3, "sources": "b412a2fa80c1eeaf"},
+    "mem_llama_n288_k32": {"fetch_kib": 59588.7, "write_kib": 238466.1, "sources": "fe1821b27002ed6d"},
+    "chain_wide_n512_k256": {"fetch_kib": 44455.0, "write_kib": 16423.4, "sources": "b0f627d51c4baf4c"},
     # mean over the 12 matrix-product launches of one forward call
-    "scan_n4096_k512": {"fetch_kib": 3035428.6, "write_kib": 1398442.5, "sources": "baf520c71302e876"},
-    "seg_gpt_n96_k81": {"fetch_kib": 3922.7, "write_kib": 1936.0, "sources": "9f3604356fb3c132"},
+    "scan_n4096_k512": {"fetch_kib": 3035253.1, "write_kib": 1398442.5, "sources": "bba6a229e4af8d7e"},
+    "seg_gpt_n96_k81": {"fetch_kib": 3922.7, "write_kib": 1936.0, "sources": "66d4b832202782ab"},
     # the memory workload run as a budget frontier (every chunk of every search active)
-    "mem_llama_n288_k32:frontier": {"fetch_kib": 77501.4, "write_kib": 307839.8, "sources": "a54c35be35daeb3e"},
+    "mem_llama_n288_k32:frontier": {"fetch_kib": 77558.9, "write_kib": 307793.0, "sources": "fe1821b27002ed6d"},
 }
 
 

@@ -7,8 +7,8 @@
 // so it does not increase with m.
 //
 // Layout.  Each search is cut into chunks of 64 memory buckets; one workgroup
-// (4 waves) computes one chunk for all K <= 32 states, lanes running over the
-// buckets m of the chunk, wave w over a quarter of the states.  Step i of a
+// (8 waves) computes one chunk for all K <= 32 states, lanes running over the
+// buckets m of the chunk, each wave over its share of the states.  Step i of a
 // chunk only reads buckets m - mem[i][s] >= m - kMemShift of step i-1, so a
 // chunk needs the top kMemShift buckets of the chunk below it: each chunk
 // publishes them in a device ring (one slot per step) and then raises a
@@ -22,7 +22,8 @@
 // Arithmetic.  Column m carries an exact int64 offset o[m] = min_s D[s][m];
 // LDS holds Q[s][m] = min(D[s][m] - o[m], cap) << b with cap = 2^(32-b) - 1.
 // A candidate is the saturating sum Q[t][m-d] + ((R[t][s] << b) | t)
-// with the resharding column of state s taken from SGPRs; its value is
+// with the resharding column of state s read from an LDS copy of the packed
+// tables (every lane reads the same words); its value is
 // relative to o[m-d], and o[m-d] - o[m] >= 0 (fewer buckets never cost
 // less) converts it.  The best candidate of any state is at most R_max
 // (through the minimum of column m-d), so it is exact for R < cap; a state
