@@ -10,11 +10,11 @@
 // state) after a few steps, and from then on both choose the same argmins.
 //   1. speculative pass, every chunk: chunk p starts at its first row from that
 //      row's costs alone, as if the chain began there.  It writes the argmin
-//      rows of its steps and, at the end of every block of 12 rows (a
+//      rows of its steps and, at the end of every quad of 4 rows (a
 //      checkpoint), its normalised row and the running sum of its offsets.
 //   2. fix-up pass, chunks 1..P-1: chunk p starts again from the last
 //      checkpoint row of chunk p-1 and recomputes its steps until its
-//      normalised row equals the stored checkpoint row of the same block,
+//      normalised row equals the stored checkpoint row of the same quad,
 //      rewriting the argmins on the way.  Equal normalised rows mean every
 //      later step of the speculative pass is exactly the true one.
 //   3. final pass, per search: sums the offsets of the chunks; if a chunk's
@@ -44,11 +44,12 @@
 // unavailable strategy (cost CFP_COST_INF) and a padding state (s >= K) get
 // x = 2^32 - 1 and stay capped.
 //
-// Work split of a workgroup: 8 waves, each with two searches of the same
-// chunk, so every wave steps through the same rows and the same tables.  The
-// packed tables of four consecutive rows (4 x 16 KiB) sit in LDS and the next
-// four are staged while these are used (double buffer, one barrier per four
-// rows); a wave's two searches share every table read.
+// Work split of a workgroup: 16 waves, each with one search of the same chunk
+// (kWG searches per wave in general), so every wave steps through the same
+// rows and the same tables.  The packed tables of four consecutive rows
+// (4 x 16 KiB) sit in LDS and the next four are staged while these are used
+// (double buffer, one barrier per four rows); the rows are cut into blocks of
+// 12, the period of the edge map the kernels are specialised for.
 #include <algorithm>
 #include <atomic>
 
