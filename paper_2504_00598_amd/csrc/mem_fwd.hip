@@ -401,6 +401,320 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
   if (flags & MEMF_OVERFLOW) atomicOr(&w.mflags[b], MEMF_OVERFLOW);
 }
 
+// Product-then-shift form of the step (the kernel the library launches).  A
+// state s with memory shift d takes its candidates from column m - d:
+//     D[i][s][m] = c + min_t (Q[t][m-d] + R[t][s]) = c + P[s][m-d],
+//     P[s][m']  = min_t (Q[t][m'] + R[t][s]),
+// so a workgroup forms the products P at its own buckets once (each lane reads
+// the K rows of its bucket's column once) and then shifts only P: one read per
+// state and bucket instead of K per state and distinct shift.  The buckets
+// below the chunk come from the chunk below, which passes its products (not
+// its rows) for its top kMemShift buckets through the ring.
+//   Phase A (products): wave w forms P for the states of rank SW w .. SW w +
+//     SW - 1, lanes over the chunk's buckets.
+//   Phase B (shift and normalise): wave w takes BPW = C / NW buckets; lane
+//     (c = lane % BPW, g = lane / BPW) bucket BPW w + c and the SB states of
+//     rank SB g ..; the column minimum is reduced over the lanes of a bucket.
+// Step i of a chunk needs slot i of the ring below (P_i and the offsets of
+// step i-1 of the top buckets) before its phase B.  A chunk stores slot i as
+// soon as its products are in LDS (after the first barrier of step i), every
+// lane one word (no branch around the stores, so the waits for later loads
+// are exact), waits for the stores during phase B and publishes the slot
+// after the second barrier: the chunk above runs about one step behind.
+// Wave 0 reads the ring below.
+#ifndef CFP_MEM2_THREADS
+#define CFP_MEM2_THREADS 512
+#endif
+constexpr int kMem2Threads = CFP_MEM2_THREADS;
+
+template <int KP>
+__global__ __launch_bounds__(kMem2Threads) void mem_fwd2_kernel(const int32_t *__restrict__ redge,
+                                                           const int32_t *__restrict__ budget,
+                                                           const uint2 *__restrict__ srec, const uint32_t *__restrict__ rpT,
+                                                           int N, int K, int M, int B, MemWs w, uint8_t *__restrict__ table,
+                                                           SearchResult *__restrict__ res, const WsHeader *__restrict__ hdr,
+                                                           int64_t *__restrict__ opt, int32_t *__restrict__ status,
+                                                           int64_t *__restrict__ frontier) {
+  constexpr int BITS = Pow2Bits<KP>::value;
+  constexpr uint32_t CAP = (1u << (32 - BITS)) - 1u;
+  constexpr int NT = kMem2Threads;
+  constexpr int NW = NT / 64;           // waves per workgroup
+  constexpr int SW = KP / NW;           // states per wave (phase A)
+  constexpr int H = kMemShift, C = kMemChunk;
+  constexpr int COLS = H + C;
+  constexpr int BPW = C / NW;           // phase B: buckets per wave
+  constexpr int LPB = 64 / BPW;         // lanes per bucket
+  constexpr int SB = KP / LPB;          // states per lane
+  constexpr int QS = C + 1;  // padded row stride: phase B writes several states of one bucket at once
+  static_assert(SW >= 1 && SB >= 1 && BPW * NW == C && SB * LPB == KP, "work split");
+
+  __shared__ uint32_t Q[KP][QS];       // normalised rows of the chunk's buckets
+  __shared__ uint32_t P[2][KP][COLS];  // products of the step, [step parity]; columns < H: the chunk below
+  __shared__ int64_t off[2][COLS];     // offsets of the previous step, [step parity]
+  __shared__ __align__(16) uint8_t argb[KP][C];  // argmin bytes of the step, written back after it
+  __shared__ int abort_flag;
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  __shared__ __align__(16) uint32_t rT[kMemTables][KP][KP];  // packed tables, read by broadcast
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int b = blockIdx.x % B, j = blockIdx.x / B;
+  const int m0 = j * C;
+  const int Bb = budget[b];
+  const int mf = w.mflags[b];  // written by the prep kernel earlier in the stream
+  if (mf & MEMF_BAD) {
+    if (frontier && tid < C && m0 + tid < M) frontier[(size_t)b * M + m0 + tid] = INT64_MAX;
+    if (j == 0 && tid == 0) {
+      status[b] = CFP_ST_BADINPUT;
+      opt[b] = INT64_MAX;
+      res[b].final_state = -1;
+      res[b].status = CFP_ST_BADINPUT;
+      res[b].final_m = -1;
+    }
+    return;
+  }
+  if (m0 > Bb) return;  // no bucket of this chunk is within the budget
+  const size_t rowbase = (size_t)b * N;
+  int flags = 0;
+  // phase B: this lane's bucket and states
+  const int pc = lane % BPW, pg = lane / BPW;
+  const int ml = BPW * wid + pc;  // bucket within the chunk
+  const bool bact = m0 + ml <= Bb;
+
+  for (int x = tid; x < kMemTables * KP * KP / 4; x += NT)
+    ((u32x4 *)&rT[0][0][0])[x] = ((const u32x4 *)rpT)[x];
+  // Chunk 0: buckets below 0 are infeasible.
+  for (int x = tid; x < 2 * KP * H; x += NT) P[x / (KP * H)][(x / H) % KP][x % H] = kSat;
+  if (tid < H) off[0][tid] = off[1][tid] = kOffInf;
+  if (tid == 0) abort_flag = 0;
+
+  const size_t chunk_id = (size_t)b * w.nchunk + j;
+  uint32_t *my_ring = w.ring + chunk_id * N * KP * H;
+  int64_t *my_roff = w.ring_off + chunk_id * N * H;
+  const uint32_t *lo_ring = w.ring + (chunk_id - 1) * N * KP * H;
+  const int64_t *lo_roff = w.ring_off + (chunk_id - 1) * N * H;
+  const bool consumer = j > 0;
+
+  // Phase B of step i from the values y of the lane's states: column minimum,
+  // normalised rows, offsets of step i (into off[nxt]).
+  // y: values of the lane's states (kSat unreachable, a reachable state at
+  // most kSat - 1); rb: their records.
+  uint32_t y[SB];
+  uint2 rb[SB];
+  auto normalise = [&](int i, int64_t od) __attribute__((always_inline)) {
+    const int nxt = (i & 1) ^ 1;
+    uint32_t x = y[0];
+#pragma unroll
+    for (int k = 1; k < SB; ++k) x = umin(x, y[k]);
+#pragma unroll
+    for (int o = BPW; o < 64; o *= 2) x = umin(x, (uint32_t)__shfl_xor((int)x, o, 64));
+    const uint32_t cm = x;
+    const bool feas = cm != kSat;
+    if (feas && cm >= 0x80000000u) {  // rare: flagged at once, complete before the step is published
+      flags |= MEMF_OVERFLOW;
+      atomicOr(&w.mflags[b], MEMF_OVERFLOW);
+      __builtin_amdgcn_s_waitcnt(0);
+    }
+    const int64_t onew = feas ? od + (int64_t)cm : kOffInf;
+#pragma unroll
+    for (int k = 0; k < SB; ++k) {
+      const int s = rb[k].x & 0xFF;
+      Q[s][ml] = ((feas && y[k] != kSat) ? umin(y[k] - cm, CAP) : CAP) << BITS;
+    }
+    if (pg == 0) off[nxt][H + ml] = onew;
+  };
+
+  // Step 0: absolute values.
+  {
+    const uint2 *rec = srec + rowbase * KP + SB * pg;
+#pragma unroll
+    for (int k = 0; k < SB; ++k) rb[k] = rec[k];
+#pragma unroll
+    for (int k = 0; k < SB; ++k) {
+      const int d = (rb[k].x >> 8) & 0xFF;
+      const int32_t c = (int32_t)rb[k].y;
+      const bool rk = bact && m0 + ml >= d && c != CFP_COST_INF;
+      y[k] = rk ? (uint32_t)c : kSat;
+    }
+    normalise(0, 0);
+  }
+  __syncthreads();
+
+  // Slot i of this chunk's ring (P_i and the offsets of step i-1 of the top
+  // buckets), read from LDS after the first barrier of step i: KP * H words,
+  // one per thread when KP = 32, and the H offsets (each stored by several
+  // lanes).
+  constexpr int HW = KP * H / 64;
+  constexpr int RPT = (KP * H + NT - 1) / NT;  // ring words per thread (repeats when fewer than NT)
+  static_assert((KP * H) % NT == 0 || NT % (KP * H) == 0, "ring words split evenly");
+  auto ring_store = [&](int i) __attribute__((always_inline)) {
+    const int pi = i & 1;
+#pragma unroll
+    for (int k = 0; k < RPT; ++k) {
+      const int x = (tid + NT * k) % (KP * H), st = x / H, h = x % H;
+      __hip_atomic_store(&my_ring[(size_t)i * KP * H + x], P[pi][st][C + h], __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __hip_atomic_store(&my_roff[(size_t)i * H + (lane & (H - 1))], off[pi][C + (lane & (H - 1))], __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  };
+  // Argmin bytes of step i from LDS to the table, buckets m0 .. min(m0 + C,
+  // Bb + 1, M) - 1, in 16-byte pieces by the threads of waves 1 .. NW-1.
+  const bool vec16 = (M % 16) == 0;
+  auto flush = [&](int i) __attribute__((always_inline)) {
+    for (int x = tid - 64; x >= 0 && x < KP * C / 16; x += NT - 64) {
+      const int s = x / (C / 16), c0 = (x % (C / 16)) * 16;
+      if (s >= K) continue;
+      uint8_t *dst = table + ((rowbase + i) * K + s) * (size_t)M + m0 + c0;
+      const int lim = min(Bb + 1, M) - (m0 + c0);
+      if (vec16 && lim >= 16) {
+        *(u32x4 *)dst = *(const u32x4 *)&argb[s][c0];
+      } else {
+        for (int q = 0; q < 16 && q < lim; ++q) dst[q] = argb[s][c0 + q];
+      }
+    }
+  };
+
+  int pubv = -1;  // wave 0: the producer's published step, read one step ahead
+  if (consumer && wid == 0)
+    pubv = __hip_atomic_load(&w.pub[chunk_id - 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
+  for (int i = 1; i < N; ++i) {
+    const int cur = i & 1;
+    // Phase A.  Memory operations in issue order: the phase B records of the
+    // step (all waves), then the halo loads of wave 0 when slot i is already
+    // published (else it waits for it after its products), then the ring
+    // stores of the last wave; so no wait for a load covers a store.
+    {
+      const uint2 *rec = srec + (rowbase + i) * KP + SB * pg;
+#pragma unroll
+      for (int k = 0; k < SB; ++k) rb[k] = rec[k];
+    }
+    uint32_t hq[HW];
+    int64_t ho = kOffInf;
+    bool early = false;
+    if (consumer && wid == 0) {
+      early = pubv >= i;
+      if (early) {
+#pragma unroll
+        for (int k = 0; k < HW; ++k)
+          hq[k] = __hip_atomic_load(&lo_ring[(size_t)i * KP * H + lane + 64 * k], __ATOMIC_RELAXED,
+                                    __HIP_MEMORY_SCOPE_AGENT);
+        if (lane < H) ho = __hip_atomic_load(&lo_roff[(size_t)i * H + lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    const int e = redge[i];
+    {
+      uint32_t A[KP];
+#pragma unroll
+      for (int t = 0; t < KP; ++t) A[t] = Q[t][lane];
+      const uint2 *rec = srec + (rowbase + i) * KP + SW * wid;
+#pragma unroll
+      for (int k = 0; k < SW; ++k) {
+        const int s = rec[k].x & 0xFF;
+        uint32_t colc[KP];
+#pragma unroll
+        for (int q = 0; q < KP / 4; ++q) {
+          const u32x4 v = ((const u32x4 *)&rT[e][s][0])[q];
+          colc[4 * q] = v.x;
+          colc[4 * q + 1] = v.y;
+          colc[4 * q + 2] = v.z;
+          colc[4 * q + 3] = v.w;
+        }
+        uint32_t acc = sat_add(A[0], colc[0]);
+#pragma unroll
+        for (int t = 1; t < KP; ++t) acc = umin(acc, sat_add(A[t], colc[t]));
+        P[cur][s][H + lane] = acc;
+      }
+    }
+    if (consumer && wid == 0) {
+      if (!early) {
+        int spins = 0;
+        while (__hip_atomic_load(&w.pub[chunk_id - 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < i) {
+          if (++spins > kSpinLimit) {
+            if (lane == 0) abort_flag = 1;
+            flags |= MEMF_TIMEOUT;
+            atomicOr(&w.mflags[b], MEMF_TIMEOUT);
+            break;
+          }
+          __builtin_amdgcn_s_sleep(1);
+        }
+#pragma unroll
+        for (int k = 0; k < HW; ++k)
+          hq[k] = __hip_atomic_load(&lo_ring[(size_t)i * KP * H + lane + 64 * k], __ATOMIC_RELAXED,
+                                    __HIP_MEMORY_SCOPE_AGENT);
+        if (lane < H) ho = __hip_atomic_load(&lo_roff[(size_t)i * H + lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+#pragma unroll
+      for (int k = 0; k < HW; ++k) {
+        const int x = lane + 64 * k;
+        P[cur][x / H][x % H] = hq[k];
+      }
+      if (lane < H) off[cur][lane] = ho;
+    }
+    __syncthreads();
+    ring_store(i);
+
+    // Phase B.
+    {
+      const int64_t od = off[cur][H + ml];
+#pragma unroll
+      for (int k = 0; k < SB; ++k) {
+        const int s = rb[k].x & 0xFF;
+        const int d = (rb[k].x >> 8) & 0xFF;
+        const int32_t c = (int32_t)rb[k].y;
+        const uint32_t pv = P[cur][s][H + ml - d];
+        const int64_t os = off[cur][H + ml - d];
+        const bool srcok = os < kOffInf;
+        const int64_t g = srcok ? os - od : 0;
+        const uint32_t goff = g > 0x7FFFFFFF ? 0x80000000u : (uint32_t)g;
+        argb[s][ml] = (uint8_t)pv;
+        const uint32_t v = pv >> BITS;
+        const bool rk = bact && srcok && v < CAP && c != CFP_COST_INF;
+        y[k] = rk ? umin(sat_add(sat_add(v, (uint32_t)c), goff), kSat - 1) : kSat;
+      }
+      normalise(i, od);
+    }
+    if (consumer && wid == 0 && i + 1 < N)
+      pubv = __hip_atomic_load(&w.pub[chunk_id - 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __builtin_amdgcn_s_waitcnt(0);  // the ring stores of slot i are complete
+    __syncthreads();
+    if (tid == 64 * (NW - 1)) __hip_atomic_store(&w.pub[chunk_id], i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    flush(i);
+  }
+  const int fin = N & 1;  // off buffer holding the last step's offsets
+  const int m = m0 + lane;
+  const bool active = m <= Bb;
+
+  // Budget frontier: the exact offset of column m is min_s D[N-1][s][m], the
+  // least cost with memory total at most m.
+  if (frontier && wid == 0 && m < M)
+    frontier[(size_t)b * M + m] = (active && off[fin][H + lane] < kOffInf) ? off[fin][H + lane] : INT64_MAX;
+
+  // The chunk holding the budget bucket reports the search.
+  if (abort_flag) flags |= MEMF_TIMEOUT;
+  if (Bb >= m0 && Bb < m0 + C) {
+    const int col = Bb - m0;
+    if (tid == 0) {
+      uint32_t f = kSat;
+      for (int s = 0; s < K; ++s) f = umin(f, Q[s][col] | (uint32_t)s);
+      const int64_t o = off[fin][H + col];
+      const int sf = __hip_atomic_load(&w.mflags[b], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) | flags;
+      int st = CFP_ST_OK;
+      if (abort_flag || (sf & MEMF_TIMEOUT)) st = CFP_ST_TIMEOUT;
+      else if (sf & MEMF_OVERFLOW) st = CFP_ST_OVERFLOW;
+      else if (hdr->rflag) st = CFP_ST_BADINPUT;
+      else if (o >= kOffInf) st = CFP_ST_INFEASIBLE;
+      else if ((f >> BITS) != 0) st = CFP_ST_OVERFLOW;
+      status[b] = st;
+      opt[b] = st == CFP_ST_OK ? o : INT64_MAX;
+      res[b].final_state = st == CFP_ST_OK ? (int32_t)(f & ((1u << BITS) - 1u)) : -1;
+      res[b].status = st;
+      res[b].final_m = Bb;
+    }
+  }
+}
+
 // Plan recovery for the memory variant.  The state is (s, m): the table gives
 // the predecessor strategy t = arg[i][s][m] and the budget shrinks by
 // mem[i][s].  The chase runs in windows of kMemWin steps: the argmin rows of
@@ -562,7 +876,7 @@ static void launch_mem(const cfp_chain_desc &d, const uint8_t *mem, int n_mem, c
   hipLaunchKernelGGL(mem_prep_kernel<KP>, dim3((B * N + 3) / 4), dim3(256), 0, st, d.cost, mem, budget, N, K, n_mem, B,
                      w.srec, mem_copy, w.mflags);
   timer_begin(st);
-  timed_launch(mem_fwd_kernel<KP>, dim3(B * w.nchunk), dim3(kMemThreads), 0, st, redge_dev, budget,
+  timed_launch(mem_fwd2_kernel<KP>, dim3(B * w.nchunk), dim3(kMem2Threads), 0, st, redge_dev, budget,
                (const uint2 *)w.srec, (const uint32_t *)w.rpT, N, K, n_mem, B, w, table, res, hdr, opt, status, frontier);
   timer_end(st);
 }
