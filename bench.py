@@ -60,13 +60,13 @@ FETCH_SCALE, WRITE_SCALE = 524288.0 / 262167.1, 524288.0 / 524288.0
 TRAFFIC = {
     "chain_gpt_n24_k16": {"fetch_kib": 18.0, "write_kib": 0.5, "sources": "4a59102f0d13e6c1"},
     "chain_gpt_n1152_k64": {"fetch_kib": 37970.3, "write_kib": 37516.3, "sources": "b412a2fa80c1eeaf"},
-    "mem_llama_n288_k32": {"fetch_kib": 59588.7, "write_kib": 238466.1, "sources": "fe1821b27002ed6d"},
+    "mem_llama_n288_k32": {"fetch_kib": 58884.1, "write_kib": 288456.7, "sources": "aa519dbe5968c06a"},
     "chain_wide_n512_k256": {"fetch_kib": 44455.0, "write_kib": 16423.4, "sources": "b0f627d51c4baf4c"},
     # mean over the 12 matrix-product launches of one forward call
     "scan_n4096_k512": {"fetch_kib": 3035253.1, "write_kib": 1398442.5, "sources": "bba6a229e4af8d7e"},
     "seg_gpt_n96_k81": {"fetch_kib": 3922.7, "write_kib": 1936.0, "sources": "66d4b832202782ab"},
     # the memory workload run as a budget frontier (every chunk of every search active)
-    "mem_llama_n288_k32:frontier": {"fetch_kib": 77558.9, "write_kib": 307793.0, "sources": "fe1821b27002ed6d"},
+    "mem_llama_n288_k32:frontier": {"fetch_kib": 76704.2, "write_kib": 372085.2, "sources": "aa519dbe5968c06a"},
 }
 
 

@@ -7,12 +7,12 @@
 // so it does not increase with m.
 //
 // Layout.  Each search is cut into chunks of 64 memory buckets; one workgroup
-// (8 waves) computes one chunk for all K <= 32 states, lanes running over the
-// buckets m of the chunk, each wave over its share of the states.  Step i of a
-// chunk only reads buckets m - mem[i][s] >= m - kMemShift of step i-1, so a
-// chunk needs the top kMemShift buckets of the chunk below it: each chunk
-// publishes them in a device ring (one slot per step) and then raises a
-// counter; the chunk above waits for the counter (bounded spin).  The ring
+// (8 waves) computes one chunk for all K <= 32 states.  Step i of a chunk
+// only reads buckets m - mem[i][s] >= m - kMemShift of step i-1, so a chunk
+// needs the top kMemShift buckets of the chunk below it: each chunk
+// publishes what the chunk above needs of them in a device ring (one slot per
+// step) and then raises a counter; the chunk above waits for the counter
+// (bounded spin).  The ring
 // and the counters are only touched by device-scope atomic stores and loads,
 // and the counter is raised after every ring store has completed, so no cache
 // write-back or invalidation is needed.  Chunks of one search have workgroup ids j*B + b, so a producer
@@ -28,9 +28,9 @@
 // less) converts it.  The best candidate of any state is at most R_max
 // (through the minimum of column m-d), so it is exact for R < cap; a state
 // whose relative value reaches the cap is beaten, at the same memory, by the
-// minimum state of its column and can never lie on an optimal plan.  States
-// are visited in order of their memory shift so each wave loads every
-// shifted row once.
+// minimum state of its column and can never lie on an optimal plan.  The
+// kernel forms the products min_t Q[t][m'] + R[t][s] at unshifted buckets m'
+// and applies each state's shift to them (see mem_fwd_kernel).
 #include "cfp_internal.h"
 #include "common.h"
 
@@ -113,296 +113,8 @@ struct MemWs {
   int nchunk;
 };
 
-template <int KP>
-__global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__restrict__ redge, const int32_t *__restrict__ budget,
-                                                           const uint2 *__restrict__ srec, const uint32_t *__restrict__ rpT,
-                                                           int N, int K, int M, int B, MemWs w, uint8_t *__restrict__ table,
-                                                           SearchResult *__restrict__ res, const WsHeader *__restrict__ hdr,
-                                                           int64_t *__restrict__ opt, int32_t *__restrict__ status,
-                                                           int64_t *__restrict__ frontier) {
-  constexpr int BITS = Pow2Bits<KP>::value;
-  constexpr uint32_t CAP = (1u << (32 - BITS)) - 1u;
-  constexpr int NW = kMemThreads / 64;       // waves per workgroup
-  constexpr int SW = KP / NW;                // states per wave
-  constexpr int H = kMemShift, C = kMemChunk;
-  constexpr int COLS = H + C;
-
-  __shared__ uint32_t Q[KP][COLS];
-  __shared__ int64_t off[2][COLS];   // column offsets, [step parity]
-  __shared__ uint32_t part[NW][C];
-  __shared__ uint32_t reach[NW][C];
-  __shared__ uint8_t argb[KP][C];    // argmin bytes of the step, written back after it
-  __shared__ int abort_flag;
-  __shared__ int halo_ready;         // wave 0 has the next halo in registers
-  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-  __shared__ __align__(16) uint32_t rT[kMemTables][KP][KP];  // packed tables, read by broadcast
-
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave: per-state data comes by scalar loads
-  const int b = blockIdx.x % B, j = blockIdx.x / B;
-  const int m0 = j * C;
-  const int Bb = budget[b];
-  const int mf = w.mflags[b];  // written by the prep kernel earlier in the stream
-  if (mf & MEMF_BAD) {
-    if (frontier && tid < C && m0 + tid < M) frontier[(size_t)b * M + m0 + tid] = INT64_MAX;
-    if (j == 0 && tid == 0) {
-      status[b] = CFP_ST_BADINPUT;
-      opt[b] = INT64_MAX;
-      res[b].final_state = -1;
-      res[b].status = CFP_ST_BADINPUT;
-      res[b].final_m = -1;
-    }
-    return;
-  }
-  if (m0 > Bb) return;  // no bucket of this chunk is within the budget
-  const int m = m0 + lane;
-  const bool active = m <= Bb;
-  const size_t rowbase = (size_t)b * N;
-  int flags = 0;
-
-  // The packed tables (all slots; only those below E are ever read).
-  for (int x = tid; x < kMemTables * KP * KP / 4; x += kMemThreads)
-    ((u32x4 *)&rT[0][0][0])[x] = ((const u32x4 *)rpT)[x];
-  // Halo of chunk 0: buckets below 0 are infeasible.
-  for (int x = tid; x < KP * H; x += kMemThreads) Q[x / H][x % H] = CAP << BITS;
-  if (tid < H) off[0][tid] = off[1][tid] = kOffInf;
-  if (tid == 0) abort_flag = 0;
-  __syncthreads();
-
-  const size_t chunk_id = (size_t)b * w.nchunk + j;
-  uint32_t *my_ring = w.ring + chunk_id * N * KP * H;
-  int64_t *my_roff = w.ring_off + chunk_id * N * H;
-  const uint32_t *lo_ring = w.ring + (chunk_id - 1) * N * KP * H;
-  const int64_t *lo_roff = w.ring_off + (chunk_id - 1) * N * H;
-  const bool consumer = j > 0;
-
-  // y[k]: value of the wave's k-th state at bucket m relative to the previous
-  // offset of column m; rk: the state is reachable.
-  uint32_t y[SW];
-  bool rk[SW];
-
-  // Halo prefetch of wave 0: the producer's published step, read at the start
-  // of a step, and its halo, read after the wave's part of the step once the
-  // producer has published it.
-  constexpr int HW = KP * H / 64;
-  uint32_t hq[HW];
-  int64_t ho = kOffInf;
-  int pubv = -1;
-  auto pub_prefetch = [&](int i) __attribute__((always_inline)) {
-    if (consumer && wid == 0 && i + 1 < N)
-      pubv = __hip_atomic_load(&w.pub[chunk_id - 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  };
-  auto halo_prefetch = [&](int i) __attribute__((always_inline)) {
-    if (wid != 0) return;
-    const bool ok = consumer && i + 1 < N && pubv >= i;
-    if (ok) {
-#pragma unroll
-      for (int k = 0; k < HW; ++k)
-        hq[k] = __hip_atomic_load(&lo_ring[(size_t)i * KP * H + lane + 64 * k], __ATOMIC_RELAXED,
-                                  __HIP_MEMORY_SCOPE_AGENT);
-      if (lane < H) ho = __hip_atomic_load(&lo_roff[(size_t)i * H + lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    if (lane == 0) halo_ready = ok;
-  };
-
-  // Argmin bytes of step i from LDS to the table, buckets m0 .. min(m0 + C, Bb + 1, M) - 1.
-  constexpr int BPT = KP * C / kMemThreads;  // bytes per thread
-  auto flush = [&](int i) __attribute__((always_inline)) {
-    const int s = tid / (C / BPT), c0 = (tid % (C / BPT)) * BPT;
-    if (s >= K) return;
-    uint8_t *dst = table + ((rowbase + i) * K + s) * (size_t)M + m0 + c0;
-    const int lim = min(Bb + 1, M) - (m0 + c0);  // bytes of this thread's piece within the budget
-#pragma unroll
-    for (int q = 0; q < BPT; ++q)
-      if (q < lim) dst[q] = argb[s][c0 + q];
-  };
-
-  // Ring stores of step i (the top kMemShift buckets of every state and their
-  // offsets, read back from LDS), by the last wave at the start of step i+1;
-  // that wave waits for them at the end of step i+1, before the barrier after
-  // which step i is published.
-  auto ring_store = [&](int i) __attribute__((always_inline)) {
-    if (wid != NW - 1 || i + 1 >= N) return;
-    const int cur = (i + 1) & 1;  // offsets of step i
-#pragma unroll
-    for (int k = 0; k < HW; ++k) {
-      const int x = lane + 64 * k, st = x / H, h = x % H;
-      __hip_atomic_store(&my_ring[(size_t)i * KP * H + x], Q[st][C + h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    if (lane < H)
-      __hip_atomic_store(&my_roff[(size_t)i * H + lane], off[cur][C + lane], __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
-  };
-
-  // End of step i: offsets, the own rows, the producer's halo for step i+1.
-  // The publication of step i-1 happens here, one step late, when its ring
-  // stores have long completed.
-  auto finish_step = [&](int i) __attribute__((always_inline)) {
-    const int cur = i & 1, nxt = cur ^ 1;
-    uint32_t pm = kSat, pr = 0;
-#pragma unroll
-    for (int k = 0; k < SW; ++k) {
-      pm = umin(pm, y[k]);
-      pr |= rk[k] ? 1u : 0u;
-    }
-    part[wid][lane] = pm;
-    reach[wid][lane] = pr;
-    if (wid == NW - 1) __builtin_amdgcn_s_waitcnt(0);  // the ring stores of step i-1 are complete
-    __syncthreads();
-    if (tid == 0 && i > 0) __hip_atomic_store(&w.pub[chunk_id], i - 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    uint32_t cm = part[0][lane], rr = reach[0][lane];
-#pragma unroll
-    for (int x = 1; x < NW; ++x) {
-      cm = umin(cm, part[x][lane]);
-      rr |= reach[x][lane];
-    }
-    const bool feas = rr != 0;
-    if (feas && cm >= 0x80000000u) flags |= MEMF_OVERFLOW;
-    const int64_t onew = (feas && cm < kSat) ? off[cur][H + lane] + (int64_t)cm : kOffInf;
-    const uint2 *rec = srec + (rowbase + i) * KP + wid * SW;
-#pragma unroll
-    for (int k = 0; k < SW; ++k) {
-      const int s = rec[k].x & 0xFF;
-      const uint32_t q = ((onew < kOffInf && y[k] < kSat) ? umin(y[k] - cm, CAP) : CAP) << BITS;
-      Q[s][H + lane] = q;
-    }
-    if (wid == 0) off[nxt][H + lane] = onew;
-    if (i > 0) flush(i);
-    // Halo for step i+1: the top buckets of the chunk below, at step i.
-    if (consumer && i + 1 < N) {
-      if (halo_ready) {
-        if (wid == 0) {
-#pragma unroll
-          for (int k = 0; k < HW; ++k) {
-            const int x = lane + 64 * k;
-            Q[x / H][x % H] = hq[k];
-          }
-          if (lane < H) off[nxt][lane] = ho;
-        }
-      } else {
-        if (tid == 0) {
-          int spins = 0;
-          while (__hip_atomic_load(&w.pub[chunk_id - 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < i) {
-            if (++spins > kSpinLimit) {
-              abort_flag = 1;
-              atomicOr(&w.mflags[b], MEMF_TIMEOUT);
-              break;
-            }
-            __builtin_amdgcn_s_sleep(1);
-          }
-        }
-        __syncthreads();
-        for (int x = tid; x < KP * H; x += kMemThreads)
-          Q[x / H][x % H] =
-              __hip_atomic_load(&lo_ring[(size_t)i * KP * H + x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (tid < H)
-          off[nxt][tid] = __hip_atomic_load(&lo_roff[(size_t)i * H + tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
-    }
-    __syncthreads();
-  };
-
-  // Block 0.
-  {
-    pub_prefetch(0);
-    const uint2 *rec = srec + rowbase * KP + wid * SW;
-#pragma unroll
-    for (int k = 0; k < SW; ++k) {
-      const int d = (rec[k].x >> 8) & 0xFF;
-      const int32_t c = (int32_t)rec[k].y;
-      rk[k] = active && m >= d && c != CFP_COST_INF;
-      y[k] = rk[k] ? (uint32_t)c : kSat;
-    }
-    if (wid == 0) off[0][H + lane] = 0;  // block 0 values are absolute
-    halo_prefetch(0);
-    __syncthreads();
-    finish_step(0);
-  }
-
-  for (int i = 1; i < N; ++i) {
-    const int cur = i & 1;
-    ring_store(i - 1);
-    pub_prefetch(i);
-    const int e = redge[i];
-    const uint2 *rec = srec + (rowbase + i) * KP + wid * SW;
-    uint32_t A[KP];
-    int dprev = -1;
-    uint32_t goff = 0;
-    bool srcok = false;
-#pragma unroll
-    for (int k = 0; k < SW; ++k) {
-      const int s = rec[k].x & 0xFF;
-      const int d = (rec[k].x >> 8) & 0xFF;
-      const int32_t c = (int32_t)rec[k].y;
-      // resharding column of state s (every lane reads the same words)
-      uint32_t colc[KP];
-#pragma unroll
-      for (int q = 0; q < KP / 4; ++q) {
-        const u32x4 v = ((const u32x4 *)&rT[e][s][0])[q];
-        colc[4 * q] = v.x;
-        colc[4 * q + 1] = v.y;
-        colc[4 * q + 2] = v.z;
-        colc[4 * q + 3] = v.w;
-      }
-      if (d != dprev) {
-        dprev = d;
-#pragma unroll
-        for (int t = 0; t < KP; ++t) A[t] = Q[t][H + lane - d];
-        const int64_t os = off[cur][H + lane - d], od = off[cur][H + lane];
-        srcok = os < kOffInf;
-        const int64_t g = srcok ? os - od : 0;
-        goff = g > 0x7FFFFFFF ? 0x80000000u : (uint32_t)g;
-      }
-      uint32_t acc = sat_add(A[0], colc[0]);
-#pragma unroll
-      for (int t = 1; t < KP; ++t) acc = umin(acc, sat_add(A[t], colc[t]));
-      argb[s][lane] = (uint8_t)acc;
-      const uint32_t v = acc >> BITS;
-      rk[k] = active && srcok && v < CAP && c != CFP_COST_INF;
-      y[k] = rk[k] ? sat_add(sat_add(v, (uint32_t)c), goff) : kSat;
-    }
-    halo_prefetch(i);
-    finish_step(i);
-  }
-  // Publication of the last step (a consumer needs at most step N-2), then
-  // the state of the final offsets.
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (tid == 0) __hip_atomic_store(&w.pub[chunk_id], N - 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  const int fin = N & 1;  // off buffer holding the last step's offsets
-
-  // Budget frontier: the exact offset of column m is min_s D[N-1][s][m], the
-  // least cost with memory total at most m.
-  if (frontier && wid == 0 && m < M)
-    frontier[(size_t)b * M + m] = (active && off[fin][H + lane] < kOffInf) ? off[fin][H + lane] : INT64_MAX;
-
-  // The chunk holding the budget bucket reports the search.
-  if (abort_flag) flags |= MEMF_TIMEOUT;
-  if (Bb >= m0 && Bb < m0 + C) {
-    const int col = H + (Bb - m0);
-    if (tid == 0) {
-      uint32_t f = kSat;
-      for (int s = 0; s < K; ++s) f = umin(f, Q[s][col] | (uint32_t)s);
-      const int64_t o = off[fin][col];
-      const int sf = __hip_atomic_load(&w.mflags[b], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) | flags;
-      int st = CFP_ST_OK;
-      if (abort_flag || (sf & MEMF_TIMEOUT)) st = CFP_ST_TIMEOUT;
-      else if (sf & MEMF_OVERFLOW) st = CFP_ST_OVERFLOW;
-      else if (hdr->rflag) st = CFP_ST_BADINPUT;
-      else if (o >= kOffInf) st = CFP_ST_INFEASIBLE;
-      else if ((f >> BITS) != 0) st = CFP_ST_OVERFLOW;
-      status[b] = st;
-      opt[b] = st == CFP_ST_OK ? o : INT64_MAX;
-      res[b].final_state = st == CFP_ST_OK ? (int32_t)(f & ((1u << BITS) - 1u)) : -1;
-      res[b].status = st;
-      res[b].final_m = Bb;
-    }
-  }
-  if (flags & MEMF_OVERFLOW) atomicOr(&w.mflags[b], MEMF_OVERFLOW);
-}
-
-// Product-then-shift form of the step (the kernel the library launches).  A
-// state s with memory shift d takes its candidates from column m - d:
+// One step in product-then-shift form.  A state s with memory shift d takes
+// its candidates from column m - d:
 //     D[i][s][m] = c + min_t (Q[t][m-d] + R[t][s]) = c + P[s][m-d],
 //     P[s][m']  = min_t (Q[t][m'] + R[t][s]),
 // so a workgroup forms the products P at its own buckets once (each lane reads
@@ -422,13 +134,8 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__r
 // are exact), waits for the stores during phase B and publishes the slot
 // after the second barrier: the chunk above runs about one step behind.
 // Wave 0 reads the ring below.
-#ifndef CFP_MEM2_THREADS
-#define CFP_MEM2_THREADS 512
-#endif
-constexpr int kMem2Threads = CFP_MEM2_THREADS;
-
 template <int KP>
-__global__ __launch_bounds__(kMem2Threads) void mem_fwd2_kernel(const int32_t *__restrict__ redge,
+__global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(const int32_t *__restrict__ redge,
                                                            const int32_t *__restrict__ budget,
                                                            const uint2 *__restrict__ srec, const uint32_t *__restrict__ rpT,
                                                            int N, int K, int M, int B, MemWs w, uint8_t *__restrict__ table,
@@ -437,7 +144,7 @@ __global__ __launch_bounds__(kMem2Threads) void mem_fwd2_kernel(const int32_t *_
                                                            int64_t *__restrict__ frontier) {
   constexpr int BITS = Pow2Bits<KP>::value;
   constexpr uint32_t CAP = (1u << (32 - BITS)) - 1u;
-  constexpr int NT = kMem2Threads;
+  constexpr int NT = kMemThreads;
   constexpr int NW = NT / 64;           // waves per workgroup
   constexpr int SW = KP / NW;           // states per wave (phase A)
   constexpr int H = kMemShift, C = kMemChunk;
@@ -876,7 +583,7 @@ static void launch_mem(const cfp_chain_desc &d, const uint8_t *mem, int n_mem, c
   hipLaunchKernelGGL(mem_prep_kernel<KP>, dim3((B * N + 3) / 4), dim3(256), 0, st, d.cost, mem, budget, N, K, n_mem, B,
                      w.srec, mem_copy, w.mflags);
   timer_begin(st);
-  timed_launch(mem_fwd2_kernel<KP>, dim3(B * w.nchunk), dim3(kMem2Threads), 0, st, redge_dev, budget,
+  timed_launch(mem_fwd_kernel<KP>, dim3(B * w.nchunk), dim3(kMemThreads), 0, st, redge_dev, budget,
                (const uint2 *)w.srec, (const uint32_t *)w.rpT, N, K, n_mem, B, w, table, res, hdr, opt, status, frontier);
   timer_end(st);
 }
