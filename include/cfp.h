@@ -26,8 +26,12 @@
  * Conventions for every call:
  *  - Arrays are C-contiguous, row-major.  "device" pointers are HIP device
  *    memory of the current device; "host" pointers are ordinary host memory.
- *  - The caller owns all memory.  The library allocates nothing, frees
- *    nothing and keeps no pointer after a call returns.
+ *  - The caller owns all memory.  The library allocates no device memory,
+ *    frees nothing of the caller's and keeps no pointer after a call
+ *    returns.  Its only allocations are host-side: per device, on the first
+ *    call that uploads a workspace header, a ring of 32 pinned host slots of
+ *    64 KiB and one event per slot (held until the process ends), so that
+ *    the header copy is asynchronous; and the benchmarking timer's events.
  *  - Work is enqueued on `stream` (a hipStream_t passed as void*; NULL is
  *    the default stream) and ordered like any other stream work; inputs must
  *    stay valid until that work has run.
@@ -218,13 +222,14 @@ int cfp_traceback_segments(const cfp_segment_desc *d, void *ws, size_t ws_bytes,
  * max_launches pairs of HIP events (1 <= max_launches <= 2^20) and arms
  * recording: from then on every launch of a forward call's main kernel (the
  * chain step kernel of cfp_dp_chain, the step kernel of cfp_dp_chain_mem,
- * each min-plus matrix-product launch of cfp_minplus_scan) is bracketed by
- * one pair recorded on the call's stream, until the pairs run out.
+ * each min-plus matrix-product launch of cfp_minplus_scan) carries one pair
+ * as the start and stop events of its dispatch (on the call's stream), until
+ * the pairs run out.
  * cfp_timer_stop waits for the recorded events, writes the summed device
  * time in milliseconds and the number of bracketed launches, disarms
  * recording and destroys the events.  The timer is process-wide state behind
- * a lock, meant for one benchmarking thread; it is the only global state of
- * the library.  Returns CFP_OK, CFP_ERR_ARG (bad count, start while armed,
+ * a lock, meant for one benchmarking thread; besides the header-upload ring
+ * it is the only global state of the library.  Returns CFP_OK, CFP_ERR_ARG (bad count, start while armed,
  * stop while not armed) or CFP_ERR_HIP. */
 int cfp_timer_start(int32_t max_launches);
 int cfp_timer_stop(double *total_ms, int32_t *launches);
