@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 from oracle import oracle as O
-from tests.gpu_util import assert_chain_parity, dev, need_gpu, run_chain, say
+from tests.gpu_util import assert_chain_parity, dev, need_gpu, oracle_threads, run_chain, say
 from workloads import configs, gen
 
 pytestmark = pytest.mark.gpu
@@ -333,3 +333,64 @@ def test_chunked_wide_ties_and_statuses():
     opt, st, plan = run_chain(cost, rtab, redge)
     assert st[7] == CFP_ST_BADINPUT and opt[7] == np.iinfo(np.int64).max and (plan[7] == -1).all()
     assert st[4] != 0 and st[6] == 0 and st[8] == 0 and (st[np.r_[0:4, 5:7]] == 0).all()
+
+
+def test_header_uploads_back_to_back():
+    """Forty calls enqueued without a synchronisation, each with its own edge
+    map and workspace: more calls than the library's ring of pinned upload
+    slots, so slots are reused while earlier copies may still be queued."""
+    need_gpu()
+    import torch
+    from paper_2504_00598_amd import search
+    say("header uploads back to back")
+    rs = np.random.default_rng(61)
+    B, N, K, E = 2, 40, 16, 4
+    rtab = rs.integers(0, 50, size=(E, K, K)).astype(np.int32)
+    cases, results = [], []
+    for c in range(40):
+        cost = rs.integers(0, 50, size=(B, N, K)).astype(np.int32)
+        redge = rs.integers(0, E, size=N).astype(np.int32)
+        cases.append((cost, redge))
+        results.append(search.dp_chain(dev(cost), dev(rtab), redge))
+    torch.cuda.synchronize()
+    for c, ((cost, redge), r) in enumerate(zip(cases, results)):
+        o_opt, o_plan, o_st = O.chain(cost, rtab, redge)
+        np.testing.assert_array_equal(r.opt.cpu().numpy(), o_opt, err_msg=f"opt call {c}")
+        np.testing.assert_array_equal(r.plan.cpu().numpy(), o_plan, err_msg=f"plan call {c}")
+
+
+def test_range_flag_does_not_leak_between_calls():
+    """The chunk-parallel K=64 path with a periodic edge map does not upload the
+    workspace header and flags an out-of-range R by call number: a workspace
+    reused after a call with bad R, or after a call on another path, gives
+    clean statuses."""
+    need_gpu()
+    import torch
+    from paper_2504_00598_amd import CFP_ST_BADINPUT, cfp_r_limit, search
+    say("range flag across calls")
+    rs = np.random.default_rng(62)
+    B, N, K = 70, 400, 64
+    cost = rs.integers(0, 1000, size=(B, N, K)).astype(np.int32)
+    rtab = rs.integers(0, 1000, size=(12, K, K)).astype(np.int32)
+    periodic = (np.arange(N) % 12).astype(np.int32)
+    bad = rtab.copy()
+    bad[3, 5, 7] = cfp_r_limit(0, K)
+    r = search.dp_chain(dev(cost), dev(bad), periodic)
+    torch.cuda.synchronize()
+    assert (r.status.cpu().numpy() == CFP_ST_BADINPUT).all()
+    ws = r.ws
+    o_opt, o_plan, o_st = O.chain(cost, rtab, periodic, nthreads=oracle_threads())
+    r2 = search.dp_chain(dev(cost), dev(rtab), periodic, ws=ws)  # same workspace, good R
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(r2.status.cpu().numpy(), o_st)
+    np.testing.assert_array_equal(r2.opt.cpu().numpy(), o_opt)
+    np.testing.assert_array_equal(r2.plan.cpu().numpy(), o_plan)
+    # a non-periodic edge map (another path, header uploaded) with bad R, then periodic again
+    other = rs.integers(0, 12, size=N).astype(np.int32)
+    r3 = search.dp_chain(dev(cost), dev(bad), other, ws=ws)
+    torch.cuda.synchronize()
+    assert (r3.status.cpu().numpy() == CFP_ST_BADINPUT).all()
+    r4 = search.dp_chain(dev(cost), dev(rtab), periodic, ws=ws)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(r4.opt.cpu().numpy(), o_opt)
+    np.testing.assert_array_equal(r4.plan.cpu().numpy(), o_plan)
