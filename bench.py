@@ -2,15 +2,19 @@
 
 A step is one whole search of a batch of synthetic chains: the forward pass
 plus the traceback of every plan, with every input already resident in
-device memory.  The default workload is the batched chain of 1152 blocks
-(96 GPT-like layers of 12 ParallelBlocks), 64 strategies per block, 256
-independent searches sharing 12 resharding tables.  Prints one JSON line.
+device memory.  Prints one JSON line.
 
     python bench.py [--steps K] [--warmup W] [--config NAME] [--no-cpu]
 
-Other workloads (--config): chain_gpt_n24_k16, mem_llama_n288_k32 (with
---frontier: every budget in one pass), chain_wide_n512_k256, scan_n4096_k512,
-seg_gpt_n96_k81 (segment-level search with boundary resharding).
+By default every workload is timed in turn and the line carries one record
+per workload under "configs"; the headline figures are those of the largest,
+scan_n4096_k512 (4096 blocks, 512 strategies, 4 searches, the min-plus
+parallel-scan form).  The records also hold the budget frontier of the memory
+workload and the scan workload run through the sequential chain search.
+With --config only that workload is timed: chain_gpt_n24_k16,
+chain_gpt_n1152_k64, mem_llama_n288_k32 (with --frontier: every budget in one
+pass), chain_wide_n512_k256, scan_n4096_k512 (with --sequential: the chain
+search), seg_gpt_n96_k81 (segment-level search with boundary resharding).
 """
 from __future__ import annotations
 
@@ -32,7 +36,7 @@ METRIC = "min-plus cell updates/sec (K² per block per search) + search latency"
 VALU_LANE_OPS = 256 * 64 * 2.4e9
 INSTR_PER_CELL = 1.5
 PEAK_CELLS = VALU_LANE_OPS / INSTR_PER_CELL
-DEFAULT_CONFIG = "chain_gpt_n1152_k64"
+SEQUENTIAL_KERNEL = "chain_fwd_split_kernel<512>"
 
 
 # The kernel that dominates the forward pass of each workload, and the source
@@ -276,15 +280,169 @@ def calibrate_copy() -> int:
     return 0
 
 
+def host_info() -> dict:
+    """CPU model and core counts of the host the baseline runs on."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:
+        avail = os.cpu_count() or 1
+    return {"cpu_model": model, "logical_cpus": os.cpu_count() or 1, "cpus_available": avail}
+
+
+def measure(name: str, steps: int, warmup: int, cpu_s: float, frontier: bool = False,
+            sequential: bool = False) -> dict:
+    """Time `steps` whole passes (forward + traceback) of one workload and
+    return its record: step time, cells/s in the metric's unit, the dominant
+    kernel's and the forward call's roofline fractions, parity against the
+    oracle on the full workload, and (cpu_s > 0) the oracle's rate on the
+    host cores."""
+    import dataclasses
+
+    import torch
+
+    from workloads import configs
+
+    cfg = configs.BY_NAME[name]
+    data = configs.make(cfg)
+    if sequential:
+        if cfg.form != "scan":
+            raise SystemExit("--sequential applies to the scan workload")
+        cfg = dataclasses.replace(cfg, form="chain")
+    if frontier:
+        if cfg.form != "mem":
+            raise SystemExit("--frontier applies to the memory workload")
+        data = dict(data, budget=np.full(cfg.B, cfg.M - 1, np.int32))  # the pass covers every budget
+    r = Runner(cfg, data, frontier=frontier)
+    for _ in range(warmup):
+        r.forward()
+        r.traceback()
+    torch.cuda.synchronize()
+
+    # Timed region: K whole steps (forward + traceback) with nothing else on the
+    # stream; an event record costs several microseconds of GPU time, so the
+    # per-phase split and the kernel timer come from a second, instrumented pass.
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        r.forward()
+        r.traceback()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    # the library brackets each launch of the dominant kernel with HIP events
+    # on the stream it is launched on
+    L = r.L
+    L.cfp_timer_start(steps * 64)
+    torch.cuda.synchronize()
+    for a, m, b in ev:
+        a.record(r.stream)
+        r.forward()
+        m.record(r.stream)
+        r.traceback()
+        b.record(r.stream)
+    torch.cuda.synchronize()
+    kern_ms, kern_launches = L.cfp_timer_stop()
+    fwd_ms = float(np.mean([a.elapsed_time(m) for a, m, _ in ev]))
+    tb_ms = float(np.mean([m.elapsed_time(b) for _, m, b in ev]))
+    ms_per_step = wall * 1e3 / steps
+
+    cells = cells_of(cfg, data)
+    value = cells / (ms_per_step * 1e-3)
+    work = scan_gemm_cells(cfg) if cfg.form == "scan" else cells
+    # per launch: the algorithmic cells of one launch over its average duration
+    # (the scan's products differ in size per level: total cells over total time)
+    kern_avg_ms = kern_ms / max(kern_launches, 1)
+    kern_cells_s = work * steps / (kern_ms * 1e-3) if kern_launches else 0.0
+    fwd_cells_s = work / (fwd_ms * 1e-3)
+
+    o_opt, o_plan, o_st = run_oracle(cfg, data)
+    g_opt = r.frontier[:, -1].cpu().numpy() if frontier else r.opt.cpu().numpy()
+    parity = bool(np.array_equal(g_opt, o_opt) and np.array_equal(r.plan.cpu().numpy(), o_plan)
+                  and np.array_equal(r.status.cpu().numpy(), o_st))
+    if frontier:
+        from oracle import oracle as O
+
+        parity = parity and bool(np.array_equal(
+            r.frontier.cpu().numpy(),
+            O.mem_frontier(data["cost"], data["rtab"], data["redge"], data["mem"], cfg.M, nthreads=oracle_threads())))
+
+    wl = {"workload": cfg.name, "blocks": cfg.N, "strategies": cfg.K, "searches": cfg.B, "resharding_tables": 12}
+    if sequential:
+        wl["form"] = "sequential chain search (cfp_dp_chain), not the scan"
+    if cfg.form == "seg":
+        wl = {"workload": cfg.name, "segments": cfg.N, "plans": cfg.K, "searches": cfg.B,
+              "boundary_tables": "2 x 3 x 3", "blocks_per_segment": 4, "strategies_per_block": 3}
+    if cfg.form == "mem":
+        wl.update({"memory_buckets": cfg.M, "budgets": "every budget 0..M-1" if frontier else "1023-32b"})
+    kernel = KERNELS[cfg.name][0]
+    if sequential:
+        kernel = SEQUENTIAL_KERNEL
+    mode = "frontier" if frontier else ""
+    rec = {
+        "config": wl,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": ms_per_step,
+        "value": value,
+        "unit": "cell/s",
+        "forward_ms": fwd_ms,
+        "traceback_ms": tb_ms,
+        "parity_vs_oracle": parity,
+        "roofline": {"bound": "alu", "achieved": kern_cells_s / 1e12, "peak": PEAK_CELLS / 1e12, "unit": "Tcell/s",
+                     "frac": kern_cells_s / PEAK_CELLS,
+                     "traffic": None if sequential else traffic_bytes(cfg.name, mode),
+                     "kernel": kernel,
+                     "kernel_launches_per_step": kern_launches / steps,
+                     "kernel_avg_us": kern_avg_ms * 1e3,
+                     "forward_call_cells_per_s": fwd_cells_s,
+                     "forward_call_frac": fwd_cells_s / PEAK_CELLS,
+                     "step_frac": (work / (ms_per_step * 1e-3)) / PEAK_CELLS},
+    }
+    if cfg.form == "scan":
+        rec["roofline"]["cells_counted"] = ("min-plus matrix-product cells (N-1)*K^3 per search; value counts "
+                                            "K^2 per block per search")
+        rec["scan_gemm_cells_per_s"] = work / (ms_per_step * 1e-3)
+    if cfg.form == "seg":
+        rec["roofline"]["cells_counted"] = ("chain-equivalent K^2 per segment step; the factorised step does "
+                                            "K + L*F work, so the fraction is not a VALU utilisation")
+    if cfg.N <= 64 and cfg.B == 1:
+        rec["search_latency_us"] = search_latency_us(r.stream)
+    if cpu_s > 0:
+        rec["cpu_baseline"] = cpu_baseline(cfg, data, budget_s=cpu_s)
+    del r
+    torch.cuda.empty_cache()
+    return rec
+
+
+# Records of the default run, in order; the headline is the largest workload.
+ALL_RUNS = [("chain_gpt_n24_k16", {}), ("chain_gpt_n1152_k64", {}), ("mem_llama_n288_k32", {}),
+            ("mem_llama_n288_k32", {"frontier": True}), ("chain_wide_n512_k256", {}),
+            ("scan_n4096_k512", {}), ("scan_n4096_k512", {"sequential": True}), ("seg_gpt_n96_k81", {})]
+HEADLINE = "scan_n4096_k512"
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", default=DEFAULT_CONFIG)
+    ap.add_argument("--config", default=None,
+                    help="time one workload only (default: every workload, headline on the largest)")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=None,
+                    help="seconds of oracle work per CPU baseline (default 12 for the headline, 4 for the others)")
     ap.add_argument("--sequential", action="store_true",
-                    help="scan workload only: run the sequential chain kernels instead of the min-plus scan")
+                    help="scan workload only: run the sequential chain search instead of the min-plus scan")
     ap.add_argument("--frontier", action="store_true",
                     help="memory workload only: time the budget frontier (every budget 0..M-1 in one pass)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -297,119 +455,39 @@ def main() -> int:
               "would only split the batch; no multi-GPU path is built.", file=sys.stderr)
         return 2
 
-    import torch
+    base = {"metric": METRIC, "n_gpus": 1, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": "u32", "data": "synthetic"}
+    if args.config is not None:
+        cpu_s = 0.0 if args.no_cpu else (args.cpu_seconds or 10.0)
+        rec = measure(args.config, args.steps, args.warmup, cpu_s, frontier=args.frontier,
+                      sequential=args.sequential)
+        if "cpu_baseline" in rec:
+            rec["cpu_baseline"]["host"] = host_info()
+        out = dict(base, **rec)
+        print(json.dumps(out), flush=True)
+        return 0 if rec["parity_vs_oracle"] else 1
 
-    from workloads import configs
-
-    cfg = configs.BY_NAME[args.config]
-    data = configs.make(cfg)
-    if args.sequential:
-        if cfg.form != "scan":
-            raise SystemExit("--sequential applies to the scan workload")
-        import dataclasses
-
-        cfg = dataclasses.replace(cfg, form="chain")
-    if args.frontier:
-        data = dict(data, budget=np.full(cfg.B, cfg.M - 1, np.int32))  # the pass covers every budget
-    r = Runner(cfg, data, frontier=args.frontier)
-    for _ in range(args.warmup):
-        r.forward()
-        r.traceback()
-    torch.cuda.synchronize()
-
-    # Timed region: K whole steps (forward + traceback) with nothing else on the
-    # stream; an event record costs several microseconds of GPU time, so the
-    # per-phase split and the kernel timer come from a second, instrumented pass.
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        r.forward()
-        r.traceback()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
-           torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    # the library brackets each launch of the dominant kernel with HIP events
-    # on the stream it is launched on
-    L = r.L
-    L.cfp_timer_start(args.steps * 64)
-    torch.cuda.synchronize()
-    for a, m, b in ev:
-        a.record(r.stream)
-        r.forward()
-        m.record(r.stream)
-        r.traceback()
-        b.record(r.stream)
-    torch.cuda.synchronize()
-    kern_ms, kern_launches = L.cfp_timer_stop()
-    fwd_ms = float(np.mean([a.elapsed_time(m) for a, m, _ in ev]))
-    tb_ms = float(np.mean([m.elapsed_time(b) for _, m, b in ev]))
-    ms_per_step = wall * 1e3 / args.steps
-
-    cells = cells_of(cfg, data)
-    value = cells / (ms_per_step * 1e-3)
-    work = scan_gemm_cells(cfg) if cfg.form == "scan" else cells
-    # per launch: the algorithmic cells of one launch over its average duration
-    # (the scan's products differ in size per level: total cells over total time)
-    kern_avg_ms = kern_ms / max(kern_launches, 1)
-    kern_cells_s = work * args.steps / (kern_ms * 1e-3) if kern_launches else 0.0
-    fwd_cells_s = work / (fwd_ms * 1e-3)
-
-    o_opt, o_plan, o_st = run_oracle(cfg, data)
-    g_opt = r.frontier[:, -1].cpu().numpy() if args.frontier else r.opt.cpu().numpy()
-    parity = bool(np.array_equal(g_opt, o_opt) and np.array_equal(r.plan.cpu().numpy(), o_plan)
-                  and np.array_equal(r.status.cpu().numpy(), o_st))
-    if args.frontier:
-        from oracle import oracle as O
-
-        parity = parity and bool(np.array_equal(
-            r.frontier.cpu().numpy(),
-            O.mem_frontier(data["cost"], data["rtab"], data["redge"], data["mem"], cfg.M, nthreads=oracle_threads())))
-
-    wl = {"workload": cfg.name, "blocks": cfg.N, "strategies": cfg.K, "searches": cfg.B, "resharding_tables": 12}
-    if args.sequential:
-        wl["form"] = "sequential chain (not the scan)"
-    if cfg.form == "seg":
-        wl = {"workload": cfg.name, "segments": cfg.N, "plans": cfg.K, "searches": cfg.B,
-              "boundary_tables": "2 x 3 x 3", "blocks_per_segment": 4, "strategies_per_block": 3}
-    if cfg.form == "mem":
-        wl.update({"memory_buckets": cfg.M, "budgets": "every budget 0..M-1" if args.frontier else "1023-32b"})
-    out = {
-        "metric": METRIC,
-        "value": value,
-        "unit": "cell/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "u32",
-        "data": "synthetic",
-        "config": wl,
-        "forward_ms": fwd_ms,
-        "traceback_ms": tb_ms,
-        "search_latency_us": search_latency_us(r.stream),
-        "pcie_inclusive": pcie_inclusive(r, data),
-        "parity_vs_oracle": parity,
-        "roofline": {"bound": "alu", "achieved": kern_cells_s / 1e12, "peak": PEAK_CELLS / 1e12, "unit": "Tcell/s",
-                     "frac": kern_cells_s / PEAK_CELLS,
-                     "traffic": None if args.sequential else traffic_bytes(cfg.name, "frontier" if args.frontier else ""),
-                     "kernel": "chain_fwd_split_kernel<512>" if args.sequential else KERNELS[cfg.name][0],
-                     "kernel_launches_per_step": kern_launches / args.steps,
-                     "kernel_avg_us": kern_avg_ms * 1e3, "forward_call_cells_per_s": fwd_cells_s},
-    }
-    if cfg.form == "scan":
-        out["roofline"]["cells_counted"] = "min-plus matrix-product cells (N-1)*K^3 per search"
-    if cfg.form == "seg":
-        out["roofline"]["cells_counted"] = ("chain-equivalent K^2 per segment step; the factorised step does "
-                                            "K + L*F work, so the fraction is not a VALU utilisation")
-    if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(cfg, data)
+    records = {}
+    for name, kw in ALL_RUNS:
+        key = name + "".join(":" + k for k in sorted(kw))
+        head = key == HEADLINE
+        cpu_s = 0.0 if args.no_cpu else (args.cpu_seconds or (12.0 if head else 4.0))
+        print(f"bench: {key}", file=sys.stderr, flush=True)
+        records[key] = measure(name, args.steps, args.warmup, cpu_s, **kw)
+    head = records[HEADLINE]
+    out = dict(base)
+    for k in ("value", "unit", "steps", "warmup", "ms_per_step", "config", "forward_ms", "traceback_ms",
+              "parity_vs_oracle", "roofline", "scan_gemm_cells_per_s", "cpu_baseline"):
+        if k in head:
+            out[k] = head[k]
+    out["config"] = dict(head["config"], note="largest workload; every workload is in `configs`")
+    if "cpu_baseline" in out:
+        out["cpu_baseline"] = dict(out["cpu_baseline"], host=host_info())
+    out["search_latency_us"] = records["chain_gpt_n24_k16"].get("search_latency_us")
+    out["parity_all"] = all(r["parity_vs_oracle"] for r in records.values())
+    out["configs"] = records
     print(json.dumps(out), flush=True)
-    return 0 if parity else 1
+    return 0 if out["parity_all"] else 1
 
 
 if __name__ == "__main__":

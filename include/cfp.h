@@ -185,7 +185,7 @@ int cfp_traceback(const cfp_chain_desc *d, int32_t variant, int32_t n_mem, void 
 /* Segment-level search (Sec. 4.2-4.4).  The units are model segments; the
  * plan t of a segment combines the strategies of its blocks (K = prod of the
  * block strategy counts, e.g. 3^4 = 81 for four blocks of three strategies,
- * Sec. 6.5).  Resharding between consecutive segments is profiled only for
+ * Sec. 5.5).  Resharding between consecutive segments is profiled only for
  * the boundary block pair (Sec. 4.2), so Eq. T's resharding term is
  *     R_{e(i)}[t][s] = rbound[e(i)][last[t]][first[s]]
  * with last[t] the strategy of the last block of plan t and first[s] that of

@@ -27,7 +27,8 @@ struct WsHeader {
   int32_t variant, n, k, batch, n_mem, elem;  // elem: bytes per argmin entry
   int32_t rflag;                               // set to 1 by the device if rtab breaks its range
   // Paths that do not upload the header flag a range error with the number of
-  // the call instead (no reset needed: a stale value never equals a new number).
+  // the call instead (no reset needed: call numbers start at a random point per
+  // process and have the top bit set, so stale workspace bytes do not match).
   uint64_t rseq;
   int32_t pad[54];
 };

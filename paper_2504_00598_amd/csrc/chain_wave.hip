@@ -52,6 +52,8 @@
 // 12, the period of the edge map the kernels are specialised for.
 #include <algorithm>
 #include <atomic>
+#include <chrono>
+#include <random>
 
 #include "res_common.h"
 
@@ -672,6 +674,27 @@ static void launch_wave_passes(const WaveArgs &a, const WsHeader *hdr, SearchRes
                      status);
 }
 
+// Number of a call, stored as the range flag of a workspace whose header is
+// not uploaded.  The word starts as whatever the workspace held, so the
+// numbers must not be guessable from stale bytes: the sequence starts at a
+// random 64-bit point drawn once per process and every number has its top bit
+// set, so no zero word (what an upload writes) and no small or non-negative
+// integer left in the workspace ever equals one.
+static uint64_t next_call_number() {
+  static std::atomic<uint64_t> counter{0};
+  static const uint64_t base = [] {
+    std::random_device rd;
+    uint64_t x = ((uint64_t)rd() << 32) ^ (uint64_t)rd();
+    x ^= (uint64_t)std::chrono::steady_clock::now().time_since_epoch().count();
+    // SplitMix64 finaliser (Steele, Lea and Flood, OOPSLA 2014)
+    x += 0x9E3779B97F4A7C15ull;
+    x = (x ^ (x >> 30)) * 0xBF58476D1CE4E5B9ull;
+    x = (x ^ (x >> 27)) * 0x94D049BB133111EBull;
+    return x ^ (x >> 31);
+  }();
+  return (base + counter.fetch_add(1, std::memory_order_relaxed)) | (1ull << 63);
+}
+
 // Period of the edge map if redge[i] == i mod E for all i >= 1 with E
 // dividing 12, else 0.
 static int wave_edge_period(const int32_t *redge, int n, int e) {
@@ -727,8 +750,7 @@ hipError_t launch_chain_wave(const cfp_chain_desc &d, const int32_t *redge_dev, 
   a.ckrow = (uint32_t *)(region + off);
   off += align_up((size_t)d.batch * c.nq * 64 * 4);
   a.endrow = (uint32_t *)(region + off);
-  static std::atomic<uint64_t> call_seq{0};
-  a.seq = call_seq.fetch_add(1, std::memory_order_relaxed) + 1;  // never 0, which an upload writes
+  a.seq = next_call_number();
   hipLaunchKernelGGL(wave_pack_kernel, dim3(std::min(1024, d.n_tables * 16)), dim3(256), 0, st, d.rtab, d.n_tables,
                      d.k, rpk, cfp_r_limit(CFP_V_CHAIN, d.k), const_cast<WsHeader *>(hdr), a.seq);
   if (wave_edge_period(d.redge, d.n_blocks, d.n_tables) == 12) launch_wave_passes<12>(a, hdr, res, opt, status, st);

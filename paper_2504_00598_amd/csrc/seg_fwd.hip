@@ -5,7 +5,7 @@
 // cost between consecutive segments depends only on the strategy of the
 // earlier segment's last block and of the later segment's first block: only
 // those boundary block pairs are profiled (Sec. 4.2; 3 x 3 = 9 pairs for
-// segments of four blocks with three strategies each, Sec. 6.5).  So Eq. T's
+// segments of four blocks with three strategies each, Sec. 5.5).  So Eq. T's
 // resharding term is r_e[last(t)][first(s)] and the step of the recurrence
 // factorises:
 //     D[i][s] = c[i][s] + min_l (M_l + r_{e(i)}[l][first(s)]),

@@ -394,3 +394,31 @@ def test_range_flag_does_not_leak_between_calls():
     torch.cuda.synchronize()
     np.testing.assert_array_equal(r4.opt.cpu().numpy(), o_opt)
     np.testing.assert_array_equal(r4.plan.cpu().numpy(), o_plan)
+
+
+def test_range_flag_ignores_stale_workspace_bytes():
+    """The headerless K=64 path keeps its range flag in a workspace word that no
+    upload clears.  Fresh workspaces whose flag word holds small integers,
+    all-ones, or other leftovers (a freed plan row, an earlier cost) must still
+    give a clean search."""
+    need_gpu()
+    import torch
+    from paper_2504_00598_amd import _lib as L, search
+    say("range flag with stale workspace bytes")
+    rs = np.random.default_rng(63)
+    B, N, K = 70, 400, 64
+    cost = rs.integers(0, 1000, size=(B, N, K)).astype(np.int32)
+    rtab = rs.integers(0, 1000, size=(12, K, K)).astype(np.int32)
+    periodic = (np.arange(N) % 12).astype(np.int32)
+    o_opt, o_plan, o_st = O.chain(cost, rtab, periodic, nthreads=oracle_threads())
+    d = L.Desc(dev(cost), dev(rtab), periodic)
+    nbytes = L.cfp_workspace_bytes(d, L.CFP_V_CHAIN)
+    words = list(range(0, 65)) + [-1, 2**31 - 1, 2**32, 2**63 - 1, -(2**63), int(rs.integers(0, 2**62))]
+    for v in words:
+        ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        ws[:64].view(torch.int64)[:] = v   # every 8-byte word of the first 64 bytes, the flag word among them
+        r = search.dp_chain(d.cost, d.rtab, periodic, ws=ws)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(r.status.cpu().numpy(), o_st, err_msg=f"status, stale word {v}")
+        np.testing.assert_array_equal(r.opt.cpu().numpy(), o_opt, err_msg=f"opt, stale word {v}")
+        np.testing.assert_array_equal(r.plan.cpu().numpy(), o_plan, err_msg=f"plan, stale word {v}")

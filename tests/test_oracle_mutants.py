@@ -40,6 +40,15 @@ MUTANTS = {
     "mem_shift_ignored": (
         "int64_t v = add_inf(D[DIDX(i - 1, t, m - ms)], (int64_t)R[(size_t)t * K + s]);",
         "int64_t v = add_inf(D[DIDX(i - 1, t, m)], (int64_t)R[(size_t)t * K + s]);"),
+    "plan_mem_drops_block0": (
+        "for (int i = 0; i < N; ++i) m += mem[(size_t)i * K + plan[i]];",
+        "for (int i = 1; i < N; ++i) m += mem[(size_t)i * K + plan[i]];"),
+    "plan_cost_drops_first_edge": (
+        "for (int i = 1; i < N; ++i) {\n    const int32_t *R = rtab + (size_t)redge[i] * K * K;\n    t = add_inf",
+        "for (int i = 2; i < N; ++i) {\n    const int32_t *R = rtab + (size_t)redge[i] * K * K;\n    t = add_inf"),
+    "plan_cost_transposed_R": (
+        "t = add_inf(t, (int64_t)R[(size_t)plan[i - 1] * K + plan[i]]);",
+        "t = add_inf(t, (int64_t)R[(size_t)plan[i] * K + plan[i - 1]]);"),
     "mem_budget_exclusive": (
         "D[DIDX(0, s, m)] = (mem[s] <= m) ? cost_value(c[s]) : ORC_INF;",
         "D[DIDX(0, s, m)] = (mem[s] < m) ? cost_value(c[s]) : ORC_INF;"),
@@ -74,6 +83,15 @@ def pins_pass() -> bool:
                 bopt, bplan, ok = brute.solve(cost, rtab, redge, mem, budget)
                 if (st == 0) != ok or (ok and (opt != bopt or not np.array_equal(plan, bplan))):
                     return False
+    # the plan evaluators against Eq. T / Eq. M summed by the enumeration helpers
+    for N, K in [(1, 3), (4, 3), (9, 5)]:
+        cost, rtab, redge = rand_chain(rs, N, K, 3, 0, 1000)
+        mem = rs.integers(0, 9, size=(N, K)).astype(np.uint8)
+        plans = rs.integers(0, K, size=(8, N)).astype(np.int64)
+        T, Mm = brute.eq_T(cost, rtab, redge, plans), brute.eq_M(mem, plans)
+        for p, t, m in zip(plans, T, Mm):
+            if O.plan_cost(cost, rtab, redge, p) != t or O.plan_mem(mem, p) != m:
+                return False
     cost, rtab, redge = rand_chain(rs, 30, 8, 4, 10_000, 10**6)
     opt, _, _ = O.chain(cost, rtab, redge)
     return opt == dijkstra_cost(cost, rtab, redge)

@@ -233,6 +233,32 @@ def test_plan_cost_equals_opt(N, K):
     assert O.plan_cost(cost, rtab, redge, plan) == opt
 
 
+@pytest.mark.parametrize("N,K,E", [(1, 1, 1), (1, 5, 2), (2, 3, 1), (7, 4, 3), (40, 9, 5), (300, 33, 12)])
+def test_plan_evaluators_vs_direct_sums(N, K, E):
+    """oracle_plan_cost and oracle_plan_mem on arbitrary plans (not only the
+    optimal one) equal Eq. T and Eq. M summed directly by the enumeration
+    helpers: every block's cost and memory, every edge's table entry, and
+    +inf for a plan through an unavailable strategy."""
+    rs = np.random.default_rng([rng_seed + 30, N, K, E])
+    cost, rtab, redge = rand_chain(rs, N, K, E, 0, 2**31 - 1, inf_frac=0.05)
+    mem = rs.integers(0, 256, size=(N, K)).astype(np.uint8)
+    plans = rs.integers(0, K, size=(50, N)).astype(np.int64)
+    T = brute.eq_T(cost, rtab, redge, plans)
+    Mm = brute.eq_M(mem, plans)
+    for p, t, m in zip(plans, T, Mm):
+        assert O.plan_cost(cost, rtab, redge, p) == t
+        assert O.plan_mem(mem, p) == m
+    # a hand-summed case: block 0 alone carries all the memory and the cost
+    cost1 = np.zeros((N, K), np.int32)
+    cost1[0, :] = 7
+    mem1 = np.zeros((N, K), np.uint8)
+    mem1[0, :] = 3
+    z = np.zeros((E, K, K), np.int32)
+    p0 = np.zeros(N, np.int64)
+    assert O.plan_cost(cost1, z, redge, p0) == 7
+    assert O.plan_mem(mem1, p0) == 3
+
+
 def test_shift_invariance():
     rs = np.random.default_rng(rng_seed + 9)
     N, K, E = 60, 12, 4
