@@ -27,7 +27,7 @@ WsLayout layout(int variant, int n, int k, int batch, int n_mem, int n_tables) {
     L.mem = off;
     off = align_up(off + cells);
     L.memreg = off;
-    L.memreg_bytes = mem_region_bytes(n, k, batch, n_mem);
+    L.memreg_bytes = mem_region_bytes(n, k, batch, n_mem, n_tables);
     off = align_up(off + L.memreg_bytes);
     L.fbudget = off;
     off = align_up(off + (size_t)batch * 4);
@@ -205,7 +205,7 @@ int32_t cfp_r_limit(int32_t variant, int32_t k) {
     case CFP_V_SCAN:
       return k <= 64 ? (int32_t)(1u << (30 - b)) : (int32_t)((1u << (32 - b)) - 1u);
     case CFP_V_MEM:
-      return k <= 32 ? (int32_t)(1u << (31 - b)) : 0;
+      return mem_r_limit(k);
     case CFP_V_SEG:
       return (int32_t)((1u << (32 - b)) - 1u);
     default:

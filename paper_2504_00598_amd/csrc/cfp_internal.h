@@ -110,7 +110,8 @@ hipError_t launch_chain_fwd_generic(const cfp_chain_desc &d, const int32_t *redg
                                     SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
                                     hipStream_t st);
 bool chain_mem_supported(int k, int n_tables);
-size_t mem_region_bytes(int n, int k, int batch, int n_mem);
+int32_t mem_r_limit(int k);
+size_t mem_region_bytes(int n, int k, int batch, int n_mem, int n_tables);
 hipError_t launch_chain_mem_fwd(const cfp_chain_desc &d, const uint8_t *mem, int n_mem, const int32_t *budget,
                                 const int32_t *redge_dev, uint8_t *table, uint8_t *mem_copy, uint8_t *region,
                                 SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,

@@ -46,6 +46,11 @@ def test_r_limit_values():
     assert L.cfp_r_limit(L.CFP_V_CHAIN, 513) == 0
     assert L.cfp_r_limit(L.CFP_V_CHAIN, 0) == 0
     assert L.cfp_r_limit(L.CFP_V_MEM, 32) == 2 ** 26
+    assert L.cfp_r_limit(L.CFP_V_MEM, 16) == 2 ** 26
+    assert L.cfp_r_limit(L.CFP_V_MEM, 64) == 2 ** 25
+    assert L.cfp_r_limit(L.CFP_V_MEM, 81) == 2 ** 24
+    assert L.cfp_r_limit(L.CFP_V_MEM, 256) == 2 ** 23
+    assert L.cfp_r_limit(L.CFP_V_MEM, 257) == 0
     assert L.cfp_r_limit(7, 32) == 0
     # the five workloads' resharding ranges fit their limits
     assert 10_000_000 < L.cfp_r_limit(L.CFP_V_CHAIN, 64)
@@ -83,7 +88,9 @@ def test_workspace_sizes():
     d = HostDesc(N=1152, K=64, B=256)
     chain = lib.cfp_workspace_bytes(d.ref, L.CFP_V_CHAIN, 0)
     assert chain >= 256 * 1152 * 64  # one argmin byte per (search, block, state)
-    assert lib.cfp_workspace_bytes(d.ref, L.CFP_V_MEM, 1024) == 0  # memory variant: K <= 32
+    assert lib.cfp_workspace_bytes(d.ref, L.CFP_V_MEM, 1024) > 0   # memory variant: K <= 256, any tables
+    wide = HostDesc(N=10, K=257, B=2)
+    assert lib.cfp_workspace_bytes(wide.ref, L.CFP_V_MEM, 64) == 0  # beyond the memory variant's K
     dm = HostDesc(N=288, K=32, B=16)
     mem = lib.cfp_workspace_bytes(dm.ref, L.CFP_V_MEM, 1024)
     assert mem >= 16 * 288 * 32 * 1024  # one argmin byte per (search, block, state, bucket)

@@ -87,3 +87,25 @@ def test_statuses():
     assert st[2] == CFP_ST_BADINPUT and (f[2] == INF64).all() and (plan[2] == -1).all()
     good = [0, 3]
     assert_frontier_parity(cost[good], rtab, redge, mem[good], 64, "inf")
+
+
+@pytest.mark.parametrize("N,K,E,M", [(30, 81, 12, 130), (20, 256, 3, 70), (40, 48, 17, 200)])
+def test_wide_states_and_many_tables(N, K, E, M):
+    need_gpu()
+    say("frontier wide", N, K, E, M)
+    rs = np.random.default_rng([22, N, K, E])
+    cost = rs.integers(10_000, 1_000_000, size=(3, N, K)).astype(np.int32)
+    rtab = rs.integers(10_000, 1_000_000, size=(E, K, K)).astype(np.int32)
+    redge = rs.integers(0, E, size=N).astype(np.int32)
+    mem = rs.integers(0, 9, size=(3, N, K)).astype(np.uint8)
+    assert_frontier_parity(cost, rtab, redge, mem, M, f"wide K={K}")
+
+
+def test_repeat_is_bit_identical():
+    need_gpu()
+    d = configs.make("mem_llama_n288_k32")
+    first = run_frontier(d["cost"], d["rtab"], d["redge"], d["mem"], d["M"])
+    for _ in range(3):
+        again = run_frontier(d["cost"], d["rtab"], d["redge"], d["mem"], d["M"])
+        for a, b in zip(first, again):
+            np.testing.assert_array_equal(a, b)

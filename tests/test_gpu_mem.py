@@ -111,3 +111,93 @@ def test_periodic_layers():
     redge = (np.arange(N) % 12).astype(np.int32)
     budget = np.array([60, 120, 200, 299], np.int32)
     assert_mem_parity(cost, rtab, redge, mem, M, budget, "periodic")
+
+
+# The memory search takes any K up to 256 (padded to 32, 64, 96, 128, 192 or
+# 256 states per workgroup) and any number of resharding tables (streamed from
+# the cache): a segment of four blocks of three strategies has 81 plans
+# (Sec. 5.5), and its memory is the sum over its blocks (Eq. M).
+
+@pytest.mark.parametrize("N,K,E,M", [(40, 33, 12, 200), (40, 64, 12, 260), (30, 81, 12, 150), (25, 128, 5, 140),
+                                     (20, 200, 3, 120), (16, 256, 12, 100), (50, 32, 20, 300), (30, 17, 40, 90)])
+def test_wide_states_and_many_tables(N, K, E, M):
+    """Budgets that bind (between the least-memory plan and the unconstrained plan's memory), ragged K."""
+    need_gpu()
+    from oracle import oracle as O
+    from paper_2504_00598_amd import cfp_r_limit
+    say("mem wide", N, K, E, M)
+    rs = np.random.default_rng([15, N, K, E, M])
+    B = 5
+    cost = rs.integers(10_000, 1_000_000, size=(B, N, K)).astype(np.int32)
+    rtab = rs.integers(10_000, min(1_000_000, cfp_r_limit(1, K)), size=(E, K, K)).astype(np.int32)
+    rtab[:, np.arange(K), np.arange(K)] = 0
+    redge = rs.integers(0, E, size=N).astype(np.int32)
+    mem = rs.integers(0, 9, size=(B, N, K)).astype(np.uint8)
+    lo = mem.min(axis=2).sum(axis=1)
+    _, free_plan, _ = O.chain(cost, rtab, redge)
+    used = np.array([int(mem[b][np.arange(N), free_plan[b]].sum()) for b in range(B)])
+    budget = np.minimum(M - 1, lo + (np.minimum(used, M - 1) - lo) * np.array([0, 1, 2, 3, 4]) // 5).astype(np.int32)
+    budget[4] = M - 1
+    g_opt, _ = assert_mem_parity(cost, rtab, redge, mem, M, budget, f"wide N={N} K={K} E={E} M={M}")
+    assert (budget[:4] < used[:4]).all() or (lo == used).any()
+
+
+def test_segment_plans_k81():
+    """A memory search over model segments: 4 blocks x 3 strategies = 81 plans,
+    plan cost = sum of its blocks' costs, plan memory = sum of its blocks'
+    memory, resharding between segments from the boundary block pair only
+    (the expanded 81 x 81 table of Sec. 4.2)."""
+    need_gpu()
+    from oracle import oracle as O
+    say("mem segment plans K=81")
+    rs = np.random.default_rng(16)
+    B, N, M = 4, 48, 400
+    P, S = 4, 3
+    K = S ** P
+    digits = np.array([[(t // S ** j) % S for j in range(P)] for t in range(K)])  # block strategies of plan t
+    bc = rs.integers(10_000, 1_000_000, size=(B, N, P, S))
+    bm = rs.integers(0, 3, size=(B, N, P, S))
+    cost = np.zeros((B, N, K), np.int64)
+    mem = np.zeros((B, N, K), np.int64)
+    for j in range(P):
+        cost += bc[:, :, j, :][:, :, digits[:, j]]
+        mem += bm[:, :, j, :][:, :, digits[:, j]]
+    cost = cost.astype(np.int32)
+    mem = mem.astype(np.uint8)
+    rbound = rs.integers(10_000, 10_000_000, size=(2, S, S)).astype(np.int32)
+    rbound[:, np.arange(S), np.arange(S)] = 0
+    last = digits[:, P - 1].astype(np.uint8)
+    first = digits[:, 0].astype(np.uint8)
+    rtab = O.expand_boundary(rbound, last, first)
+    redge = np.ones(N, np.int32)
+    redge[1] = 0
+    lo = mem.min(axis=2).sum(axis=1)
+    budget = np.minimum(M - 1, lo + np.array([0, 20, 60, 400])).astype(np.int32)
+    assert_mem_parity(cost, rtab, redge, mem, M, budget, "segment plans K=81")
+
+
+def test_launch_rounds():
+    """Many searches with many 64-bucket chunks each: the chunks of one launch
+    must be resident together, so the searches run in several rounds."""
+    need_gpu()
+    say("mem launch rounds")
+    rs = np.random.default_rng(17)
+    B, N, K, M = 40, 20, 8, 4096
+    cost = rs.integers(0, 1000, size=(B, N, K)).astype(np.int32)
+    rtab = rs.integers(0, 1000, size=(3, K, K)).astype(np.int32)
+    redge = (np.arange(N) % 3).astype(np.int32)
+    mem = rs.integers(0, 17, size=(B, N, K)).astype(np.uint8)
+    budget = rs.integers(0, M, size=B).astype(np.int32)
+    budget[:4] = M - 1
+    assert_mem_parity(cost, rtab, redge, mem, M, budget, "rounds")
+
+
+def test_repeat_is_bit_identical():
+    """The chunk pipeline gives the same bits on every run."""
+    need_gpu()
+    d = configs.make("mem_llama_n288_k32")
+    first = run_mem(d["cost"], d["rtab"], d["redge"], d["mem"], d["M"], d["budget"])
+    for _ in range(3):
+        again = run_mem(d["cost"], d["rtab"], d["redge"], d["mem"], d["M"], d["budget"])
+        for a, b in zip(first, again):
+            np.testing.assert_array_equal(a, b)
