@@ -57,8 +57,7 @@ namespace cfp {
 
 constexpr int kMemChunk = 64;        // buckets per workgroup
 constexpr int kMemShift = 16;        // largest supported mem entry = halo width = buckets per wave
-constexpr int kMemWaves = 4;                  // compute waves per workgroup
-constexpr int kMemThreads = 64 * (kMemWaves + 2);  // and a loading and a storing wave
+constexpr int kMemBlocks = 4;        // bucket blocks of 16 per chunk
 constexpr int kMemSlots = 8;         // ring slots per chunk
 constexpr int kMemFlagStride = 16;   // ints per chunk flag (one 64-byte line each)
 constexpr int kMemMaxK = 256;
@@ -74,15 +73,17 @@ enum { MEMF_BAD = 1, MEMF_TIMEOUT = 2 };
 template <int KP>
 struct MemShape {
   static constexpr int BITS = KP <= 32 ? 5 : KP <= 64 ? 6 : KP <= 128 ? 7 : 8;
+  static constexpr bool ALIAS = KP > 128;   // rows kept in the product buffer, single-buffered
+  static constexpr int CW = kMemBlocks;     // compute waves, one per bucket block
+  static constexpr int THREADS = 64 * (CW + 2);    // and a loading and a storing wave
   static constexpr int SPL = KP / 4;        // states per lane
   static constexpr int TB = KP / 32;        // blocks of 32 predecessors
-  static constexpr bool ALIAS = KP > 128;   // rows kept in the product buffer, single-buffered
-  static constexpr bool RLDS = KP <= 64;    // tables staged in LDS by the I/O wave
+  static constexpr bool RLDS = KP <= 64;    // tables staged in LDS by the loading wave
   static constexpr int SP = kMemShift + kMemChunk + 1;  // product buffer row stride (words)
   static constexpr int QS = KP + 4;         // row stride of a wave's rows (words)
   static constexpr uint32_t QCAP = 1u << (31 - BITS);
   static constexpr uint32_t MASK = (1u << BITS) - 1u;
-  static_assert(SPL % kMemPD == 0 && SPL % 4 == 0, "items and record words per lane");
+  static_assert(SPL % kMemPD == 0 && SPL % 4 == 0 && SPL % 2 == 0, "items and record words per lane");
 };
 
 static int mem_kp(int k) { return k <= 32 ? 32 : k <= 64 ? 64 : k <= 96 ? 96 : k <= 128 ? 128 : k <= 192 ? 192 : 256; }
@@ -225,45 +226,49 @@ __device__ __forceinline__ bool spin_until(const int32_t *flag, int target, int 
   return true;
 }
 
-// Work split.  Waves 0..3 compute (wave w owns buckets 16w .. 16w+15 of the
-// chunk, all states); wave 4 does every global load of a step (the chunk
-// below's top products into the halo columns, the next steps' tables and
-// records into LDS) and wave 5 every global store (the chunk's top products
-// to the ring for the chunk above, the argmin bytes to the table).  Loads and
-// stores of one wave complete in order, so a wave that both stored and loaded
-// would wait for its stores whenever it needed a load; the compute waves
-// issue no global stores at all and, when the tables fit in LDS (K <= 64), no
-// global loads either.  One barrier per step (two when the rows share the
-// product buffer) orders the three kinds of waves.
+// Work split.  Compute wave w owns bucket block w of the chunk (buckets
+// 16w .. 16w+15); its lane (g, m) has bucket 16w + m and the K/4 states of row
+// g.  (Two waves per block, each with half of the states, were measured
+// slower: the products already keep a SIMD's vector unit busy, and the pair
+// costs two more barriers per step.)  Of the two I/O waves one does
+// every global load of a step (the chunk below's top products into the halo
+// columns, the next steps' tables and records into LDS) and one every global
+// store (the chunk's top products to the ring for the chunk above, the argmin
+// bytes to the table).  Loads and stores of one wave complete in order, so a
+// wave that both stored and loaded would wait for its stores whenever it
+// needed a load; the compute waves issue no global stores at all and, when
+// the tables fit in LDS (K <= 64), no global loads either.
 //
-// Schedule of step i (P_i: products of step i, o_i: offsets after step i):
-//   compute: products from Q_{i-1} and the table of step i -> P_i in the
-//            product buffer                                              | barrier
+// Barriers of step i (P_i: products of step i, o_i: offsets after step i):
+//   compute: products from Q_{i-1} and the table of step i -> P_i      | B
 //            shifted products, offset gaps, bucket minima -> Q_i, o_i,
-//            argmin bytes of step i
-//   loads, before the barrier of step i: halo of step i (slot i of the chunk
-//            below: P_i and o_{i-1} of its top buckets), table of step i+1,
-//            records of step i;
-//   stores, before the barrier of step i: slot i-1 of this chunk (P_{i-1},
-//            o_{i-2}; both complete at the previous barrier), argmin bytes of
-//            step i-2.
+//            argmin bytes of step i (K > 128: the rows overwrite the
+//            products, after a second barrier B2)
+//   I/O, between the previous step's last barrier and B: halo of step i
+//            (slot i of the chunk below: P_i and o_{i-1} of its top
+//            buckets), table and records of step i+1, slot i-1 of this
+//            chunk (P_{i-1}, o_{i-2}), argmin bytes of step i-2 (K > 128:
+//            of step i-1, and slot i between B and B2, before the rows
+//            overwrite P_i).
 // The edge map and the least shifts are read through restrict-qualified
 // arguments, so that their uniform per-step loads are scalar loads.
 template <int KP>
-__global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(MemArgs a, const int32_t *__restrict__ redge,
-                                                              const int32_t *__restrict__ dmin) {
+__global__ __launch_bounds__(MemShape<KP>::THREADS) void mem_fwd_kernel(MemArgs a, const int32_t *__restrict__ redge,
+                                                                        const int32_t *__restrict__ dmin) {
   using S = MemShape<KP>;
   constexpr int BITS = S::BITS, SPL = S::SPL, TB = S::TB, H = kMemShift, C = kMemChunk, SP = S::SP;
   constexpr uint32_t QCAP = S::QCAP;
   constexpr bool ALIAS = S::ALIAS, RLDS = S::RLDS;
+  constexpr int CW = S::CW;
+  constexpr int FL = ALIAS ? 1 : 2;  // the argmin bytes of step t are written back during step t + FL
   constexpr int NPB = ALIAS ? 1 : 2;
   constexpr int PD = kMemPD;
-  constexpr int NW = kMemWaves;  // compute waves
+  constexpr int NBK = kMemBlocks;
 
   __shared__ uint32_t Pb[NPB][KP][SP];                                         // products (and, ALIAS, rows)
-  __shared__ __align__(16) uint32_t Qw[ALIAS ? 1 : NW][ALIAS ? 1 : 16][ALIAS ? 4 : S::QS];  // rows
+  __shared__ __align__(16) uint32_t Qw[ALIAS ? 1 : NBK][ALIAS ? 1 : 16][ALIAS ? 4 : S::QS];  // rows
   __shared__ int64_t offs[2][H + C];                                           // offsets by step parity
-  __shared__ __align__(16) uint8_t argb[2][NW][KP][16];                        // argmin bytes by step parity
+  __shared__ __align__(16) uint8_t argb[2][NBK][KP][16];                       // argmin bytes by step parity
   __shared__ __align__(16) uint32_t rbuf[RLDS ? 2 : 1][RLDS ? KP : 1][RLDS ? KP : 4];  // tables by step parity
   __shared__ __align__(16) uint32_t rcost[2][KP];                             // records by step parity
   __shared__ __align__(16) uint8_t rshift[2][KP];
@@ -274,16 +279,17 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(MemArgs a, const i
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const bool io = w >= NW;
+  const bool io = w >= CW;
+  const int blk = w;  // compute waves: bucket block
   const int g = lane >> 4, m = lane & 15;
-  const int col = H + 16 * w + m;  // compute waves: this lane's column
+  const int col = H + 16 * blk + m;  // compute waves: this lane's column
 
   const int bl = blockIdx.x % a.B8, j = blockIdx.x / a.B8;
   if (bl >= a.nb) return;
   const int b = a.b0 + bl;
   const int N = a.N, K = a.K, M = a.M;
   const int m0 = j * C;
-  const int bucket = m0 + 16 * w + m;
+  const int bucket = m0 + 16 * blk + m;
   const MemWs &W = a.w;
 
   if (W.mflags[b] & MEMF_BAD) {  // written by the prep kernel earlier in the stream
@@ -307,14 +313,10 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(MemArgs a, const i
   const bool vec16 = (M % 16) == 0;
   if (tid == 0) s_timeout = 0;
 
+
   if (io) {
     // ------------------------------------------------------------ I/O waves --
-    // Wave NW loads (slot i of the chunk below into the halo columns, the table
-    // of step i + 1, the records of step i, the progress of the chunk above)
-    // and wave NW + 1 stores (slot i - 1 of this chunk, the argmin bytes of step
-    // i - 2, this chunk's progress); loads and stores of one wave complete in
-    // order, so neither kind waits for the other.
-    const bool loader = w == NW;
+    const bool loader = w == CW;
     const size_t lo_id = consumer ? chunk_id - 1 : chunk_id;
     const size_t up_id = has_consumer ? chunk_id + 1 : chunk_id;
     int32_t *my_cons = W.cons + chunk_id * kMemFlagStride;
@@ -343,11 +345,33 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(MemArgs a, const i
           for (int u = 0; u < RW; ++u) ((u32x4 *)&rbuf[par][0][0])[lane + 64 * u] = rv[u];
         }
       };
-      if (RLDS && N > 1) {  // the table of step 1
-        load_table(redge[1]);
-        store_table(1);
+      // records of step t into parity buffer t & 1: KP costs and KP shift bytes,
+      // four per lane, and the least shift
+      auto stage_records = [&](int t, const u32x4 &c4, uint32_t s4, int dmt) __attribute__((always_inline)) {
+        if (lane < KP / 4) {
+          *(u32x4 *)&rcost[t & 1][4 * lane] = c4;
+          *(uint32_t *)&rshift[t & 1][4 * lane] = s4;
+        }
+        if (lane == 0) rdmin[t & 1] = dmt;
+      };
+      auto load_records = [&](int t, u32x4 &c4, uint32_t &s4) __attribute__((always_inline)) {
+        if (lane < KP / 4) {
+          c4 = *(const u32x4 *)(W.cst + (rowbase + t) * KP + 4 * lane);
+          s4 = *(const uint32_t *)(W.dsh + (rowbase + t) * KP + 4 * lane);
+        }
+      };
+      if (N > 1) {  // the table and the records of step 1
+        if (RLDS) load_table(redge[1]);
+        u32x4 c4 = {};
+        uint32_t s4 = 0;
+        load_records(1, c4, s4);
+        if (RLDS) store_table(1);
+        stage_records(1, c4, s4, dmin[rowbase + 1]);
       }
-      if (lane == 0) s_done = -1;
+      if (lane == 0) {
+        s_done = -1;
+        s_upcons = -1;
+      }
       __syncthreads();  // step 0 of the compute waves
       for (int i = 1; i < N; ++i) {
         const int par = i & 1, pprev = par ^ 1;
@@ -371,14 +395,10 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(MemArgs a, const i
           if (lane < 32) ho = __hip_atomic_load(src + 16 * KP + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         if (RLDS && i + 1 < N) load_table(redge[i + 1]);
-        // records of step i: KP costs and KP shift bytes, four per lane
-        u32x4 cpc = {};
+        u32x4 cpc = {};  // records of step i + 1
         uint32_t spc = 0;
-        if (lane < KP / 4) {
-          cpc = *(const u32x4 *)(W.cst + (rowbase + i) * KP + 4 * lane);
-          spc = *(const uint32_t *)(W.dsh + (rowbase + i) * KP + 4 * lane);
-        }
-        const int dmi = dmin[rowbase + i];
+        if (i + 1 < N) load_records(i + 1, cpc, spc);
+        const int dmi = i + 1 < N ? dmin[rowbase + i + 1] : 0;
         int upc = -1;
         if (has_consumer) upc = __hip_atomic_load(up_cons, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
@@ -413,16 +433,10 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(MemArgs a, const i
           if (lane == 0) s_done = i;  // published by the storing wave
         }
         if (RLDS && i + 1 < N) store_table(par ^ 1);
-        if (lane < KP / 4) {
-          *(u32x4 *)&rcost[par][4 * lane] = cpc;
-          *(uint32_t *)&rshift[par][4 * lane] = spc;
-        }
-        if (lane == 0) {
-          rdmin[par] = dmi;
-          s_upcons = upc;
-        }
-        __syncthreads();
-        if constexpr (ALIAS) __syncthreads();
+        if (i + 1 < N) stage_records(i + 1, cpc, spc, dmi);
+        if (lane == 0) s_upcons = upc;
+        __syncthreads();  // B
+        if constexpr (ALIAS) __syncthreads();  // B2
       }
       __syncthreads();  // the last step's rows, offsets and argmin bytes
     } else {
@@ -453,12 +467,12 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(MemArgs a, const i
       // Argmin bytes of step t (parity buffer t & 1) to the table, the buckets
       // within the budget only.
       auto flush = [&](int t) __attribute__((always_inline)) {
-        for (int x = lane; x < NW * K; x += 64) {
-          const int ww = x / K, s = x % K;
-          const int lim = top + 1 - (m0 + 16 * ww);
+        for (int x = lane; x < NBK * K; x += 64) {
+          const int bb = x / K, s = x % K;
+          const int lim = top + 1 - (m0 + 16 * bb);
           if (lim <= 0) continue;
-          uint8_t *dst = a.table + ((rowbase + t) * K + s) * (size_t)M + m0 + 16 * ww;
-          const u32x4 v = *(const u32x4 *)&argb[t & 1][ww][s][0];
+          uint8_t *dst = a.table + ((rowbase + t) * K + s) * (size_t)M + m0 + 16 * bb;
+          const u32x4 v = *(const u32x4 *)&argb[t & 1][bb][s][0];
           if (vec16 && lim >= 16) {
             *(u32x4 *)dst = v;
           } else {
@@ -482,24 +496,24 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(MemArgs a, const i
           wait_consumed(i - 1);
           store_slot(i - 1, (i - 1) & 1, (i - 2) & 1);
         }
-        if (i >= 3) flush(i - 2);
-        __syncthreads();
-        if constexpr (ALIAS) {  // P_i is overwritten by the rows after the second barrier
+        if (i - FL >= 1) flush(i - FL);  // written before the previous step's last barrier
+        __syncthreads();  // B
+        if constexpr (ALIAS) {  // P_i is overwritten by the rows after B2
           if (has_consumer) {
             wait_consumed(i);
             store_slot(i, 0, (i - 1) & 1);
           }
-          __syncthreads();
+          __syncthreads();  // B2
         }
       }
       __syncthreads();  // the last step's rows, offsets and argmin bytes
+      // the progress, slot N-1 (P_{N-1}, o_{N-2}) and the last steps' argmin bytes
       publish();
       if (!ALIAS && has_consumer && N >= 2) {
         wait_consumed(N - 1);
         store_slot(N - 1, (N - 1) & 1, (N - 2) & 1);
       }
-      if (N >= 3) flush(N - 2);
-      if (N >= 2) flush(N - 1);
+      for (int t = N - FL > 1 ? N - FL : 1; t < N; ++t) flush(t);
     }
     if (timeout) {
       s_timeout = 1;  // read by the reporting wave after the last barrier
@@ -512,7 +526,7 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(MemArgs a, const i
   // -------------------------------------------------------- compute waves --
   const int s0 = g * SPL;  // first state of this lane
 
-  // Rows of the lane's states to LDS: non-ALIAS the wave's row buffer
+  // Rows of the lane's states to LDS: non-ALIAS the block's row buffer
   // [bucket][state], ALIAS the wave's own columns of the product buffer.
   auto store_rows = [&](const uint32_t *q) __attribute__((always_inline)) {
     if constexpr (ALIAS) {
@@ -521,13 +535,12 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(MemArgs a, const i
     } else {
 #pragma unroll
       for (int v = 0; v < SPL / 4; ++v)
-        *(u32x4 *)&Qw[w][m][s0 + 4 * v] = u32x4{q[4 * v], q[4 * v + 1], q[4 * v + 2], q[4 * v + 3]};
+        *(u32x4 *)&Qw[blk][m][s0 + 4 * v] = u32x4{q[4 * v], q[4 * v + 1], q[4 * v + 2], q[4 * v + 3]};
     }
   };
 
   // Normalisation of the lane's values y (kSat = unreachable) against the
-  // bucket minimum; returns the new offset relative to `base`.  ALIAS: a
-  // barrier first, as the rows overwrite products other waves still read.
+  // bucket minimum over all states; returns the new offset relative to `base`.
   uint32_t y[SPL];
   auto normalise = [&](int64_t base) __attribute__((always_inline)) -> int64_t {
     uint32_t x = y[0];
@@ -558,8 +571,8 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(MemArgs a, const i
     if (g == 0) offs[0][col] = o0;
   }
   if (!consumer) {  // below bucket 0: infeasible
-    for (int x = tid; x < 2 * H; x += 64 * NW) offs[x / H][x % H] = kOffInf;
-    for (int x = tid; x < NPB * KP * H; x += 64 * NW) Pb[x / (KP * H)][(x / H) % KP][x % H] = kSat;
+    for (int x = tid; x < 2 * H; x += 64 * CW) offs[x / H][x % H] = kOffInf;
+    for (int x = tid; x < NPB * KP * H; x += 64 * CW) Pb[x / (KP * H)][(x / H) % KP][x % H] = kSat;
   }
   __syncthreads();
 
@@ -582,10 +595,31 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(MemArgs a, const i
     }
   }
 
+  // Records of the lane's states for step t: costs, shift bytes (four per
+  // word) and the least shift, from the parity buffer t & 1.
+  constexpr int RB = ALIAS ? 8 : SPL;  // states whose records are held at once
+  uint32_t cr[RB], dr[RB / 4];
+  int dm = 0;
+  auto read_records = [&](int par, int v0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int v = 0; v < RB / 4; ++v) {
+      const u32x4 c4 = *(const u32x4 *)&rcost[par][s0 + v0 + 4 * v];
+      cr[4 * v] = c4.x;
+      cr[4 * v + 1] = c4.y;
+      cr[4 * v + 2] = c4.z;
+      cr[4 * v + 3] = c4.w;
+      dr[v] = *(const uint32_t *)&rshift[par][s0 + v0 + 4 * v];
+    }
+  };
+
   for (int i = 1; i < N; ++i) {
     const int par = i & 1, pprev = par ^ 1;
     const int pb = ALIAS ? 0 : par;
     const int e_next = e_nn;
+    if constexpr (!ALIAS) {  // this step's records: the buffer is restaged after the step's barrier
+      read_records(par, 0);
+      dm = rdmin[par];
+    }
     if constexpr (!RLDS) e_nn = i + 2 < N ? redge[i + 2] : e_next;
     if constexpr (RLDS) {
 #pragma unroll
@@ -595,7 +629,7 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(MemArgs a, const i
       }
     }
 
-    // Phase A: products of the wave's buckets for all states.
+    // Phase A: products of the block's buckets for the wave's states.
     uint32_t acc[SPL];
 #pragma unroll
     for (int k = 0; k < SPL; ++k) acc[k] = kSat;
@@ -607,7 +641,7 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(MemArgs a, const i
       } else {
 #pragma unroll
         for (int v = 0; v < 8; ++v) {
-          const u32x4 q = *(const u32x4 *)&Qw[w][m][32 * tb + 4 * v];
+          const u32x4 q = *(const u32x4 *)&Qw[blk][m][32 * tb + 4 * v];
           qb[4 * v] = q.x;
           qb[4 * v + 1] = q.y;
           qb[4 * v + 2] = q.z;
@@ -647,55 +681,50 @@ __global__ __launch_bounds__(kMemThreads) void mem_fwd_kernel(MemArgs a, const i
     e_cur = e_next;
 #pragma unroll
     for (int k = 0; k < SPL; ++k) Pb[pb][s0 + k][col] = acc[k];
-    __syncthreads();
+    __syncthreads();  // B
 
     // Phase B: the shifted products, their offset gaps, the bucket minimum and
     // the new rows.  The gap o[m - d] - o[m - dmin] of an available state is
     // >= 0, and infinite (saturated) when column m - d is infeasible; an
     // unavailable state has cost kSat, so its gap does not matter.
     const int64_t *O = offs[pprev];
-    const int dm = rdmin[par];
+    if constexpr (ALIAS) dm = rdmin[par];
     const int64_t base = O[col - dm];
 #pragma unroll
     for (int v0 = 0; v0 < SPL; v0 += 8) {  // eight states at a time (registers)
-      uint32_t pvs[8], cr[8];
-      int64_t ods[8];
+      if constexpr (ALIAS) read_records(par, v0);
+      constexpr int V = ALIAS ? 0 : 1;  // ALIAS: the records of states v0 .. v0+7 are in cr[0..7]
+      constexpr int NK = SPL < 8 ? SPL : 8;
+      uint32_t pvs[NK];
+      int64_t ods[NK];
 #pragma unroll
-      for (int v = 0; v < 2; ++v) {
-        const u32x4 c4 = *(const u32x4 *)&rcost[par][s0 + v0 + 4 * v];
-        const uint32_t d4 = *(const uint32_t *)&rshift[par][s0 + v0 + 4 * v];
-        cr[4 * v] = c4.x;
-        cr[4 * v + 1] = c4.y;
-        cr[4 * v + 2] = c4.z;
-        cr[4 * v + 3] = c4.w;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int d = (int)((d4 >> (8 * u)) & 0xFF);
-          pvs[4 * v + u] = Pb[pb][s0 + v0 + 4 * v + u][col - d];
-          ods[4 * v + u] = O[col - d];
-        }
+      for (int k = 0; k < NK; ++k) {
+        const int kr = V * v0 + k;
+        const int d = (int)((dr[kr >> 2] >> (8 * (kr & 3))) & 0xFF);
+        pvs[k] = Pb[pb][s0 + v0 + k][col - d];
+        ods[k] = O[col - d];
       }
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
+      for (int k = 0; k < NK; ++k) {
         const uint64_t gap = (uint64_t)(ods[k] - base);
-        const uint32_t dk = (ods[k] >= kOffInf || (gap >> 32) != 0) ? kSat : (uint32_t)gap;
-        argb[par][w][s0 + v0 + k][m] = (uint8_t)(pvs[k] & S::MASK);
-        y[v0 + k] = sat_add(sat_add(pvs[k] >> BITS, cr[k]), dk);
+        const uint32_t dk = gap > (uint64_t)kSat ? kSat : (uint32_t)gap;  // an infinite offset gives a huge gap
+        argb[par][blk][s0 + v0 + k][m] = (uint8_t)(pvs[k] & S::MASK);
+        y[v0 + k] = sat_add(sat_add(pvs[k] >> BITS, cr[V * v0 + k]), dk);
       }
     }
     const int64_t onew = normalise(base);
-    if constexpr (ALIAS) __syncthreads();  // every product read before the rows overwrite them
+    if constexpr (ALIAS) __syncthreads();  // B2: every product read before the rows overwrite them
     store_rows(y);
     if (g == 0) offs[par][col] = onew;
   }
-  __syncthreads();  // the last step's rows and offsets (matches the I/O wave's)
+  __syncthreads();  // the last step's rows and offsets (matches the I/O waves')
 
   const int fin = (N - 1) & 1;  // offsets of the last step
   // Budget frontier: the offset of bucket m is min_s D[N-1][s][m], the least
   // cost with memory total at most m.
   if (a.frontier && g == 0 && bucket < M)
     a.frontier[(size_t)b * M + bucket] = (bucket <= top && offs[fin][col] < kOffInf) ? offs[fin][col] : INT64_MAX;
-  __syncthreads();  // the I/O wave's timeout flag
+  __syncthreads();  // the I/O waves' timeout flag
 
   // The chunk holding the budget bucket reports the search.
   if (Bb >= m0 && Bb < m0 + C && w == 0) {
@@ -891,7 +920,8 @@ static int mem_xcd_capacity() {
     int dev = 0, cus = 0, per_cu = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, mem_fwd_kernel<KP>, kMemThreads, 0) != hipSuccess)
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, mem_fwd_kernel<KP>, MemShape<KP>::THREADS, 0) !=
+            hipSuccess)
       return;
     cap = (cus / 8) * per_cu;
   });
@@ -939,7 +969,7 @@ static hipError_t launch_mem(const cfp_chain_desc &d, const uint8_t *mem, int n_
     a.b0 = b0;
     a.nb = std::min(round, B - b0);
     a.B8 = (a.nb + 7) / 8 * 8;
-    timed_launch(mem_fwd_kernel<KP>, dim3(w.nchunk * a.B8), dim3(kMemThreads), 0, st, a, redge_dev,
+    timed_launch(mem_fwd_kernel<KP>, dim3(w.nchunk * a.B8), dim3(MemShape<KP>::THREADS), 0, st, a, redge_dev,
                  (const int32_t *)w.dmin);
   }
   timer_end(st);
