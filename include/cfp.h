@@ -218,6 +218,26 @@ int cfp_dp_segments(const cfp_segment_desc *d, void *ws, size_t ws_bytes, int64_
  * descriptor (lowest optimal final plan, lowest predecessor at every step). */
 int cfp_traceback_segments(const cfp_segment_desc *d, void *ws, size_t ws_bytes, int32_t *plan, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * search as cfp_dp_chain followed by cfp_traceback, with the workspace taken
+ * from a static device array of CFP_NOALLOC_MAX_BYTES bytes that the library
+ * holds on every GPU it runs on until the process ends.  The call allocates
+ * nothing: the header and the edge map reach the device as kernel arguments
+ * and the upload ring of the other calls is not used.
+ *   d       as for cfp_dp_chain (redge on the host)
+ *   opt     device [B] int64, status device [B] int32, plan device [B][N] int32:
+ *           as cfp_dp_chain and cfp_traceback write them.
+ * Returns CFP_ERR_WORKSPACE when the search needs more than
+ * CFP_NOALLOC_MAX_BYTES of workspace (cfp_workspace_bytes(d, CFP_V_CHAIN, 0)),
+ * CFP_ERR_HIP if the array's device address cannot be obtained, otherwise as
+ * cfp_dp_chain.  Every call on one GPU uses that GPU's one array: calls that
+ * overlap on a GPU (different streams or threads with work in flight at the
+ * same time) race and must be serialised by the caller; calls in one stream
+ * are ordered and safe. */
+#define CFP_NOALLOC_MAX_BYTES (32u << 20)
+int cfp_search_chain_noalloc(const cfp_chain_desc *d, int64_t *opt, int32_t *status, int32_t *plan, void *stream);
+
 /* Benchmarking aid (not needed for searching).  cfp_timer_start creates
  * max_launches pairs of HIP events (1 <= max_launches <= 2^20) and arms
  * recording: from then on every launch of a forward call's main kernel (the

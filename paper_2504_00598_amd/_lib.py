@@ -36,7 +36,8 @@ CFP_MAX_K = 512
 
 EXPORTED = ("cfp_r_limit", "cfp_workspace_bytes", "cfp_dp_chain", "cfp_dp_chain_mem", "cfp_mem_frontier",
             "cfp_minplus_scan", "cfp_traceback", "cfp_segment_workspace_bytes", "cfp_dp_segments",
-            "cfp_traceback_segments", "cfp_status_string", "cfp_timer_start", "cfp_timer_stop")
+            "cfp_traceback_segments", "cfp_status_string", "cfp_timer_start", "cfp_timer_stop",
+            "cfp_search_chain_noalloc")
 
 
 class CfpError(RuntimeError):
@@ -106,6 +107,8 @@ def lib() -> ctypes.CDLL:
         L.cfp_dp_segments.restype = ctypes.c_int
         L.cfp_traceback_segments.argtypes = [SD, P, ctypes.c_size_t, P, P]
         L.cfp_traceback_segments.restype = ctypes.c_int
+        L.cfp_search_chain_noalloc.argtypes = [D, P, P, P, P]
+        L.cfp_search_chain_noalloc.restype = ctypes.c_int
         L.cfp_timer_start.argtypes = [I32]
         L.cfp_timer_start.restype = ctypes.c_int
         L.cfp_timer_stop.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I32)]
@@ -242,6 +245,23 @@ def cfp_traceback_segments(desc: SegDesc, ws, plan=None, stream=None):
     _check("cfp_traceback_segments", lib().cfp_traceback_segments(desc.ref, _ptr(ws), ws.numel(), _ptr(plan),
                                                                   _stream(stream)))
     return plan
+
+
+CFP_NOALLOC_MAX_BYTES = 32 << 20
+
+
+def cfp_search_chain_noalloc(desc: Desc, opt=None, status=None, plan=None, stream=None):
+    """Enqueue the chain search and its traceback with the workspace in the
+    library's static device scratch.  Returns (opt, status, plan)."""
+    import torch
+
+    dev = desc.cost.device
+    opt = torch.empty(desc.B, dtype=torch.int64, device=dev) if opt is None else opt
+    status = torch.empty(desc.B, dtype=torch.int32, device=dev) if status is None else status
+    plan = torch.empty((desc.B, desc.N), dtype=torch.int32, device=dev) if plan is None else plan
+    _check("cfp_search_chain_noalloc", lib().cfp_search_chain_noalloc(desc.ref, _ptr(opt), _ptr(status), _ptr(plan),
+                                                                      _stream(stream)))
+    return opt, status, plan
 
 
 def cfp_workspace_bytes(desc: Desc, variant: int, n_mem: int = 0) -> int:

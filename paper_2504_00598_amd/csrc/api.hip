@@ -192,6 +192,96 @@ int upload_header(const cfp_chain_desc *d, int variant, int n_mem, const WsLayou
   });
 }
 
+// Workspace of cfp_search_chain_noalloc: a static device array, one per GPU,
+// held until the process ends.  Host code never uses its name as an address:
+// the device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) uint8_t scratch[CFP_NOALLOC_MAX_BYTES];
+
+constexpr int kNoAllocDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kNoAllocDevices] = {};
+
+// Device address of `scratch` on the current device (nullptr on failure).
+void *scratch_address() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kNoAllocDevices) return nullptr;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
+// Words carried by one launch of put_words_kernel as its argument, so that
+// host data reaches the device without a staging buffer.
+constexpr int kPutWords = 960;
+struct PutChunk {
+  int32_t n, off;
+  int32_t v[kPutWords];
+};
+static_assert(sizeof(PutChunk) + 16 < 4096, "one kernel argument block");
+
+__global__ void put_words_kernel(int32_t *__restrict__ dst, PutChunk c) {
+  for (int x = threadIdx.x; x < c.n; x += blockDim.x) dst[c.off + x] = c.v[x];
+}
+
+// Header and edge map of a chain call (the words [0, L.redge/4 + N) of the
+// workspace) written by kernels whose arguments carry them.
+int put_header(const cfp_chain_desc *d, const WsLayout &L, uint8_t *w, hipStream_t st) {
+  WsHeader h;
+  memset(&h, 0, sizeof h);
+  h.magic = kMagic;
+  h.variant = CFP_V_CHAIN;
+  h.n = d->n_blocks;
+  h.k = d->k;
+  h.batch = d->batch;
+  h.n_mem = 0;
+  h.elem = L.elem;
+  const int hw = (int)(L.redge / 4), total = hw + d->n_blocks;
+  PutChunk c;
+  for (int off = 0; off < total; off += kPutWords) {
+    c.n = total - off < kPutWords ? total - off : kPutWords;
+    c.off = off;
+    for (int x = 0; x < c.n; ++x) {
+      const int word = off + x;
+      if (word < (int)(sizeof h / 4)) c.v[x] = ((const int32_t *)&h)[word];
+      else if (word < hw) c.v[x] = 0;
+      else c.v[x] = word == hw ? 0 : d->redge[word - hw];  // redge[0] is ignored; keep it a valid table index
+    }
+    hipLaunchKernelGGL(put_words_kernel, dim3(1), dim3(256), 0, st, (int32_t *)w, c);
+    if (hipGetLastError() != hipSuccess) return CFP_ERR_HIP;
+  }
+  return CFP_OK;
+}
+
+// The launches of a chain forward call once the header and the edge map are
+// in the workspace (or not needed: the periodic chunk-parallel K <= 64 path).
+int dp_chain_launch(const cfp_chain_desc *d, const WsLayout &L, uint8_t *w, int64_t *opt, int32_t *status,
+                    hipStream_t st) {
+  WsHeader *hdr = (WsHeader *)w;
+  const bool wave = chain_wave_supported(d->n_blocks, d->k, d->n_tables, d->batch);
+  const bool cw = !wave && chain_cw_supported(d->n_blocks, d->k, d->batch);
+  if (!wave && !cw &&
+      launch_validate_rtab(d->rtab, d->n_tables, d->k, cfp_r_limit(CFP_V_CHAIN, d->k), hdr, st) != hipSuccess)
+    return CFP_ERR_HIP;
+  hipError_t e;
+  if (wave)
+    e = launch_chain_wave(*d, (const int32_t *)(w + L.redge), w + L.wave, w + L.table,
+                          (SearchResult *)(w + L.result), hdr, opt, status, st);
+  else if (cw)
+    e = launch_chain_cw(*d, (const int32_t *)(w + L.redge), w + L.cw, w + L.table, (SearchResult *)(w + L.result),
+                        hdr, opt, status, st);
+  else if (chain_fwd_split_supported(d->k, d->n_tables, d->batch))
+    e = launch_chain_fwd_split(*d, (const int32_t *)(w + L.redge), w + L.split, (uint32_t *)(w + L.wide),
+                               w + L.table, (SearchResult *)(w + L.result), hdr, opt, status, st);
+  else
+    e = launch_chain_fwd(*d, (const int32_t *)(w + L.redge), w + L.table, L.elem, w + L.wide,
+                         (SearchResult *)(w + L.result), hdr, opt, status, st);
+  return e == hipSuccess ? CFP_OK : CFP_ERR_HIP;
+}
+
 }  // namespace
 
 #pragma GCC visibility push(default)
@@ -231,34 +321,13 @@ int cfp_dp_chain(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t *op
   WsLayout L = layout(CFP_V_CHAIN, d->n_blocks, d->k, d->batch, 0, d->n_tables);
   if (!ws || ws_bytes < L.total) return CFP_ERR_WORKSPACE;
   hipStream_t st = (hipStream_t)stream;
-  uint8_t *w = (uint8_t *)ws;
-  WsHeader *hdr = (WsHeader *)w;
   // The chunk-parallel paths check the range of R while packing it; the K <= 64
   // one with a periodic edge map reads nothing of the header, which is then not
   // uploaded (a host-to-device copy costs several microseconds of GPU time).
   const bool wave = chain_wave_supported(d->n_blocks, d->k, d->n_tables, d->batch);
   if (!(wave && chain_wave_headerless(*d)) && (rc = upload_header(d, CFP_V_CHAIN, 0, L, ws, st)) != CFP_OK)
     return rc;
-  const bool cw = !wave && chain_cw_supported(d->n_blocks, d->k, d->batch);
-  if (!wave && !cw &&
-      launch_validate_rtab(d->rtab, d->n_tables, d->k, cfp_r_limit(CFP_V_CHAIN, d->k), hdr, st) != hipSuccess)
-    return CFP_ERR_HIP;
-  hipError_t e;
-  if (wave)
-    e = launch_chain_wave(*d, (const int32_t *)(w + L.redge), w + L.wave, w + L.table,
-                          (SearchResult *)(w + L.result), hdr, opt, status, st);
-  else if (cw)
-    e = launch_chain_cw(*d, (const int32_t *)(w + L.redge), w + L.cw, w + L.table, (SearchResult *)(w + L.result),
-                        hdr, opt, status, st);
-  else if (chain_fwd_split_supported(d->k, d->n_tables, d->batch))
-    e = launch_chain_fwd_split(*d, (const int32_t *)(w + L.redge), w + L.split, (uint32_t *)(w + L.wide),
-                               w + L.table, (SearchResult *)(w + L.result), hdr, opt, status, st);
-  else
-    e = launch_chain_fwd(*d, (const int32_t *)(w + L.redge), w + L.table, L.elem, w + L.wide,
-                         (SearchResult *)(w + L.result), hdr, opt, status, st);
-  if (e != hipSuccess)
-    return CFP_ERR_HIP;
-  return CFP_OK;
+  return dp_chain_launch(d, L, (uint8_t *)ws, opt, status, st);
 }
 
 int cfp_dp_chain_mem(const cfp_chain_desc *d, const uint8_t *mem, int32_t n_mem, const int32_t *budget,
@@ -342,6 +411,26 @@ int cfp_traceback(const cfp_chain_desc *d, int32_t variant, int32_t n_mem, void 
     e = launch_traceback_chain(d->n_blocks, d->k, d->batch, L.elem, w + L.table,
                                (const SearchResult *)(w + L.result), (uint16_t *)(w + L.maps),
                                (int32_t *)(w + L.bounds), L.nchunks, plan, st);
+  return e == hipSuccess ? CFP_OK : CFP_ERR_HIP;
+}
+
+int cfp_search_chain_noalloc(const cfp_chain_desc *d, int64_t *opt, int32_t *status, int32_t *plan,
+                             void *stream) {
+  int rc = check_desc(d);
+  if (rc != CFP_OK) return rc;
+  if (!opt || !status || !plan) return CFP_ERR_ARG;
+  const WsLayout L = layout(CFP_V_CHAIN, d->n_blocks, d->k, d->batch, 0, d->n_tables);
+  if (L.total > (size_t)CFP_NOALLOC_MAX_BYTES) return CFP_ERR_WORKSPACE;  // beyond the static scratch
+  uint8_t *w = (uint8_t *)scratch_address();
+  if (!w) return CFP_ERR_HIP;
+  hipStream_t st = (hipStream_t)stream;
+  // Every region the kernels read is written earlier in the same call; the
+  // header (range flags included) is rewritten whole.
+  if ((rc = put_header(d, L, w, st)) != CFP_OK) return rc;
+  if ((rc = dp_chain_launch(d, L, w, opt, status, st)) != CFP_OK) return rc;
+  const hipError_t e = launch_traceback_chain(d->n_blocks, d->k, d->batch, L.elem, w + L.table,
+                                              (const SearchResult *)(w + L.result), (uint16_t *)(w + L.maps),
+                                              (int32_t *)(w + L.bounds), L.nchunks, plan, st);
   return e == hipSuccess ? CFP_OK : CFP_ERR_HIP;
 }
 
