@@ -43,9 +43,17 @@
  *    documented range, CFP_ST_INFEASIBLE when no plan exists (a block with
  *    every strategy unavailable, or no plan within the memory budget).  When
  *    status[b] != CFP_ST_OK, opt[b] = INT64_MAX and the traced plan is all -1.
- *  - No global mutable state (apart from the opt-in benchmarking timer at
- *    the end of this file): calls on different streams with different
- *    workspaces may run concurrently.
+ *  - No global mutable state apart from the opt-in benchmarking timer and
+ *    the static workspace of cfp_search_chain_noalloc (both declared
+ *    below): calls on different streams with different workspaces may
+ *    run concurrently.  Two paths wait on the device for other workgroups of
+ *    the same launch and need them resident at the same time: the memory
+ *    variant (cfp_dp_chain_mem, cfp_mem_frontier) and the split chain kernel
+ *    that cfp_dp_chain uses for K > 64 when the chunk-parallel kernels do not
+ *    apply.  Their waits are bounded; if another long kernel keeps their
+ *    workgroups from being dispatched (a shared GPU, concurrent calls), a
+ *    wait may expire and the search ends with CFP_ST_TIMEOUT, never with a
+ *    wrong answer.
  */
 #ifndef CFP_H
 #define CFP_H
@@ -76,7 +84,8 @@ enum {
   CFP_ST_OK = 0,
   CFP_ST_INFEASIBLE = 1, /* no plan (all strategies unavailable at a block, or budget too small) */
   CFP_ST_OVERFLOW = 2,   /* reserved: device arithmetic left its exact range (not reachable with valid inputs) */
-  CFP_ST_TIMEOUT = 3,    /* a bounded device wait of the memory variant's pipeline expired */
+  CFP_ST_TIMEOUT = 3,    /* a bounded device wait expired (memory variant, or the K > 64 split chain
+                            kernel, while other work held the GPU; see above) */
   CFP_ST_BADINPUT = 4    /* a device array value is outside its documented range */
 };
 
@@ -100,10 +109,10 @@ typedef struct {
 /* Exclusive upper bound on resharding-table entries for which `variant` with
  * K strategies is exact.  The kernels carry (cost, argmin) packed in one
  * 32-bit word with ceil(log2 K) index bits (at least 4), so the bound depends
- * on K: 2^(30-b) for K <= 64, 2^(32-b) - 1 for K > 64 (chain and scan),
- * 2^(31-b) for the memory variant and 2^(32-b) - 1 for the boundary tables of
- * the segment search, with b = max(4, ceil(log2 K)).  Returns 0
- * for an unsupported K or variant. */
+ * on K: 2^(30-b) for K <= 64, 2^(32-b) - 1 for K > 64 (chain and scan) and
+ * 2^(32-b) - 1 for the boundary tables of the segment search, with
+ * b = max(4, ceil(log2 K)); 2^(31-b) with b = max(5, ceil(log2 K)) for the
+ * memory variant (K <= 256).  Returns 0 for an unsupported K or variant. */
 int32_t cfp_r_limit(int32_t variant, int32_t k);
 
 /* Bytes of device workspace a forward call of `variant` needs (n_mem is the
@@ -131,10 +140,13 @@ int cfp_dp_chain(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t *op
  *          entry gives status CFP_ST_BADINPUT)
  *   n_mem  M, the number of memory buckets, 1 <= M <= 4096
  *   budget device [B] int32, each in [0, M)
- * Supported for K <= 32 and n_tables <= 12 (CFP_ERR_UNSUPPORTED otherwise).
- * The buckets of a search are cut into chunks of 64 that run as a pipeline of
- * workgroups; a chunk that waits too long for the chunk below it (which
- * cannot happen when the GPU is not shared) ends its search with
+ * Supported for 1 <= K <= 256 and any n_tables >= 1 (CFP_ERR_UNSUPPORTED for
+ * K > 256).  Every cost and resharding entry in its documented range gives
+ * the exact optimum (CFP_ST_OVERFLOW is not reachable).  The buckets of a
+ * search are cut into chunks of 64 that run as a pipeline of workgroups;
+ * searches are launched in rounds small enough that every chunk of a round
+ * is resident at once.  A chunk that waits too long for the chunk below it
+ * (which cannot happen when the GPU is not shared) ends its search with
  * CFP_ST_TIMEOUT.  ws must hold cfp_workspace_bytes(d, CFP_V_MEM, n_mem)
  * bytes. */
 int cfp_dp_chain_mem(const cfp_chain_desc *d, const uint8_t *mem, int32_t n_mem, const int32_t *budget,
@@ -149,7 +161,7 @@ int cfp_dp_chain_mem(const cfp_chain_desc *d, const uint8_t *mem, int32_t n_mem,
  * with m; its last entry equals cfp_dp_chain_mem at budget M-1, and
  * cfp_traceback(d, CFP_V_MEM, n_mem, ...) on the same workspace returns the
  * plans at budget M-1.
- *   mem, n_mem  as for cfp_dp_chain_mem (K <= 32, n_tables <= 12)
+ *   mem, n_mem  as for cfp_dp_chain_mem (K <= 256, any n_tables)
  *   frontier    device [B][n_mem] int64
  *   status      device [B] int32: CFP_ST_OK, CFP_ST_INFEASIBLE when no plan
  *               fits even M-1 buckets (frontier all INT64_MAX), or an error
