@@ -62,15 +62,15 @@ COMMON_SOURCES = ["common.h", "cfp_internal.h", "../../include/cfp.h"]
 # changed and the figure is withheld.
 FETCH_SCALE, WRITE_SCALE = 524288.0 / 262167.1, 524288.0 / 524288.0
 TRAFFIC = {
-    "chain_gpt_n24_k16": {"fetch_kib": 18.0, "write_kib": 0.5, "sources": "4a59102f0d13e6c1"},
-    "chain_gpt_n1152_k64": {"fetch_kib": 37970.3, "write_kib": 37516.3, "sources": "b412a2fa80c1eeaf"},
-    "mem_llama_n288_k32": {"fetch_kib": 58884.1, "write_kib": 288456.7, "sources": "aa519dbe5968c06a"},
-    "chain_wide_n512_k256": {"fetch_kib": 44455.0, "write_kib": 16423.4, "sources": "b0f627d51c4baf4c"},
+    "chain_gpt_n24_k16": {"fetch_kib": 18.0, "write_kib": 0.5, "sources": "44bed4f0eb55d922"},
+    "chain_gpt_n1152_k64": {"fetch_kib": 37972.6, "write_kib": 37516.1, "sources": "cec3c986f0b278db"},
+    "mem_llama_n288_k32": {"fetch_kib": 127642.5, "write_kib": 338789.9, "sources": "8819739b408e81c0"},
+    "chain_wide_n512_k256": {"fetch_kib": 44580.6, "write_kib": 16424.0, "sources": "089a067565012ace"},
     # mean over the 12 matrix-product launches of one forward call
-    "scan_n4096_k512": {"fetch_kib": 3035253.1, "write_kib": 1398442.5, "sources": "bba6a229e4af8d7e"},
-    "seg_gpt_n96_k81": {"fetch_kib": 3922.7, "write_kib": 1936.0, "sources": "66d4b832202782ab"},
+    "scan_n4096_k512": {"fetch_kib": 3035064.5, "write_kib": 1398442.5, "sources": "f9f8fcff938ec825"},
+    "seg_gpt_n96_k81": {"fetch_kib": 3922.9, "write_kib": 1936.0, "sources": "3cb0a9594fc4041e"},
     # the memory workload run as a budget frontier (every chunk of every search active)
-    "mem_llama_n288_k32:frontier": {"fetch_kib": 76704.2, "write_kib": 372085.2, "sources": "aa519dbe5968c06a"},
+    "mem_llama_n288_k32:frontier": {"fetch_kib": 166635.1, "write_kib": 442222.7, "sources": "8819739b408e81c0"},
 }
 
 
