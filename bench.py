@@ -10,10 +10,10 @@ By default every workload is timed in turn and the line carries one record
 per workload under "configs"; the headline figures are those of the largest,
 scan_n4096_k512 (4096 blocks, 512 strategies, 4 searches, the min-plus
 parallel-scan form).  The records also hold the budget frontier of the memory
-workload and the scan workload run through the sequential chain search.
+workload and the scan workload run through the chain search.
 With --config only that workload is timed: chain_gpt_n24_k16,
 chain_gpt_n1152_k64, mem_llama_n288_k32 (with --frontier: every budget in one
-pass), chain_wide_n512_k256, scan_n4096_k512 (with --sequential: the chain
+pass), chain_wide_n512_k256, scan_n4096_k512 (with --chain: the chain
 search), seg_gpt_n96_k81 (segment-level search with boundary resharding).
 """
 from __future__ import annotations
@@ -36,7 +36,6 @@ METRIC = "min-plus cell updates/sec (K² per block per search) + search latency"
 VALU_LANE_OPS = 256 * 64 * 2.4e9
 INSTR_PER_CELL = 1.5
 PEAK_CELLS = VALU_LANE_OPS / INSTR_PER_CELL
-SEQUENTIAL_KERNEL = "chain_fwd_split_kernel<512>"
 
 
 # The kernel that dominates the forward pass of each workload, and the source
@@ -47,7 +46,9 @@ KERNELS = {
     "chain_gpt_n1152_k64": ("chain_wave_kernel<12>", ["chain_wave.hip", "res_common.h"]),
     "mem_llama_n288_k32": ("mem_fwd_kernel<32>", ["mem_fwd.hip", "res_common.h"]),
     # speculative pass of the chunk-parallel search
-    "chain_wide_n512_k256": ("chain_cw_kernel<0>", ["chain_cw.hip", "chain_fwd_wide.hip"]),
+    "chain_wide_n512_k256": ("chain_cw_kernel<256,0>", ["chain_cw.hip", "chain_fwd_wide.hip"]),
+    # the scan workload through the chain search: speculative pass of the chunk-parallel form
+    "scan_n4096_k512:chain": ("chain_cw_kernel<512,0>", ["chain_cw.hip", "chain_fwd_wide.hip"]),
     "scan_n4096_k512": ("scan_gemm_kernel", ["scan.hip"]),
     "seg_gpt_n96_k81": ("seg_fwd_kernel<2>", ["seg_fwd.hip"]),
 }
@@ -91,8 +92,9 @@ def sources_hash(config: str) -> str:
 
 
 def traffic_bytes(config: str, mode: str = ""):
-    t = TRAFFIC.get(config + (":" + mode if mode else ""))
-    if t is None or t["sources"] != sources_hash(config):
+    key = config + (":" + mode if mode else "")
+    t = TRAFFIC.get(key)
+    if t is None or t["sources"] != sources_hash(key if key in KERNELS else config):
         return None
     return (t["fetch_kib"] * FETCH_SCALE + t["write_kib"] * WRITE_SCALE) * 1024.0
 
@@ -299,7 +301,7 @@ def host_info() -> dict:
 
 
 def measure(name: str, steps: int, warmup: int, cpu_s: float, frontier: bool = False,
-            sequential: bool = False) -> dict:
+            chain: bool = False) -> dict:
     """Time `steps` whole passes (forward + traceback) of one workload and
     return its record: step time, cells/s in the metric's unit, the dominant
     kernel's and the forward call's roofline fractions, parity against the
@@ -313,9 +315,9 @@ def measure(name: str, steps: int, warmup: int, cpu_s: float, frontier: bool = F
 
     cfg = configs.BY_NAME[name]
     data = configs.make(cfg)
-    if sequential:
+    if chain:
         if cfg.form != "scan":
-            raise SystemExit("--sequential applies to the scan workload")
+            raise SystemExit("--chain applies to the scan workload")
         cfg = dataclasses.replace(cfg, form="chain")
     if frontier:
         if cfg.form != "mem":
@@ -377,17 +379,15 @@ def measure(name: str, steps: int, warmup: int, cpu_s: float, frontier: bool = F
             O.mem_frontier(data["cost"], data["rtab"], data["redge"], data["mem"], cfg.M, nthreads=oracle_threads())))
 
     wl = {"workload": cfg.name, "blocks": cfg.N, "strategies": cfg.K, "searches": cfg.B, "resharding_tables": 12}
-    if sequential:
-        wl["form"] = "sequential chain search (cfp_dp_chain), not the scan"
+    if chain:
+        wl["form"] = "chain search (cfp_dp_chain, chunk-parallel), not the scan"
     if cfg.form == "seg":
         wl = {"workload": cfg.name, "segments": cfg.N, "plans": cfg.K, "searches": cfg.B,
               "boundary_tables": "2 x 3 x 3", "blocks_per_segment": 4, "strategies_per_block": 3}
     if cfg.form == "mem":
         wl.update({"memory_buckets": cfg.M, "budgets": "every budget 0..M-1" if frontier else "1023-32b"})
-    kernel = KERNELS[cfg.name][0]
-    if sequential:
-        kernel = SEQUENTIAL_KERNEL
-    mode = "frontier" if frontier else ""
+    mode = "frontier" if frontier else "chain" if chain else ""
+    kernel = KERNELS[cfg.name + ":chain" if chain else cfg.name][0]
     rec = {
         "config": wl,
         "steps": steps,
@@ -400,7 +400,7 @@ def measure(name: str, steps: int, warmup: int, cpu_s: float, frontier: bool = F
         "parity_vs_oracle": parity,
         "roofline": {"bound": "alu", "achieved": kern_cells_s / 1e12, "peak": PEAK_CELLS / 1e12, "unit": "Tcell/s",
                      "frac": kern_cells_s / PEAK_CELLS,
-                     "traffic": None if sequential else traffic_bytes(cfg.name, mode),
+                     "traffic": traffic_bytes(cfg.name, mode),
                      "kernel": kernel,
                      "kernel_launches_per_step": kern_launches / steps,
                      "kernel_avg_us": kern_avg_ms * 1e3,
@@ -427,7 +427,7 @@ def measure(name: str, steps: int, warmup: int, cpu_s: float, frontier: bool = F
 # Records of the default run, in order; the headline is the largest workload.
 ALL_RUNS = [("chain_gpt_n24_k16", {}), ("chain_gpt_n1152_k64", {}), ("mem_llama_n288_k32", {}),
             ("mem_llama_n288_k32", {"frontier": True}), ("chain_wide_n512_k256", {}),
-            ("scan_n4096_k512", {}), ("scan_n4096_k512", {"sequential": True}), ("seg_gpt_n96_k81", {})]
+            ("scan_n4096_k512", {}), ("scan_n4096_k512", {"chain": True}), ("seg_gpt_n96_k81", {})]
 HEADLINE = "scan_n4096_k512"
 
 
@@ -441,8 +441,8 @@ def main() -> int:
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=None,
                     help="seconds of oracle work per CPU baseline (default 12 for the headline, 4 for the others)")
-    ap.add_argument("--sequential", action="store_true",
-                    help="scan workload only: run the sequential chain search instead of the min-plus scan")
+    ap.add_argument("--chain", action="store_true",
+                    help="scan workload only: run the chain search (cfp_dp_chain) instead of the min-plus scan")
     ap.add_argument("--frontier", action="store_true",
                     help="memory workload only: time the budget frontier (every budget 0..M-1 in one pass)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -460,7 +460,7 @@ def main() -> int:
     if args.config is not None:
         cpu_s = 0.0 if args.no_cpu else (args.cpu_seconds or 10.0)
         rec = measure(args.config, args.steps, args.warmup, cpu_s, frontier=args.frontier,
-                      sequential=args.sequential)
+                      chain=args.chain)
         if "cpu_baseline" in rec:
             rec["cpu_baseline"]["host"] = host_info()
         out = dict(base, **rec)

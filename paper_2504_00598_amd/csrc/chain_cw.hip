@@ -1,4 +1,4 @@
-// Chunk-parallel forward pass of the chain search for 128 < K <= 256 (Sec. 4.4,
+// Chunk-parallel forward pass of the chain search for 128 < K <= 512 (Sec. 4.4,
 // Eq. T recurrence), for batches whose chains are long.
 //
 // Parallelism over the chain: as in the K <= 64 form, every chain is cut into
@@ -11,35 +11,41 @@
 //   2. fix-up pass, chunks p >= 1: start again from the last checkpoint row of
 //      chunk p-1 and recompute until the row equals chunk p's checkpoint of the
 //      same quad (from there on the speculative rows are the true ones);
-//   3. final pass: sum the chunk offsets; a chunk whose fix-up met no
-//      checkpoint has its true end row, and the rest of the chain is rerun from
-//      it.  The result is the sequential recurrence's bit for bit.
+//   3. final pass: sum the chunk offsets.  The fix-up of a chunk is valid when
+//      the chunk before it ends on a true row; a chunk whose fix-up met no
+//      checkpoint has its true end row, from which the next chunk is rerun
+//      whole; the chunks after a rerun chunk whose rows met its checkpoints
+//      are valid again.  The result is the sequential recurrence's bit for bit.
 //
-// One workgroup of 512 threads carries four chains (four searches of the same
-// chunk: every chain of a launch is at the same row, so all use the same
-// table) and all KP = 256 states.  Thread tid = 64 g + q (wave g) works for the
-// states 4q .. 4q+3 of every chain over the predecessors t = 32 g .. 32 g + 31,
-// so every table load of a wave reads 1 KiB of one row contiguously.  Per
-// step it reads its 32 x 4 packed words (R_e[t][s] << 8) | t of the edge's
-// table from the cache-resident array (each word serves the four chains), in
-// four pieces of eight rows, each loaded one step ahead into its own registers,
-// and the predecessors' values from the previous rows in LDS (broadcast
-// reads).  A candidate is a saturating add, and one unsigned minimum keeps the
-// value and the lowest predecessor.  The eight group minima of a state are
-// combined through LDS, after which thread tid holds state tid % 256 of chains
-// tid / 256 and 2 + tid / 256.
+// One workgroup of 512 threads (8 waves) carries four chains (four searches of
+// the same chunk: every chain of a launch is at the same row, so all use the
+// same table) and all KP states, KP = 256 or 512.  Wave g works for the
+// predecessors t = g KP/8 .. (g+1) KP/8 - 1 and lane q for the states
+// q KP/64 .. (q+1) KP/64 - 1 of every chain, so every table load of a wave
+// reads one row's KP words contiguously.  Per step a thread reads its share of
+// the packed words (R_e[t][s] << b) | t of the edge's table (each word serves
+// the four chains) in pieces of a few rows, four pieces in flight in their
+// own registers (at KP = 256 that is the whole step, loaded a step ahead), and
+// the predecessors' values from the previous rows in LDS (broadcast reads).
+// A candidate is a saturating add, and one unsigned minimum keeps the value
+// and the lowest predecessor.  The eight group minima of a state are combined
+// through LDS, after which a thread holds one state of two chains (KP = 256)
+// or of all four (KP = 512).
 //
-// The table stream is what bounds a step: 256 KiB per workgroup and step,
-// which one CU takes in from L2 at about 14 bytes per clock (measured: the
-// step time does not change with the number of workgroups), hence four chains
-// per workgroup rather than two.
+// The table stream is what bounds a step: KP^2 words per workgroup and step
+// from the cache hierarchy (the step time does not change with the number of
+// workgroups), hence four chains per workgroup.  Chunks are at least 16 rows
+// long at KP = 256 and 64 at KP = 512, where runs take longer to become
+// parallel (tens of rows on random costs).
 //
-// Normalisation: x[s] = (m >> 8) + c[i][s]; the row is divided into the part
-// d = min_s x[s] (summed exactly, per chain) and Q[s] = min(x[s] - d, cap) << 8,
-// cap = 2^24 - 1.  The best candidate of every state is at most R_max << 8 | t
-// through the row's minimum, so with R below cfp_r_limit a capped state never
-// wins; unavailable strategies and padding states take x = 2^32 - 1 (capped).
+// Normalisation: x[s] = (m >> b) + c[i][s]; the row is divided into the part
+// d = min_s x[s] (summed exactly, per chain) and Q[s] = min(x[s] - d, cap) << b,
+// cap = 2^(32-b) - 1.  The best candidate of every state is at most
+// R_max << b | t through the row's minimum, so with R below cfp_r_limit a
+// capped state never wins; unavailable strategies and padding states take
+// x = 2^32 - 1 (capped).
 #include <algorithm>
+#include <type_traits>
 
 #include "cfp_internal.h"
 #include "common.h"
@@ -50,25 +56,37 @@ namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kCKP = 256;               // states (padded)
-constexpr int kCBits = 8;               // index bits of a packed word
 constexpr int kCThreads = 512;          // threads per workgroup
 constexpr int kCWaves = kCThreads / 64;
-constexpr int kCRows = 8;               // predecessor rows per streamed piece
-constexpr int kCPieces = 4;             // pieces per step (32 predecessors per thread)
-constexpr int kCQS = kCKP + kCKP / 8;   // LDS row stride: 4 words of padding after every 32
-constexpr uint32_t kCCap = (1u << (32 - kCBits)) - 1u;
 constexpr uint32_t kCX = 0xFFFFFFFFu;   // x of an unavailable or padding state
 constexpr int kCMaxChunks = 64;
-constexpr int kCMinRows = 16;           // least rows per chunk
 // Rows a speculative run starts before its chunk.  Starting early makes the
 // run parallel to the true one sooner, so the fix-up pass stops earlier, but
 // at K = 256 the rows saved there equal the rows added here (measured), so 0.
 constexpr int kCWarm = 0;
 
 constexpr int kCG = 4;                  // chains per workgroup (searches of the same chunk)
-constexpr int kCH = kCG / 2;            // chains per thread after the reduce-scatter
+// Run modes: speculative; fix-up (stops once every chain met a checkpoint);
+// repair (a whole chunk from a true row, noting where it meets).
 constexpr int kCSpec = 0, kCFix = 1, kCRepair = 2;
+
+template <int KP>
+struct CwShape {
+  static constexpr int BITS = KP <= 256 ? 8 : 9;   // index bits of a packed word
+  static constexpr int PG = KP / kCWaves;           // predecessors per wave
+  static constexpr int SPL = KP / 64;               // states per lane in the products
+  static constexpr int V4 = SPL / 4;                // 4-word vectors per table row and lane
+  static constexpr int ROWS = KP <= 256 ? 8 : 2;    // table rows per piece
+  static constexpr int PIECES = PG / ROWS;          // pieces per step
+  static constexpr int NB = 4;                      // pieces held in registers
+  static constexpr int TPS = kCThreads / KP;        // threads per state after the reduction
+  static constexpr int CH = kCG / TPS;              // chains per thread after the reduction
+  static constexpr int QS = KP + KP / 8;            // LDS row stride: 4 words of padding after every 32
+  static constexpr int MINROWS = KP <= 256 ? 16 : 64;  // least rows per chunk
+  static constexpr uint32_t CAP = (1u << (32 - BITS)) - 1u;
+  using Arg = typename std::conditional<(KP <= 256), uint8_t, uint16_t>::type;
+  static_assert(PIECES % NB == 0 && ROWS % 2 == 0 && SPL % 4 == 0, "piece layout");
+};
 
 struct CwRec {
   int64_t dfix;   // fix-up pass: offset sum at the meeting checkpoint, or at the chunk end
@@ -81,18 +99,19 @@ struct CwArgs {
   const uint32_t *rpk;  // packed tables [E][KP][KP]
   const int32_t *redge;
   int N, K, B, P, CL, nq;  // CL rows per chunk (a multiple of 4); nq quads of rows
-  uint8_t *table;          // argmin entries [B][N][K]
+  uint8_t *table;          // argmin entries [B][N][K] (1 byte for KP = 256, 2 for 512)
   CwRec *rec;              // [B][P]
   int64_t *dck;            // speculative offset sum at every checkpoint [B][nq]
   uint32_t *ckrow;         // speculative row at every checkpoint [B][nq][KP]
   uint32_t *endrow;        // fix-up end row of chunks that met no checkpoint [B][P][KP]
 };
 
+template <int KP>
 struct CwSmem {
-  uint32_t part[kCG][kCWaves][kCKP];  // partial minima [chain][predecessor group][state]
-  uint32_t q[2][kCG][kCQS];   // rows [buffer][chain][state, padded]
-  uint32_t wm[kCWaves][kCG];  // wave minima of the new row, per chain
-  int32_t wd[kCWaves][kCG];   // fix-up: the wave found a state off the checkpoint, per chain
+  uint32_t part[kCG][kCWaves][KP];         // partial minima [chain][predecessor group][state]
+  uint32_t q[2][kCG][CwShape<KP>::QS];     // rows [buffer][chain][state, padded]
+  uint32_t wm[kCWaves][kCG];               // wave minima of the new row, per chain
+  int32_t wd[kCWaves][kCG];                // fix-up: the wave found a state off the checkpoint, per chain
 };
 
 __device__ __forceinline__ int qpad(int t) { return t + (t >> 5) * 4; }
@@ -118,13 +137,13 @@ __device__ __forceinline__ uint32_t cw_wave_min(uint32_t x) {
 }
 
 // State of the workgroup's chains as seen by one thread.  After the
-// reduction a thread holds, for its state s = tid % 256, the chains 2h + f2,
-// h = 0 .. kCG/2 - 1 (f2 = tid / 256).
-template <int MODE>
+// reduction thread tid holds, for its state s = tid % KP, the chains
+// h TPS + tid / KP, h = 0 .. CH - 1.
+template <int KP>
 struct CwChains {
-  uint32_t x[kCH];      // the thread's values of the current row, normalised and shifted
+  uint32_t x[CwShape<KP>::CH];  // the thread's values of the current row, normalised and shifted
   uint64_t dsum[kCG];   // offset sums since the start row (uniform)
-  int conv[kCG];        // fix-up: quad of the meeting checkpoint, -1 before
+  int conv[kCG];        // fix-up and repair: quad of the meeting checkpoint, -1 before
   uint64_t dconv[kCG];  // fix-up: dsum at that checkpoint
   uint32_t flags[kCG];  // speculative: bit 0 a negative cost, bit 1 a row with no available strategy
 };
@@ -132,32 +151,40 @@ struct CwChains {
 // Runs rows [r0, r1] of the workgroup's chains (searches bs[c], real where
 // valid[c]).  Speculative: the start row is row rs <= r0 from its costs alone
 // (rows before r0 warm the run up and write nothing); argmins from row r0 and
-// checkpoints are written.  Fix-up: the start row (row r0 - 1)
-// is start[c]; stops at the first quad end where every real chain has met its
-// checkpoint.  Repair: like fix-up without checkpoints.
-template <int MODE>
+// checkpoints are written.  Fix-up: the start row (row r0 - 1) is start[c];
+// stops at the first quad end where every real chain has met its checkpoint.
+// Repair: like fix-up, run to r1.
+template <int KP, int MODE>
 __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const bool *valid, int rs, int r0, int r1,
-                                       const uint32_t *const *start, CwSmem &sm, CwChains<MODE> &ch) {
+                                       const uint32_t *const *start, CwSmem<KP> &sm, CwChains<KP> &ch) {
+  using S = CwShape<KP>;
+  using Arg = typename S::Arg;
+  constexpr int CH = S::CH, TPS = S::TPS, BITS = S::BITS;
+  constexpr bool CHECK = MODE != kCSpec;
   const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int qd = lane, g = wid;  // state quad, predecessor group (one wave each)
+  const int qd = lane, g = wid;  // state group, predecessor group (one wave each)
   const int N = a.N, K = a.K;
   // the thread's state and chains after the reduction
-  const bool f2 = tid >= kCKP;
-  const int ms = tid & (kCKP - 1);
+  const int sub = TPS == 1 ? 0 : tid / KP;
+  const int ms = tid & (KP - 1);
   const bool sin = ms < K;
-  int hc[kCH];  // chain of pair h
-  bool hv[kCH];
-  const int32_t *cbase[kCH];
-  uint8_t *tbase[kCH];
-  uint32_t *ckb[kCH];
+  // element h of the thread's chains from an array indexed by chain
+  auto pick = [&](const auto &arr, int h) __attribute__((always_inline)) {
+    return TPS == 1 ? arr[h] : (sub ? arr[TPS * h + 1] : arr[TPS * h]);
+  };
+  int hc[CH];  // chain of pair h
+  bool hv[CH];
+  const int32_t *cbase[CH];
+  Arg *tbase[CH];
+  uint32_t *ckb[CH];
 #pragma unroll
-  for (int h = 0; h < kCH; ++h) {
-    hc[h] = 2 * h + (f2 ? 1 : 0);
-    const int b = f2 ? bs[2 * h + 1] : bs[2 * h];
-    hv[h] = f2 ? valid[2 * h + 1] : valid[2 * h];
+  for (int h = 0; h < CH; ++h) {
+    hc[h] = TPS * h + sub;
+    const int b = pick(bs, h);
+    hv[h] = pick(valid, h);
     cbase[h] = a.cost + (size_t)b * N * K + min(ms, K - 1);
-    tbase[h] = a.table + (size_t)b * N * K + ms;
-    ckb[h] = a.ckrow + (size_t)b * a.nq * kCKP + ms;
+    tbase[h] = (Arg *)a.table + (size_t)b * N * K + ms;
+    ckb[h] = a.ckrow + (size_t)b * a.nq * KP + ms;
   }
   // redge is read-only for the kernel's lifetime: read through the constant
   // address space, so a row's table index is one scalar load.
@@ -166,21 +193,23 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
   auto edge = [&](int row) __attribute__((always_inline)) { return redge_c[row]; };
   const int i0 = MODE == kCSpec ? rs + 1 : r0;
 
-  // Table pieces of the next row, [piece][row in piece]; word offset of the
+  // Table pieces in flight, [buffer][row in piece][vector]; word offset of the
   // thread's first word within a table.
-  const uint32_t toff = (uint32_t)(32 * g * kCKP + 4 * qd);
-  u32x4 tb[kCPieces][kCRows];
-  auto tload = [&](int piece, int row) __attribute__((always_inline)) {
-    const uint32_t *tab = a.rpk + (size_t)edge(row) * kCKP * kCKP + toff + piece * kCRows * kCKP;
+  const uint32_t toff = (uint32_t)(S::PG * g * KP + S::SPL * qd);
+  u32x4 tb[S::NB][S::ROWS][S::V4];
+  auto tload = [&](int buf, int piece, int row) __attribute__((always_inline)) {
+    const uint32_t *tab = a.rpk + (size_t)edge(row) * KP * KP + toff + piece * S::ROWS * KP;
 #pragma unroll
-    for (int j = 0; j < kCRows; ++j) tb[piece][j] = *(const u32x4 *)(tab + j * kCKP);
+    for (int j = 0; j < S::ROWS; ++j)
+#pragma unroll
+      for (int v = 0; v < S::V4; ++v) tb[buf][j][v] = *(const u32x4 *)(tab + j * KP + 4 * v);
   };
   // Row minima of every chain from the threads' values: wave minima to LDS,
   // one barrier, then the minimum over the waves (uniform).
-  auto row_min = [&](const uint32_t(&x)[kCH], uint32_t(&d)[kCG]) __attribute__((always_inline)) {
+  auto row_min = [&](const uint32_t(&x)[CH], uint32_t(&d)[kCG]) __attribute__((always_inline)) {
 #pragma unroll
     for (int c = 0; c < kCG; ++c) {
-      const uint32_t w = cw_wave_min(((c & 1) == (f2 ? 1 : 0)) ? x[c >> 1] : kCX);
+      const uint32_t w = cw_wave_min((c % TPS) == sub ? x[c / TPS] : kCX);
       if (lane == 0) sm.wm[wid][c] = w;
     }
     __syncthreads();
@@ -201,11 +230,11 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
     ch.dconv[c] = 0;
     ch.dsum[c] = 0;
   }
-  uint32_t cor[kCH];
+  uint32_t cor[CH];
   if (MODE == kCSpec) {
-    uint32_t x[kCH], d[kCG];
+    uint32_t x[CH], d[kCG];
 #pragma unroll
-    for (int h = 0; h < kCH; ++h) {
+    for (int h = 0; h < CH; ++h) {
       const uint32_t cv = (uint32_t)cbase[h][(size_t)rs * K];
       cor[h] = cv;
       x[h] = (sin && cv != (uint32_t)CFP_COST_INF) ? cv : kCX;
@@ -217,22 +246,22 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
       ch.dsum[c] = d[c];
     }
 #pragma unroll
-    for (int h = 0; h < kCH; ++h) {
-      ch.x[h] = umin(x[h] - (f2 ? d[2 * h + 1] : d[2 * h]), kCCap) << kCBits;
+    for (int h = 0; h < CH; ++h) {
+      ch.x[h] = umin(x[h] - pick(d, h), S::CAP) << BITS;
       sm.q[0][hc[h]][qpad(ms)] = ch.x[h];
     }
     if (i0 > r1) {  // a run of one row (rs = r0): the start row is its checkpoint
 #pragma unroll
-      for (int h = 0; h < kCH; ++h)
-        if (hv[h]) ckb[h][(size_t)(r0 / 4) * kCKP] = ch.x[h];
+      for (int h = 0; h < CH; ++h)
+        if (hv[h]) ckb[h][(size_t)(r0 / 4) * KP] = ch.x[h];
 #pragma unroll
       for (int c = 0; c < kCG; ++c)
         if (tid == c && valid[c]) a.dck[(size_t)bs[c] * a.nq + r0 / 4] = (int64_t)ch.dsum[c];
     }
   } else {
 #pragma unroll
-    for (int h = 0; h < kCH; ++h) {
-      ch.x[h] = (f2 ? start[2 * h + 1] : start[2 * h])[ms];
+    for (int h = 0; h < CH; ++h) {
+      ch.x[h] = pick(start, h)[ms];
       sm.q[0][hc[h]][qpad(ms)] = ch.x[h];
       cor[h] = 0;
     }
@@ -240,24 +269,24 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
   auto negative_costs = [&]() __attribute__((always_inline)) {
 #pragma unroll
     for (int c = 0; c < kCG; ++c)
-      if (__syncthreads_or(((c & 1) == (f2 ? 1 : 0)) && (cor[c >> 1] >> 31))) ch.flags[c] |= 1;
+      if (__syncthreads_or(((c % TPS) == sub) && (cor[c / TPS] >> 31))) ch.flags[c] |= 1;
   };
   if (i0 > r1) {
     if (MODE == kCSpec) negative_costs();
     return;
   }
 #pragma unroll
-  for (int k = 0; k < kCPieces; ++k) tload(k, i0);
+  for (int k = 0; k < S::NB; ++k) tload(k, k, i0);
   // Costs of the next two rows, [row parity][pair]: step i uses set i - i0 mod 2
   // and reloads it with row i + 2 (the loop runs two rows per turn, so every
   // index is a constant and no register is copied from a load in flight).
-  uint32_t cq[2][kCH], ckv[kCH];
+  uint32_t cq[2][CH], ckv[CH];
 #pragma unroll
-  for (int h = 0; h < kCH; ++h) {
+  for (int h = 0; h < CH; ++h) {
     cq[0][h] = (uint32_t)cbase[h][(size_t)i0 * K];
     cq[1][h] = (uint32_t)cbase[h][(size_t)min(i0 + 1, r1) * K];
     ckv[h] = 0;
-    if (MODE == kCFix) ckv[h] = ckb[h][(size_t)(i0 >> 2) * kCKP];
+    if (CHECK) ckv[h] = ckb[h][(size_t)(i0 >> 2) * KP];
   }
   __syncthreads();
 
@@ -265,65 +294,91 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
   // fix-up pass is done.
   auto step = [&](int i, auto Pc) __attribute__((always_inline)) -> bool {
     constexpr int cur = decltype(Pc)::value, nxt = cur ^ 1;
-    uint32_t acc[kCG][4];
+    uint32_t acc[kCG][S::SPL];
 #pragma unroll
     for (int c = 0; c < kCG; ++c)
 #pragma unroll
-      for (int u = 0; u < 4; ++u) acc[c][u] = kSat;
+      for (int u = 0; u < S::SPL; ++u) acc[c][u] = kSat;
     const int inext = min(i + 1, r1);
+    for (int kk = 0; kk < S::PIECES; kk += S::NB) {
 #pragma unroll
-    for (int k = 0; k < kCPieces; ++k) {
-      uint32_t v[kCG][kCRows];  // the predecessors' values of this piece, per chain
-#pragma unroll
-      for (int c = 0; c < kCG; ++c) {
-        const uint32_t *qc = &sm.q[cur][c][qpad(32 * g) + 8 * k];
-        const u32x4 lo = *(const u32x4 *)qc, hi = *(const u32x4 *)(qc + 4);
-        v[c][0] = lo.x; v[c][1] = lo.y; v[c][2] = lo.z; v[c][3] = lo.w;
-        v[c][4] = hi.x; v[c][5] = hi.y; v[c][6] = hi.z; v[c][7] = hi.w;
-      }
-#pragma unroll
-      for (int j = 0; j < kCRows; j += 2) {
-        const u32x4 w = tb[k][j], y = tb[k][j + 1];
+      for (int bb = 0; bb < S::NB; ++bb) {
+        const int k = kk + bb;
+        uint32_t v[kCG][S::ROWS];  // the predecessors' values of this piece, per chain
 #pragma unroll
         for (int c = 0; c < kCG; ++c) {
-          acc[c][0] = umin(umin(acc[c][0], sat_add(v[c][j], w.x)), sat_add(v[c][j + 1], y.x));
-          acc[c][1] = umin(umin(acc[c][1], sat_add(v[c][j], w.y)), sat_add(v[c][j + 1], y.y));
-          acc[c][2] = umin(umin(acc[c][2], sat_add(v[c][j], w.z)), sat_add(v[c][j + 1], y.z));
-          acc[c][3] = umin(umin(acc[c][3], sat_add(v[c][j], w.w)), sat_add(v[c][j + 1], y.w));
+          const uint32_t *qc = &sm.q[cur][c][qpad(S::PG * g + S::ROWS * k)];
+          if constexpr (S::ROWS % 4 == 0) {
+#pragma unroll
+            for (int r4 = 0; r4 < S::ROWS / 4; ++r4) {
+              const u32x4 w = *(const u32x4 *)(qc + 4 * r4);
+              v[c][4 * r4] = w.x;
+              v[c][4 * r4 + 1] = w.y;
+              v[c][4 * r4 + 2] = w.z;
+              v[c][4 * r4 + 3] = w.w;
+            }
+          } else {
+#pragma unroll
+            for (int r2 = 0; r2 < S::ROWS / 2; ++r2) {
+              const uint2 w = *(const uint2 *)(qc + 2 * r2);
+              v[c][2 * r2] = w.x;
+              v[c][2 * r2 + 1] = w.y;
+            }
+          }
         }
+#pragma unroll
+        for (int j = 0; j < S::ROWS; j += 2) {
+#pragma unroll
+          for (int vv = 0; vv < S::V4; ++vv) {
+            const u32x4 w = tb[bb][j][vv], y = tb[bb][j + 1][vv];
+#pragma unroll
+            for (int c = 0; c < kCG; ++c) {
+              uint32_t *ac = &acc[c][4 * vv];
+              ac[0] = umin(umin(ac[0], sat_add(v[c][j], w.x)), sat_add(v[c][j + 1], y.x));
+              ac[1] = umin(umin(ac[1], sat_add(v[c][j], w.y)), sat_add(v[c][j + 1], y.y));
+              ac[2] = umin(umin(ac[2], sat_add(v[c][j], w.z)), sat_add(v[c][j + 1], y.z));
+              ac[3] = umin(umin(ac[3], sat_add(v[c][j], w.w)), sat_add(v[c][j + 1], y.w));
+            }
+          }
+        }
+        // the registers just consumed take the piece NB further on (of this row or the next)
+        const int nk = k + S::NB;
+        if (nk < S::PIECES) tload(bb, nk, i);
+        else tload(bb, nk - S::PIECES, inext);
       }
-      tload(k, inext);  // this piece of the next row into the registers just consumed
     }
     // Minima over the eight predecessor groups (one wave each) through LDS.
 #pragma unroll
-    for (int c = 0; c < kCG; ++c) {
-      u32x4 pv;
-      pv.x = acc[c][0];
-      pv.y = acc[c][1];
-      pv.z = acc[c][2];
-      pv.w = acc[c][3];
-      *(u32x4 *)&sm.part[c][g][4 * qd] = pv;
-    }
-    __syncthreads();
-    uint32_t m[kCH];
+    for (int c = 0; c < kCG; ++c)
 #pragma unroll
-    for (int h = 0; h < kCH; ++h) {
-      const int c = 2 * h + (f2 ? 1 : 0);
+      for (int vv = 0; vv < S::V4; ++vv) {
+        u32x4 pv;
+        pv.x = acc[c][4 * vv];
+        pv.y = acc[c][4 * vv + 1];
+        pv.z = acc[c][4 * vv + 2];
+        pv.w = acc[c][4 * vv + 3];
+        *(u32x4 *)&sm.part[c][g][S::SPL * qd + 4 * vv] = pv;
+      }
+    __syncthreads();
+    uint32_t m[CH];
+#pragma unroll
+    for (int h = 0; h < CH; ++h) {
+      const int c = hc[h];
       uint32_t v = sm.part[c][0][ms];
 #pragma unroll
       for (int w = 1; w < kCWaves; ++w) v = umin(v, sm.part[c][w][ms]);
       m[h] = v;
     }
 
-    // New row: the thread's pairs.
-    uint32_t x[kCH];
+    // New row: the thread's chains.
+    uint32_t x[CH];
 #pragma unroll
-    for (int h = 0; h < kCH; ++h) {
+    for (int h = 0; h < CH; ++h) {
       const uint32_t cv = cq[cur][h];
       cq[cur][h] = (uint32_t)cbase[h][(size_t)min(i + 2, r1) * K];
       if (MODE == kCSpec) cor[h] |= cv;
-      x[h] = (sin && cv != (uint32_t)CFP_COST_INF) ? (m[h] >> kCBits) + cv : kCX;
-      if (sin && hv[h] && i >= r0) tbase[h][(size_t)i * K] = (uint8_t)(m[h] & (kCKP - 1));
+      x[h] = (sin && cv != (uint32_t)CFP_COST_INF) ? (m[h] >> BITS) + cv : kCX;
+      if (sin && hv[h] && i >= r0) tbase[h][(size_t)i * K] = (Arg)(m[h] & (KP - 1));
     }
     uint32_t d[kCG];
     row_min(x, d);
@@ -333,8 +388,8 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
       ch.dsum[c] += d[c];
     }
 #pragma unroll
-    for (int h = 0; h < kCH; ++h) {
-      ch.x[h] = umin(x[h] - (f2 ? d[2 * h + 1] : d[2 * h]), kCCap) << kCBits;
+    for (int h = 0; h < CH; ++h) {
+      ch.x[h] = umin(x[h] - pick(d, h), S::CAP) << BITS;
       sm.q[nxt][hc[h]][qpad(ms)] = ch.x[h];
     }
     const bool qend = (i & 3) == 3 || i == r1;
@@ -342,26 +397,26 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
       const int q = i >> 2;
       if (MODE == kCSpec && i >= r0) {
 #pragma unroll
-        for (int h = 0; h < kCH; ++h)
-          if (hv[h]) ckb[h][(size_t)q * kCKP] = ch.x[h];
+        for (int h = 0; h < CH; ++h)
+          if (hv[h]) ckb[h][(size_t)q * KP] = ch.x[h];
 #pragma unroll
         for (int c = 0; c < kCG; ++c)
           if (tid == c && valid[c]) a.dck[(size_t)bs[c] * a.nq + q] = (int64_t)ch.dsum[c];
       }
-      if (MODE == kCFix) {
+      if (CHECK) {
 #pragma unroll
         for (int c = 0; c < kCG; ++c) {
-          const uint64_t off = __ballot(((c & 1) == (f2 ? 1 : 0)) && ch.x[c >> 1] != ckv[c >> 1]);
+          const uint64_t off = __ballot(((c % TPS) == sub) && ch.x[c / TPS] != ckv[c / TPS]);
           if (lane == 0) sm.wd[wid][c] = off != 0;
         }
         if (i < r1) {
 #pragma unroll
-          for (int h = 0; h < kCH; ++h) ckv[h] = ckb[h][(size_t)(q + 1) * kCKP];
+          for (int h = 0; h < CH; ++h) ckv[h] = ckb[h][(size_t)(q + 1) * KP];
         }
       }
     }
     __syncthreads();
-    if (MODE == kCFix && qend) {
+    if (CHECK && qend) {
       const int q = i >> 2;
       bool all = true;
 #pragma unroll
@@ -375,7 +430,7 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
         }
         all = all && (ch.conv[c] >= 0 || !valid[c]);
       }
-      if (all) return true;
+      if (MODE == kCFix && all) return true;
     }
     return false;
   };
@@ -388,9 +443,10 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
 
 // Speculative (MODE kCSpec, grid (ceil(B/kCG), P)) and fix-up (kCFix, grid
 // (ceil(B/kCG), P-1)) passes.
-template <int MODE>
+template <int KP, int MODE>
 __global__ __launch_bounds__(kCThreads, 1) void chain_cw_kernel(CwArgs a) {
-  __shared__ __align__(16) CwSmem sm;
+  using S = CwShape<KP>;
+  __shared__ __align__(16) CwSmem<KP> sm;
   int bs[kCG];
   bool valid[kCG];
 #pragma unroll
@@ -405,25 +461,24 @@ __global__ __launch_bounds__(kCThreads, 1) void chain_cw_kernel(CwArgs a) {
   const int rs = (MODE == kCSpec && p > 0) ? max(r0 - kCWarm, 0) : r0;
   const uint32_t *start[kCG];
 #pragma unroll
-  for (int c = 0; c < kCG; ++c) start[c] = a.ckrow + ((size_t)bs[c] * a.nq + (r0 > 0 ? r0 / 4 - 1 : 0)) * kCKP;
-  CwChains<MODE> ch;
-  cw_run<MODE>(a, bs, valid, rs, r0, r1, start, sm, ch);
+  for (int c = 0; c < kCG; ++c) start[c] = a.ckrow + ((size_t)bs[c] * a.nq + (r0 > 0 ? r0 / 4 - 1 : 0)) * KP;
+  CwChains<KP> ch;
+  cw_run<KP, MODE>(a, bs, valid, rs, r0, r1, start, sm, ch);
   const int tid = threadIdx.x;
-  const bool f2 = tid >= kCKP;
-  const int ms = tid & (kCKP - 1);
+  const int sub = S::TPS == 1 ? 0 : tid / KP;
+  const int ms = tid & (KP - 1);
   if (MODE == kCSpec) {
 #pragma unroll
     for (int c = 0; c < kCG; ++c)
       if (tid == 0 && valid[c]) a.rec[(size_t)bs[c] * a.P + p].flags = (int32_t)ch.flags[c];
   } else {
 #pragma unroll
-    for (int h = 0; h < kCH; ++h) {
-      const int c = 2 * h + (f2 ? 1 : 0);
-      const bool v = f2 ? valid[2 * h + 1] : valid[2 * h];
-      const int b = f2 ? bs[2 * h + 1] : bs[2 * h];
-      const int cv = f2 ? ch.conv[2 * h + 1] : ch.conv[2 * h];
-      (void)c;
-      if (v && cv < 0) a.endrow[((size_t)b * a.P + p) * kCKP + ms] = ch.x[h];
+    for (int h = 0; h < S::CH; ++h) {
+      const int c0 = S::TPS * h;  // chain c0 + sub
+      const bool v = sub ? valid[c0 + S::TPS - 1] : valid[c0];
+      const int cv = sub ? ch.conv[c0 + S::TPS - 1] : ch.conv[c0];
+      const int bh = sub ? bs[c0 + S::TPS - 1] : bs[c0];
+      if (v && cv < 0) a.endrow[((size_t)bh * a.P + p) * KP + ms] = ch.x[h];
     }
 #pragma unroll
     for (int c = 0; c < kCG; ++c) {
@@ -435,76 +490,93 @@ __global__ __launch_bounds__(kCThreads, 1) void chain_cw_kernel(CwArgs a) {
   }
 }
 
-// Final pass, one workgroup per search: chunk offsets, the rerun of the chain
-// after a chunk whose fix-up met no checkpoint, and the lowest optimal final
-// state.
+// Final pass, one workgroup per search: the chunk offsets, the reruns after
+// chunks whose fix-up met no checkpoint, and the lowest optimal final state.
+template <int KP>
 __global__ __launch_bounds__(kCThreads, 1) void chain_cw_final_kernel(CwArgs a, const WsHeader *__restrict__ hdr,
                                                                        SearchResult *__restrict__ res,
                                                                        int64_t *__restrict__ opt,
                                                                        int32_t *__restrict__ status) {
-  __shared__ __align__(16) CwSmem sm;
+  using S = CwShape<KP>;
+  __shared__ __align__(16) CwSmem<KP> sm;
+  __shared__ uint32_t s_row[KP];  // a true end row of the last chunk accounted
   __shared__ int s_q, s_flags;
-  __shared__ int64_t s_dtot;
+  __shared__ int64_t s_sum;
   __shared__ uint32_t s_fin[kCWaves];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int b = blockIdx.x, P = a.P;
+  const int ms = tid & (KP - 1);
+  const int64_t *dk = a.dck + (size_t)b * a.nq;
+  const CwRec *rec = a.rec + (size_t)b * P;
+  auto endq = [&](int p) __attribute__((always_inline)) { return (min((p + 1) * a.CL, a.N) - 1) >> 2; };
   if (wid == 0) {
-    const bool in = lane < P;
-    CwRec r{};
-    if (in) r = a.rec[(size_t)b * P + lane];
-    const int endq = (min((lane + 1) * a.CL, a.N) - 1) >> 2;  // quad of the chunk's last row
-    const uint64_t nc = __ballot(in && lane >= 1 && r.conv < 0);
-    const int q = nc ? __ffsll((long long)nc) - 1 : P;  // first chunk whose fix-up met no checkpoint
-    int64_t delta = 0;
-    if (in && lane < q) {
-      const int64_t *dk = a.dck + (size_t)b * a.nq;
-      delta = lane == 0 ? dk[endq] : r.dfix + dk[endq] - dk[r.conv];
-    } else if (lane == q) {
-      delta = r.dfix;  // its fix-up started from the true row and ran to the end
-    }
-    int fl = in ? r.flags : 0;
+    int fl = lane < P ? rec[lane].flags : 0;
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-      delta += __shfl_xor(delta, off, 64);
-      fl |= __shfl_xor(fl, off, 64);
-    }
-    if (lane == 0) {
-      s_q = q;
-      s_dtot = delta;
-      s_flags = fl;
-    }
+    for (int off = 32; off >= 1; off >>= 1) fl |= __shfl_xor(fl, off, 64);
+    if (lane == 0) s_flags = fl;
   }
-  __syncthreads();
-  const int q = s_q;
-  uint64_t drep = 0;
-  // the final row: chain 0 of state s is held by thread s, as pair 0
-  const bool f2 = tid >= kCKP;
-  const int ms = tid & (kCKP - 1);
-  uint32_t xv;
-  if (q < P - 1) {
-    // Rerun the chain after chunk q from its true end row (the other chains
-    // duplicate it and are discarded).
-    const uint32_t *st = a.endrow + ((size_t)b * P + q) * kCKP;
-    int bs[kCG];
-    bool valid[kCG];
-    const uint32_t *start[kCG];
+  // Chunk 0 runs from the true first row.  Invariant at the top of the loop:
+  // chunks < p are accounted in `total`; if spec_true, the speculative end row
+  // of chunk p-1 is a true row (so the fix-up of chunk p is valid), otherwise
+  // s_row holds the true end row of chunk p-1.
+  int64_t total = dk[endq(0)];
+  bool spec_true = true;
+  int p = 1;
+  while (p < P) {
+    if (spec_true) {
+      // With wave 0: the first chunk q >= p whose fix-up met no checkpoint, and
+      // the offsets of chunks p .. q (chunk q's fix-up ran from a true row to its end).
+      if (wid == 0) {
+        const int pl = p + lane;
+        const bool in = pl < P;
+        CwRec r{};
+        if (in) r = rec[pl];
+        const uint64_t nc = __ballot(in && r.conv < 0);
+        const int q = nc ? p + __ffsll((long long)nc) - 1 : P;
+        int64_t delta = 0;
+        if (in && pl < q) delta = r.dfix + dk[endq(pl)] - dk[r.conv];
+        else if (in && pl == q) delta = r.dfix;
 #pragma unroll
-    for (int c = 0; c < kCG; ++c) {
-      bs[c] = b;
-      valid[c] = c == 0;
-      start[c] = st;
+        for (int off = 32; off >= 1; off >>= 1) delta += __shfl_xor(delta, off, 64);
+        if (lane == 0) {
+          s_q = q;
+          s_sum = delta;
+        }
+      }
+      __syncthreads();
+      const int q = s_q;
+      total += s_sum;
+      if (q >= P) break;
+      if (tid < KP) s_row[tid] = a.endrow[((size_t)b * P + q) * KP + tid];
+      spec_true = false;
+      p = q + 1;
+      __syncthreads();
+    } else {
+      // Rerun chunk p whole from the true row in s_row; its rows are then
+      // true, and so is its speculative end row if the rerun met a checkpoint.
+      int bs[kCG];
+      bool valid[kCG];
+      const uint32_t *start[kCG];
+#pragma unroll
+      for (int c = 0; c < kCG; ++c) {
+        bs[c] = b;
+        valid[c] = c == 0;  // the other chains duplicate it and are discarded
+        start[c] = s_row;
+      }
+      CwChains<KP> ch;
+      const int r0 = p * a.CL, r1 = min(r0 + a.CL, a.N) - 1;
+      cw_run<KP, kCRepair>(a, bs, valid, r0, r0, r1, start, sm, ch);
+      total += (int64_t)ch.dsum[0];
+      spec_true = ch.conv[0] >= 0;
+      __syncthreads();  // every thread has read s_row
+      if (!spec_true && tid < KP) s_row[tid] = ch.x[0];  // chain 0 of state tid is the thread's first
+      __syncthreads();
+      ++p;
     }
-    CwChains<kCRepair> ch;
-    cw_run<kCRepair>(a, bs, valid, (q + 1) * a.CL, (q + 1) * a.CL, a.N - 1, start, sm, ch);
-    xv = ch.x[0];
-    drep = ch.dsum[0];
-  } else if (q == P - 1) {
-    xv = a.endrow[((size_t)b * P + q) * kCKP + ms];
-  } else {
-    xv = a.ckrow[((size_t)b * a.nq + a.nq - 1) * kCKP + ms];
   }
   // The final row has minimum 0: the lowest state at the minimum.
-  const uint32_t pk = cw_wave_min((!f2 && ms < a.K) ? (xv | (uint32_t)ms) : kSat);
+  const uint32_t xv = spec_true ? a.ckrow[((size_t)b * a.nq + a.nq - 1) * KP + ms] : s_row[ms];
+  const uint32_t pk = cw_wave_min((tid < KP && ms < a.K) ? (xv | (uint32_t)ms) : kSat);
   if (lane == 0) s_fin[wid] = pk;
   __syncthreads();
   if (tid == 0) {
@@ -514,32 +586,46 @@ __global__ __launch_bounds__(kCThreads, 1) void chain_cw_final_kernel(CwArgs a, 
     int st = CFP_ST_OK;
     if ((fl & 1) || hdr->rflag) st = CFP_ST_BADINPUT;
     else if (fl & 2) st = CFP_ST_INFEASIBLE;
-    else if ((fin >> kCBits) != 0) st = CFP_ST_OVERFLOW;
+    else if ((fin >> S::BITS) != 0) st = CFP_ST_OVERFLOW;
     status[b] = st;
-    opt[b] = st == CFP_ST_OK ? s_dtot + (int64_t)drep : INT64_MAX;
-    res[b].final_state = st == CFP_ST_OK ? (int32_t)(fin & (kCKP - 1)) : -1;
+    opt[b] = st == CFP_ST_OK ? total : INT64_MAX;
+    res[b].final_state = st == CFP_ST_OK ? (int32_t)(fin & (KP - 1)) : -1;
     res[b].status = st;
     res[b].final_m = 0;
   }
 }
 
 struct CwPlan {
-  int P, CL, nq;
+  int KP, P, CL, nq;
 };
 
 CwPlan cw_plan(int n, int k, int batch) {
-  CwPlan c{0, 0, 0};
-  if (k <= 128 || k > kCKP || n < 2 * kCMinRows) return c;
+  CwPlan c{0, 0, 0, 0};
+  if (k <= 128 || k > 512) return c;
+  const int kp = k <= 256 ? 256 : 512;
+  const int minrows = kp == 256 ? CwShape<256>::MINROWS : CwShape<512>::MINROWS;
+  if (n < 2 * minrows) return c;
   const int groups = (batch + kCG - 1) / kCG;
   int P = std::max(2, (256 + groups - 1) / groups);  // about one workgroup per compute unit
-  P = std::min(P, std::min(kCMaxChunks, n / kCMinRows));
+  P = std::min(P, std::min(kCMaxChunks, n / minrows));
   int CL = ((n + P - 1) / P + 3) & ~3;
   P = (n + CL - 1) / CL;
   if (P < 2) return c;
+  c.KP = kp;
   c.P = P;
   c.CL = CL;
   c.nq = (n + 3) / 4;
   return c;
+}
+
+template <int KP>
+void launch_cw_kp(const CwArgs &a, int groups, const WsHeader *hdr, SearchResult *res, int64_t *opt,
+                  int32_t *status, hipStream_t st) {
+  timer_begin(st);
+  timed_launch(chain_cw_kernel<KP, kCSpec>, dim3(groups, a.P), dim3(kCThreads), 0, st, a);
+  timer_end(st);
+  hipLaunchKernelGGL((chain_cw_kernel<KP, kCFix>), dim3(groups, a.P - 1), dim3(kCThreads), 0, st, a);
+  hipLaunchKernelGGL(chain_cw_final_kernel<KP>, dim3(a.B), dim3(kCThreads), 0, st, a, hdr, res, opt, status);
 }
 
 }  // namespace
@@ -549,17 +635,19 @@ bool chain_cw_supported(int n, int k, int batch) { return cw_plan(n, k, batch).P
 size_t cw_region_bytes(int n, int k, int n_tables, int batch) {
   const CwPlan c = cw_plan(n, k, batch);
   if (c.P < 2) return 0;
-  size_t off = align_up((size_t)n_tables * kCKP * kCKP * 4);
+  const size_t kp = c.KP;
+  size_t off = align_up((size_t)n_tables * kp * kp * 4);
   off += align_up((size_t)batch * c.P * sizeof(CwRec));
   off += align_up((size_t)batch * c.nq * 8);
-  off += align_up((size_t)batch * c.nq * kCKP * 4);
-  off += align_up((size_t)batch * c.P * kCKP * 4);
+  off += align_up((size_t)batch * c.nq * kp * 4);
+  off += align_up((size_t)batch * c.P * kp * 4);
   return off;
 }
 
 hipError_t launch_chain_cw(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *region, uint8_t *table,
                            SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st) {
   const CwPlan c = cw_plan(d.n_blocks, d.k, d.batch);
+  const size_t kp = c.KP;
   CwArgs a;
   a.cost = d.cost;
   a.redge = redge_dev;
@@ -573,22 +661,19 @@ hipError_t launch_chain_cw(const cfp_chain_desc &d, const int32_t *redge_dev, ui
   size_t off = 0;
   uint32_t *rpk = (uint32_t *)(region + off);
   a.rpk = rpk;
-  off += align_up((size_t)d.n_tables * kCKP * kCKP * 4);
+  off += align_up((size_t)d.n_tables * kp * kp * 4);
   a.rec = (CwRec *)(region + off);
   off += align_up((size_t)d.batch * c.P * sizeof(CwRec));
   a.dck = (int64_t *)(region + off);
   off += align_up((size_t)d.batch * c.nq * 8);
   a.ckrow = (uint32_t *)(region + off);
-  off += align_up((size_t)d.batch * c.nq * kCKP * 4);
+  off += align_up((size_t)d.batch * c.nq * kp * 4);
   a.endrow = (uint32_t *)(region + off);
-  launch_pack_rtab(d.rtab, d.n_tables, d.k, kCKP, kCBits, rpk, st, cfp_r_limit(CFP_V_CHAIN, d.k),
-                   const_cast<WsHeader *>(hdr));
+  launch_pack_rtab(d.rtab, d.n_tables, d.k, (int)kp, kp == 256 ? CwShape<256>::BITS : CwShape<512>::BITS, rpk, st,
+                   cfp_r_limit(CFP_V_CHAIN, d.k), const_cast<WsHeader *>(hdr));
   const int groups = (d.batch + kCG - 1) / kCG;
-  timer_begin(st);
-  timed_launch(chain_cw_kernel<kCSpec>, dim3(groups, c.P), dim3(kCThreads), 0, st, a);
-  timer_end(st);
-  hipLaunchKernelGGL(chain_cw_kernel<kCFix>, dim3(groups, c.P - 1), dim3(kCThreads), 0, st, a);
-  hipLaunchKernelGGL(chain_cw_final_kernel, dim3(d.batch), dim3(kCThreads), 0, st, a, hdr, res, opt, status);
+  if (kp == 256) launch_cw_kp<256>(a, groups, hdr, res, opt, status, st);
+  else launch_cw_kp<512>(a, groups, hdr, res, opt, status, st);
   return hipGetLastError();
 }
 

@@ -179,9 +179,10 @@ def test_wide_path_many_tables():
     assert_chain_parity(cost, rtab, redge, "wide E=17")
 
 
-@pytest.mark.parametrize("N,K,B", [(300, 65, 4), (500, 128, 60), (400, 256, 16), (257, 257, 4), (200, 512, 4)])
+@pytest.mark.parametrize("N,K,B", [(300, 65, 4), (500, 128, 60), (31, 256, 16), (120, 257, 4), (127, 512, 4)])
 def test_split_path_long_chains(N, K, B):
-    """Few long chains spread over many workgroups (B * P = 256 at the largest)."""
+    """Few chains spread over many workgroups (B * P = 256 at the largest); the
+    chains with K > 128 are too short for the chunk-parallel form."""
     need_gpu()
     from paper_2504_00598_amd import cfp_r_limit
     say("split path", N, K, B)
@@ -190,12 +191,13 @@ def test_split_path_long_chains(N, K, B):
     assert_chain_parity(cost, rtab, redge, f"split N={N} K={K} B={B}")
 
 
-def test_long_chain_workload_sequential():
-    """The 4096-block K=512 workload of the scan through the chain search."""
+def test_long_chain_workload():
+    """The 4096-block K=512 workload of the scan through the chain search (64
+    chunks of 64 rows)."""
     need_gpu()
     say("config scan_n4096_k512 through cfp_dp_chain")
     d = configs.make("scan_n4096_k512")
-    assert_chain_parity(d["cost"], d["rtab"], d["redge"], "long chain sequential")
+    assert_chain_parity(d["cost"], d["rtab"], d["redge"], "long chain K=512")
 
 
 # 32 < K <= 64 on long chains (at least 8 blocks of 12 rows) with at most 12 tables runs
@@ -422,3 +424,66 @@ def test_range_flag_ignores_stale_workspace_bytes():
         np.testing.assert_array_equal(r.status.cpu().numpy(), o_st, err_msg=f"status, stale word {v}")
         np.testing.assert_array_equal(r.opt.cpu().numpy(), o_opt, err_msg=f"opt, stale word {v}")
         np.testing.assert_array_equal(r.plan.cpu().numpy(), o_plan, err_msg=f"plan, stale word {v}")
+
+
+# 256 < K <= 512 on chains of at least 128 blocks runs chunk-parallel with chunks of at
+# least 64 rows (runs take tens of rows to become parallel at this width).  The final
+# pass reruns, whole, each chunk that follows one whose fix-up met no checkpoint.
+
+@pytest.mark.parametrize("N,K,B", [(128, 512, 1), (300, 400, 5), (1000, 512, 3), (640, 300, 8), (129, 257, 2),
+                                   (4096, 512, 1)])
+def test_chunked_k512_shapes(N, K, B):
+    """Two chunks of 64 rows, ragged K and batches, ragged last chunks, 64 chunks."""
+    need_gpu()
+    from paper_2504_00598_amd import cfp_r_limit
+    rhi = min(1_000_000, cfp_r_limit(0, K))
+    cost, rtab, redge = rand_case([48, N, K, B], B, N, K, 12, 10_000, 1_000_000, rlo=10_000, rhi=rhi)
+    if N % 2 == 0:
+        redge = (np.arange(N) % 12).astype(np.int32)
+    say("chunked K>256 shape", N, K, B)
+    assert_chain_parity(cost, rtab, redge, f"chunked K>256 N={N} K={K} B={B}")
+
+
+@pytest.mark.parametrize("K,B", [(512, 2), (300, 5)])
+def test_chunked_k512_rows_never_meet(K, B):
+    """No chunk meets its checkpoints: every chunk after the first is rerun in turn."""
+    need_gpu()
+    from paper_2504_00598_amd import cfp_r_limit
+    rs = np.random.default_rng([49, K, B])
+    N = 400
+    cost = rs.integers(0, 50, size=(B, N, K)).astype(np.int32)
+    rtab = _no_switch_tables(rs, 12, K, cfp_r_limit(0, K))
+    redge = (np.arange(N) % 12).astype(np.int32)
+    say("chunked K>256, no convergence", K, B)
+    assert_chain_parity(cost, rtab, redge, f"K>256 never meet K={K} B={B}")
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_chunked_k512_some_chunks_meet(seed):
+    """Zero tables on a few edges: a seeded mix of chunks that meet in the fix-up
+    pass, chunks that meet only when rerun, and chunks that never meet."""
+    need_gpu()
+    from paper_2504_00598_amd import cfp_r_limit
+    rs = np.random.default_rng([50, seed])
+    K, B, N = 512, 3, 900
+    cost = rs.integers(0, 1000, size=(B, N, K)).astype(np.int32)
+    rtab = _no_switch_tables(rs, 3, K, cfp_r_limit(0, K))
+    rtab[2] = 0
+    redge = rs.integers(0, 2, size=N).astype(np.int32)
+    resets = rs.choice(np.arange(1, N), size=int(rs.integers(1, 8)), replace=False)
+    redge[resets] = 2
+    say("chunked K>256, partial convergence", seed, sorted(resets.tolist()))
+    assert_chain_parity(cost, rtab, redge, f"K>256 partial seed={seed}")
+
+
+def test_chunked_k512_ties_and_statuses():
+    """Tie-heavy values, unavailable strategies, an infeasible search and a negative cost."""
+    need_gpu()
+    from paper_2504_00598_amd import CFP_ST_BADINPUT
+    cost, rtab, redge = rand_case([51], 5, 300, 512, 5, 0, 3, inf_frac=0.1)
+    cost[2, 250, :] = INF   # infeasible search, in a late chunk
+    assert_chain_parity(cost, rtab, redge, "chunked K>256 ties")
+    cost[4, 70, 3] = -7     # a negative cost is rejected by the library
+    opt, st, plan = run_chain(cost, rtab, redge)
+    assert st[4] == CFP_ST_BADINPUT and opt[4] == np.iinfo(np.int64).max and (plan[4] == -1).all()
+    assert st[2] != 0 and (st[[0, 1, 3]] == 0).all()

@@ -7,7 +7,7 @@ cost row, so that states far above a row's minimum (where the kernels cap
 their normalised values) are reached by finite costs and not only by
 unavailable strategies and padding.  Each shape is chosen to land on one
 kernel family of the chain search (register-resident K <= 32 and K <= 64,
-chunk-parallel K <= 64 and K <= 256, split, split with streamed tables, wide,
+chunk-parallel K <= 64, K <= 256 and K <= 512, split, split with streamed tables, wide,
 the generic kernel for many tables), and the memory, frontier, scan and
 segment entry points get the same treatment.  The bar is the oracle's answer
 bit for bit: optimum, status and every plan entry (Sec. 4.4, Eq. T and Eq. M).
@@ -57,6 +57,8 @@ CHAIN_CASES = [
     (300, 48, 20, 12, False, "chunk-parallel K<=64"),
     (200, 256, 9, 12, True, "chunk-parallel K<=256"),
     (100, 200, 3, 5, False, "chunk-parallel K<=256, ragged K"),
+    (200, 512, 4, 12, True, "chunk-parallel K<=512"),
+    (130, 300, 3, 7, False, "chunk-parallel K<=512, ragged K"),
     (100, 100, 4, 12, False, "split, tables in registers"),
     (30, 512, 2, 12, False, "split K=512"),
     (60, 100, 8, 17, False, "split, streamed tables"),
