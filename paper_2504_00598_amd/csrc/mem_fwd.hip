@@ -12,8 +12,10 @@
 // a step is one min-plus product of the previous rows (buckets x states) with
 // the K x K table, followed by a per-state shift of the product along m.
 //
-// Layout.  The buckets of a search are cut into chunks of 64; one workgroup of
-// four waves computes one chunk for all states.  Wave w owns buckets
+// Layout.  The buckets of a search are cut into chunks of 64; one workgroup
+// computes one chunk for all states with four compute waves, a loading wave
+// and a storing wave (the compute waves issue no global stores, so none of
+// their waits for a load ever covers a store).  Compute wave w owns buckets
 // 16w .. 16w+15 of its chunk, lane (g, m) = (lane / 16, lane % 16) the bucket
 // 16w + m and the K/4 states g K/4 .. g K/4 + K/4 - 1.  The previous row of a
 // bucket sits in registers (32 predecessors at a time), and the table entry
@@ -24,11 +26,14 @@
 // the 16 entries of its row's state, a few items ahead.
 // Step i of bucket m reads products at m - d >= m - 16, i.e. of the wave below
 // (through a product buffer in LDS) or, for wave 0, of the top 16 buckets of
-// the chunk below, which that chunk's wave 3 passes through a ring of eight
-// slots in device memory together with its offsets.  Every ring word carries
+// the chunk below, which that chunk's storing wave passes through a ring of
+// eight slots in device memory together with its offsets.  The loading wave
+// fetches the slots and stages the next step's per-state records (and, for
+// K <= 64, the step's table) in LDS; the storing wave writes the ring slots,
+// the publication counter and the argmin bytes of earlier steps.  Every ring word carries
 // the number of its step in its upper half, so no store is ever waited for:
-// the chunk above loads a slot at the start of a step and, after its products,
-// reloads it until every word has the step's number; a chunk waits before
+// the chunk above loads a slot ahead of the step that needs it and reloads it
+// until every word has the step's number; a chunk waits before
 // reusing a slot until the chunk above has consumed it (all waits bounded).
 // The chunks of one launch are resident together (the host launches the
 // searches in rounds that fit), so the ring stays in the L2 cache.
