@@ -230,6 +230,26 @@ int cfp_dp_segments(const cfp_segment_desc *d, void *ws, size_t ws_bytes, int64_
  * descriptor (lowest optimal final plan, lowest predecessor at every step). */
 int cfp_traceback_segments(const cfp_segment_desc *d, void *ws, size_t ws_bytes, int32_t *plan, void *stream);
 
+/* Whole search in one call: cfp_dp_chain followed by cfp_traceback (Sec. 4.4:
+ * the Eq. T recurrence, then the lowest-index optimal plan), with the same
+ * results, statuses and plans.
+ *   ws, ws_bytes  as for cfp_dp_chain.  Small searches (K <= 64, N <= 512,
+ *                 B <= 256, n_tables <= 255 and
+ *                 E*KP*(KP+4)*4 + N*(5*KP+1) <= 61440 with KP = K rounded
+ *                 up to 16, 32 or 64) do not use it (it may then be NULL):
+ *                 they run as one kernel launch that also checks the range
+ *                 of R, with the edge map passed in the launch's arguments
+ *                 (no host-to-device copy).  Larger searches run the two
+ *                 calls and return CFP_ERR_WORKSPACE for a missing or short
+ *                 workspace.
+ *   opt, status   device [B], as cfp_dp_chain writes them.
+ *   plan          device [B][N] int32, as cfp_traceback writes it.
+ * opt, status and plan may also be pinned host memory mapped into the
+ * device's address space (hipHostMalloc) on the one-launch path, which then
+ * needs no copy back. */
+int cfp_search_chain(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t *opt, int32_t *status,
+                     int32_t *plan, void *stream);
+
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid allocation): the same
  * search as cfp_dp_chain followed by cfp_traceback, with the workspace taken

@@ -37,7 +37,7 @@ CFP_MAX_K = 512
 EXPORTED = ("cfp_r_limit", "cfp_workspace_bytes", "cfp_dp_chain", "cfp_dp_chain_mem", "cfp_mem_frontier",
             "cfp_minplus_scan", "cfp_traceback", "cfp_segment_workspace_bytes", "cfp_dp_segments",
             "cfp_traceback_segments", "cfp_status_string", "cfp_timer_start", "cfp_timer_stop",
-            "cfp_search_chain_noalloc")
+            "cfp_search_chain", "cfp_search_chain_noalloc")
 
 
 class CfpError(RuntimeError):
@@ -107,6 +107,8 @@ def lib() -> ctypes.CDLL:
         L.cfp_dp_segments.restype = ctypes.c_int
         L.cfp_traceback_segments.argtypes = [SD, P, ctypes.c_size_t, P, P]
         L.cfp_traceback_segments.restype = ctypes.c_int
+        L.cfp_search_chain.argtypes = [D, P, ctypes.c_size_t, P, P, P, P]
+        L.cfp_search_chain.restype = ctypes.c_int
         L.cfp_search_chain_noalloc.argtypes = [D, P, P, P, P]
         L.cfp_search_chain_noalloc.restype = ctypes.c_int
         L.cfp_timer_start.argtypes = [I32]
@@ -248,6 +250,34 @@ def cfp_traceback_segments(desc: SegDesc, ws, plan=None, stream=None):
 
 
 CFP_NOALLOC_MAX_BYTES = 32 << 20
+
+
+def cfp_search_chain(desc: Desc, ws=None, opt=None, status=None, plan=None, stream=None):
+    """Enqueue the whole chain search (forward and traceback) in one call; small
+    searches run as one kernel launch and need no workspace (ws may be None then,
+    and is allocated otherwise).  Returns (opt, status, plan)."""
+    import torch
+
+    dev = desc.cost.device
+    if ws is None and not chain_search_is_one_launch(desc):
+        ws = _alloc(cfp_workspace_bytes(desc, CFP_V_CHAIN), dev)
+    opt = torch.empty(desc.B, dtype=torch.int64, device=dev) if opt is None else opt
+    status = torch.empty(desc.B, dtype=torch.int32, device=dev) if status is None else status
+    plan = torch.empty((desc.B, desc.N), dtype=torch.int32, device=dev) if plan is None else plan
+    _check("cfp_search_chain", lib().cfp_search_chain(desc.ref, _ptr(ws) if ws is not None else None,
+                                                      ws.numel() if ws is not None else 0, _ptr(opt),
+                                                      _ptr(status), _ptr(plan), _stream(stream)))
+    return opt, status, plan
+
+
+def chain_search_is_one_launch(desc: Desc) -> bool:
+    """Whether cfp_search_chain runs `desc` as its one-launch path (the rule
+    documented in cfp.h)."""
+    K, N, B, E = desc.K, desc.N, desc.B, desc.E
+    if K > 64 or N > 512 or B > 256 or E > 255:
+        return False
+    kp = 16 if K <= 16 else 32 if K <= 32 else 64
+    return E * kp * (kp + 4) * 4 + N * (5 * kp + 1) <= 61440
 
 
 def cfp_search_chain_noalloc(desc: Desc, opt=None, status=None, plan=None, stream=None):

@@ -414,6 +414,18 @@ int cfp_traceback(const cfp_chain_desc *d, int32_t variant, int32_t n_mem, void 
   return e == hipSuccess ? CFP_OK : CFP_ERR_HIP;
 }
 
+int cfp_search_chain(const cfp_chain_desc *d, void *ws, size_t ws_bytes, int64_t *opt, int32_t *status,
+                     int32_t *plan, void *stream) {
+  int rc = check_desc(d);
+  if (rc != CFP_OK) return rc;
+  if (!opt || !status || !plan) return CFP_ERR_ARG;
+  hipStream_t st = (hipStream_t)stream;
+  if (chain_small_supported(d->n_blocks, d->k, d->n_tables, d->batch))
+    return launch_chain_small(*d, opt, status, plan, st) == hipSuccess ? CFP_OK : CFP_ERR_HIP;
+  if ((rc = cfp_dp_chain(d, ws, ws_bytes, opt, status, stream)) != CFP_OK) return rc;
+  return cfp_traceback(d, CFP_V_CHAIN, 0, ws, ws_bytes, plan, stream);
+}
+
 int cfp_search_chain_noalloc(const cfp_chain_desc *d, int64_t *opt, int32_t *status, int32_t *plan,
                              void *stream) {
   int rc = check_desc(d);

@@ -87,6 +87,13 @@ hipError_t launch_chain_wave(const cfp_chain_desc &d, const int32_t *redge_dev, 
                              SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
                              hipStream_t st);
 bool chain_cw_supported(int n, int k, int batch);
+// One-launch search of small chains (forward, range checks and traceback).
+constexpr int kSmallMaxN = 512;
+constexpr int kSmallMaxBatch = 256;
+constexpr size_t kSmallMaxLds = 60 * 1024;  // dynamic LDS, with room for the kernel's static words
+bool chain_small_supported(int n, int k, int n_tables, int batch);
+hipError_t launch_chain_small(const cfp_chain_desc &d, int64_t *opt, int32_t *status, int32_t *plan,
+                              hipStream_t st);
 size_t cw_region_bytes(int n, int k, int n_tables, int batch);
 hipError_t launch_chain_cw(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *region, uint8_t *table,
                            SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st);
