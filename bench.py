@@ -41,7 +41,8 @@ PEAK_CELLS = VALU_LANE_OPS / INSTR_PER_CELL
 # The kernel that dominates the forward pass of each workload, and the source
 # files it is built from.
 KERNELS = {
-    "chain_gpt_n24_k16": ("chain_fwd_res_kernel<16,12>", ["chain_fwd_res.hip", "res_common.h"]),
+    # one launch of cfp_search_chain: forward pass and traceback
+    "chain_gpt_n24_k16": ("chain_small_kernel<16>", ["chain_small.hip"]),
     # speculative pass of the chunk-parallel search: it computes every step of every chain
     "chain_gpt_n1152_k64": ("chain_wave_kernel<12>", ["chain_wave.hip", "res_common.h"]),
     "mem_llama_n288_k32": ("mem_fwd_kernel<32>", ["mem_fwd.hip", "res_common.h"]),
@@ -63,15 +64,17 @@ COMMON_SOURCES = ["common.h", "cfp_internal.h", "../../include/cfp.h"]
 # changed and the figure is withheld.
 FETCH_SCALE, WRITE_SCALE = 524288.0 / 262167.1, 524288.0 / 524288.0
 TRAFFIC = {
-    "chain_gpt_n24_k16": {"fetch_kib": 18.0, "write_kib": 0.5, "sources": "44bed4f0eb55d922"},
+    "chain_gpt_n24_k16": {"fetch_kib": 12.7, "write_kib": 0.2, "sources": "08c51b7710b5e094"},
     "chain_gpt_n1152_k64": {"fetch_kib": 37972.6, "write_kib": 37516.1, "sources": "cec3c986f0b278db"},
     "mem_llama_n288_k32": {"fetch_kib": 127642.5, "write_kib": 338789.9, "sources": "8819739b408e81c0"},
-    "chain_wide_n512_k256": {"fetch_kib": 44580.6, "write_kib": 16424.0, "sources": "089a067565012ace"},
+    "chain_wide_n512_k256": {"fetch_kib": 44222.6, "write_kib": 16425.8, "sources": "c125e5f6d9988dd4"},
     # mean over the 12 matrix-product launches of one forward call
     "scan_n4096_k512": {"fetch_kib": 3035064.5, "write_kib": 1398442.5, "sources": "f9f8fcff938ec825"},
     "seg_gpt_n96_k81": {"fetch_kib": 3922.9, "write_kib": 1936.0, "sources": "3cb0a9594fc4041e"},
     # the memory workload run as a budget frontier (every chunk of every search active)
     "mem_llama_n288_k32:frontier": {"fetch_kib": 166635.1, "write_kib": 442222.7, "sources": "8819739b408e81c0"},
+    # the scan workload through the chain search (speculative pass)
+    "scan_n4096_k512:chain": {"fetch_kib": 801615.2, "write_kib": 25992.0, "sources": "c125e5f6d9988dd4"},
 }
 
 
@@ -172,7 +175,10 @@ def cpu_baseline(cfg, data, budget_s: float = 10.0) -> dict:
 class Runner:
     """Device buffers and the two calls of one search pass.  With frontier=True
     (memory workload) the forward pass is the budget frontier: the least cost
-    at every budget 0 .. M-1, and the traceback returns the plans at M-1."""
+    at every budget 0 .. M-1, and the traceback returns the plans at M-1.  A
+    chain search small enough for the one-launch path of cfp_search_chain runs
+    as that one call (forward pass and traceback together, the traceback step
+    then empty)."""
 
     def __init__(self, cfg, data, frontier: bool = False):
         import torch
@@ -202,6 +208,7 @@ class Runner:
             self.budget = torch.from_numpy(data["budget"]).cuda()
         self.ws = torch.empty(L.cfp_workspace_bytes(self.desc, self.variant, self.n_mem), dtype=torch.uint8,
                               device="cuda")
+        self.one_call = cfg.form == "chain" and L.chain_search_is_one_launch(self.desc)
         if frontier:
             if cfg.form != "mem":
                 raise ValueError("the budget frontier needs the memory workload")
@@ -211,6 +218,9 @@ class Runner:
         L = self.L
         if self.variant == L.CFP_V_SEG:
             L.cfp_dp_segments(self.sdesc, ws=self.ws, opt=self.opt, status=self.status, stream=self.stream)
+        elif self.variant == L.CFP_V_CHAIN and self.one_call:
+            L.cfp_search_chain(self.desc, ws=self.ws, opt=self.opt, status=self.status, plan=self.plan,
+                               stream=self.stream)
         elif self.variant == L.CFP_V_CHAIN:
             L.cfp_dp_chain(self.desc, ws=self.ws, opt=self.opt, status=self.status, stream=self.stream)
         elif self.frontier is not None:
@@ -223,6 +233,8 @@ class Runner:
             L.cfp_minplus_scan(self.desc, ws=self.ws, opt=self.opt, status=self.status, stream=self.stream)
 
     def traceback(self):
+        if getattr(self, "one_call", False):
+            return
         if self.variant == self.L.CFP_V_SEG:
             self.L.cfp_traceback_segments(self.sdesc, self.ws, plan=self.plan, stream=self.stream)
             return

@@ -298,11 +298,13 @@ hipError_t launch_chain_small(const cfp_chain_desc &d, int64_t *opt, int32_t *st
   for (int i = 1; i < d.n_blocks; ++i) a.redge[i] = (uint8_t)d.redge[i];
   const int kp = small_kp(d.k);
   const size_t lds = small_bytes(kp, d.n_blocks, d.n_tables);
+  timer_begin(st);
   switch (kp) {
-    case 16: hipLaunchKernelGGL(chain_small_kernel<16>, dim3(d.batch), dim3(kSmallThreads), lds, st, a); break;
-    case 32: hipLaunchKernelGGL(chain_small_kernel<32>, dim3(d.batch), dim3(kSmallThreads), lds, st, a); break;
-    default: hipLaunchKernelGGL(chain_small_kernel<64>, dim3(d.batch), dim3(kSmallThreads), lds, st, a); break;
+    case 16: timed_launch(chain_small_kernel<16>, dim3(d.batch), dim3(kSmallThreads), (uint32_t)lds, st, a); break;
+    case 32: timed_launch(chain_small_kernel<32>, dim3(d.batch), dim3(kSmallThreads), (uint32_t)lds, st, a); break;
+    default: timed_launch(chain_small_kernel<64>, dim3(d.batch), dim3(kSmallThreads), (uint32_t)lds, st, a); break;
   }
+  timer_end(st);
   return hipGetLastError();
 }
 
