@@ -39,7 +39,6 @@ Host-side analysis: no part of it runs on the GPU.
 """
 from __future__ import annotations
 
-import itertools
 from dataclasses import dataclass, field
 from typing import Dict, List, Optional, Sequence, Tuple
 
