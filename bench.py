@@ -40,6 +40,14 @@ PEAK_CELLS = VALU_LANE_OPS / INSTR_PER_CELL
 
 # The kernel that dominates the forward pass of each workload, and the source
 # files it is built from.
+# What the dominant kernel's figure covers, where it is not the whole forward call.
+KERNEL_ROLE = {
+    "chain_gpt_n24_k16": "the whole search (forward pass and traceback) in one launch",
+    "chain_gpt_n1152_k64": "speculative pass only; forward_call_frac covers the whole forward call",
+    "chain_wide_n512_k256": "speculative pass only; forward_call_frac covers the whole forward call",
+    "scan_n4096_k512:chain": "speculative pass only; forward_call_frac covers the whole forward call",
+    "scan_n4096_k512": "the 12 min-plus matrix-product launches of the up-sweep",
+}
 KERNELS = {
     # one launch of cfp_search_chain: forward pass and traceback
     "chain_gpt_n24_k16": ("chain_small_kernel<16>", ["chain_small.hip"]),
@@ -477,6 +485,7 @@ def measure(name: str, steps: int, warmup: int, cpu_s: float, frontier: bool = F
                      "frac": kern_cells_s / PEAK_CELLS,
                      "traffic": traffic_bytes(cfg.name, mode),
                      "kernel": kernel,
+                     "kernel_role": KERNEL_ROLE.get(cfg.name + ":chain" if chain else cfg.name, "the forward pass"),
                      "kernel_launches_per_step": kern_launches / steps,
                      "kernel_avg_us": kern_avg_ms * 1e3,
                      "forward_call_cells_per_s": fwd_cells_s,
