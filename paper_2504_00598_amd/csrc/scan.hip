@@ -356,6 +356,8 @@ struct DownArgs {
   int cnt, ccnt;
 };
 
+constexpr int kVmRows = 16;  // matrix rows in flight per thread in vecmat
+
 // v (x) M for one vector and one matrix (a block's transfer matrix when
 // the matrices are level 0); returns the minimum of the output in `mn` and
 // writes out - mn.  256 threads, KP/256 outputs each.
@@ -365,20 +367,52 @@ __device__ void vecmat(const uint32_t *v, int KP, int K, const uint32_t *Mm, uin
                        uint32_t *args_out, uint32_t *red) {
   const int tid = threadIdx.x;
   uint32_t best[2] = {kSat, kSat}, arg[2] = {0, 0};
-  for (int t = 0; t < KP; ++t) {
+  // Rows t are taken kVmRows at a time: every load of a batch is issued
+  // before any is used (one memory latency per batch rather than per row),
+  // from clamped addresses, so that no load sits behind a branch; entries of
+  // columns past KP (or past K for R) are never used.
+  const int c0 = tid, c1 = tid + 256;
+  auto take = [&](int t, uint32_t a0, uint32_t a1) __attribute__((always_inline)) {
     const uint32_t vt = umin(v[t], kBig);
+    const uint32_t x0 = vt + a0, x1 = vt + a1;  // both below 2^32
+    if (x0 < best[0]) {
+      best[0] = x0;
+      arg[0] = t;
+    }
+    if (x1 < best[1]) {
+      best[1] = x1;
+      arg[1] = t;
+    }
+  };
+  if (Mm) {
+    const uint32_t *p0 = Mm + min(c0, KP - 1), *p1 = Mm + min(c1, KP - 1);
+    for (int t0 = 0; t0 < KP; t0 += kVmRows) {
+      uint32_t m0[kVmRows], m1[kVmRows];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int s = tid + 256 * h;
-      if (s >= KP) continue;
-      uint32_t m;
-      if (Mm) m = umin(Mm[(size_t)t * KP + s] - mmn, kBig);
-      else if (block0) m = 0u;
-      else m = (t < K && s < K) ? (uint32_t)R[(size_t)t * K + s] : kBig;
-      const uint32_t x = vt + m;
-      if (x < best[h]) {
-        best[h] = x;
-        arg[h] = t;
+      for (int u = 0; u < kVmRows; ++u) {
+        m0[u] = p0[(size_t)(t0 + u) * KP];
+        m1[u] = p1[(size_t)(t0 + u) * KP];
+      }
+#pragma unroll
+      for (int u = 0; u < kVmRows; ++u) take(t0 + u, umin(m0[u] - mmn, kBig), umin(m1[u] - mmn, kBig));
+    }
+  } else if (block0) {
+    for (int t = 0; t < KP; ++t) take(t, 0u, 0u);
+  } else {
+    const int32_t *p0 = R + min(c0, K - 1), *p1 = R + min(c1, K - 1);
+    const bool k0 = c0 < K, k1 = c1 < K;
+    for (int t0 = 0; t0 < KP; t0 += kVmRows) {
+      uint32_t m0[kVmRows], m1[kVmRows];
+#pragma unroll
+      for (int u = 0; u < kVmRows; ++u) {
+        const size_t row = (size_t)min(t0 + u, K - 1) * K;
+        m0[u] = (uint32_t)p0[row];
+        m1[u] = (uint32_t)p1[row];
+      }
+#pragma unroll
+      for (int u = 0; u < kVmRows; ++u) {
+        const bool tin = t0 + u < K;
+        take(t0 + u, tin && k0 ? m0[u] : kBig, tin && k1 ? m1[u] : kBig);
       }
     }
   }
