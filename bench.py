@@ -59,7 +59,7 @@ KERNELS = {
     # the scan workload through the chain search: speculative pass of the chunk-parallel form
     "scan_n4096_k512:chain": ("chain_cw_kernel<512,0>", ["chain_cw.hip", "chain_fwd_wide.hip"]),
     "scan_n4096_k512": ("scan_gemm_kernel", ["scan.hip"]),
-    "seg_gpt_n96_k81": ("seg_fwd_kernel<2>", ["seg_fwd.hip"]),
+    "seg_gpt_n96_k81": ("seg_fwd_kernel<2, 4>", ["seg_fwd.hip"]),
 }
 COMMON_SOURCES = ["common.h", "cfp_internal.h", "../../include/cfp.h"]
 
