@@ -82,6 +82,18 @@ __device__ __forceinline__ uint32_t seg_wave_min(uint32_t x) {
   return seg_cross_rows(x);
 }
 
+// Minimum over the 64 lanes of a wave, as a scalar: the four row minima are
+// read independently and combined on the scalar unit.
+__device__ __forceinline__ uint32_t seg_wave_min_s(uint32_t x) {
+  x = min_dpp<kXor1>(x, x);
+  x = min_dpp<kXor2>(x, x);
+  x = min_dpp<kHalfMirror>(x, x);
+  x = min_dpp<kMirror>(x, x);
+  const uint32_t r0 = __builtin_amdgcn_readlane(x, 0), r1 = __builtin_amdgcn_readlane(x, 16);
+  const uint32_t r2 = __builtin_amdgcn_readlane(x, 32), r3 = __builtin_amdgcn_readlane(x, 48);
+  return umin(umin(r0, r1), umin(r2, r3));
+}
+
 }  // namespace
 
 // SPL states per lane (K <= 64 SPL); LM >= n_last, n_first is 4 or 8.  The
@@ -216,10 +228,14 @@ __global__ __launch_bounds__(kSegWaves * 64) void seg_fwd_kernel(
 #pragma unroll
     for (int j = 0; j < SPL; ++j) pk[j] = (q[j] << bits) | (uint32_t)(lane + 64 * j);
     auto part = [&](int cls) __attribute__((always_inline)) {
-      uint32_t x = kSat;
+      uint32_t x[SPL];
 #pragma unroll
-      for (int j = 0; j < SPL; ++j) x = ls[j] == cls ? umin(x, pk[j]) : x;
-      return x;
+      for (int j = 0; j < SPL; ++j) x[j] = ls[j] == cls ? pk[j] : kSat;
+#pragma unroll
+      for (int w = 1; w < SPL; w *= 2)  // a tree, not a chain
+#pragma unroll
+        for (int j = 0; j + w < SPL; j += 2 * w) x[j] = umin(x[j], x[j + w]);
+      return x[0];
     };
     // first exchange (lane ^ 1): keep the classes H b0 + m, send H (1 - b0) + m
     uint32_t A[H];
@@ -293,7 +309,7 @@ __global__ __launch_bounds__(kSegWaves * 64) void seg_fwd_kernel(
     rring[U] = load_r(__builtin_amdgcn_readfirstlane(ering[U]));
     ering[U] = load_e(edge_off(i + 2 * kSegAhead));
     load_row(row_off(i + kSegAhead), ring[U]);
-    const uint32_t rm = __builtin_amdgcn_readfirstlane(seg_wave_min(ym));
+    const uint32_t rm = seg_wave_min_s(ym);
     if (valid) {  // uniform; no memory operation below
       o += rm;
       rmax = max(rmax, rm);
