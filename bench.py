@@ -70,19 +70,19 @@ COMMON_SOURCES = ["common.h", "cfp_internal.h", "../../include/cfp.h"]
 # WRITE_SIZE reads 524288 KiB -> x1.000).  "sources" is sources_hash() of the
 # kernel when the counters were taken; a different hash means the kernel has
 # changed and the figure is withheld.
-FETCH_SCALE, WRITE_SCALE = 524288.0 / 262167.1, 524288.0 / 524288.0
+FETCH_SCALE, WRITE_SCALE = 524288.0 / 262166.9, 524288.0 / 524288.0
 TRAFFIC = {
     "chain_gpt_n24_k16": {"fetch_kib": 12.7, "write_kib": 0.2, "sources": "08c51b7710b5e094"},
-    "chain_gpt_n1152_k64": {"fetch_kib": 37972.6, "write_kib": 37516.1, "sources": "cec3c986f0b278db"},
-    "mem_llama_n288_k32": {"fetch_kib": 127642.5, "write_kib": 338789.9, "sources": "8819739b408e81c0"},
-    "chain_wide_n512_k256": {"fetch_kib": 44222.6, "write_kib": 16425.8, "sources": "c125e5f6d9988dd4"},
+    "chain_gpt_n1152_k64": {"fetch_kib": 37975.4, "write_kib": 37515.1, "sources": "b3609396e310cc0b"},
+    "mem_llama_n288_k32": {"fetch_kib": 127696.6, "write_kib": 338789.8, "sources": "b1c04725b6a0843d"},
+    "chain_wide_n512_k256": {"fetch_kib": 44184.9, "write_kib": 16425.8, "sources": "c125e5f6d9988dd4"},
     # mean over the 12 matrix-product launches of one forward call
-    "scan_n4096_k512": {"fetch_kib": 3035064.5, "write_kib": 1398442.5, "sources": "f9f8fcff938ec825"},
-    "seg_gpt_n96_k81": {"fetch_kib": 3922.9, "write_kib": 1936.0, "sources": "3cb0a9594fc4041e"},
+    "scan_n4096_k512": {"fetch_kib": 3033680.5, "write_kib": 1398442.5, "sources": "1c91451c813b5cea"},
+    "seg_gpt_n96_k81": {"fetch_kib": 3956.4, "write_kib": 1952.0, "sources": "c10bb791ae973515"},
     # the memory workload run as a budget frontier (every chunk of every search active)
-    "mem_llama_n288_k32:frontier": {"fetch_kib": 166635.1, "write_kib": 442222.7, "sources": "8819739b408e81c0"},
+    "mem_llama_n288_k32:frontier": {"fetch_kib": 166315.1, "write_kib": 442223.0, "sources": "b1c04725b6a0843d"},
     # the scan workload through the chain search (speculative pass)
-    "scan_n4096_k512:chain": {"fetch_kib": 801615.2, "write_kib": 25992.0, "sources": "c125e5f6d9988dd4"},
+    "scan_n4096_k512:chain": {"fetch_kib": 801691.1, "write_kib": 25992.0, "sources": "c125e5f6d9988dd4"},
 }
 
 

@@ -54,8 +54,11 @@ def test_config_full():
     assert_seg_parity(d["cost"], d["rbound"], d["last"], d["first"], d["redge"], "seg config")
 
 
+# K = S^P spans every kernel shape: states per lane 1, 2, 4, 8 (K up to 64, 128, 256, 512) with up to
+# 4 or up to 8 boundary strategies; N = 9 and 17 end one row into a group of 8 steps
 @pytest.mark.parametrize("N,P,S", [(1, 1, 2), (2, 1, 5), (5, 2, 3), (50, 4, 3), (30, 3, 4), (20, 5, 2), (40, 4, 4),
-                                   (10, 2, 8), (8, 3, 8), (70, 2, 7)])
+                                   (10, 2, 8), (8, 3, 8), (70, 2, 7), (25, 3, 6), (12, 9, 2), (9, 4, 3),
+                                   (17, 2, 3)])
 def test_shapes(N, P, S):
     need_gpu()
     say("seg shape", N, P, S)
@@ -103,6 +106,10 @@ def test_unavailable_and_statuses():
     bad_last = last.copy()
     bad_last[17] = 3
     _, st, _ = run_seg(cost[[0, 3]], rbound, bad_last, first, redge)
+    assert (st == CFP_ST_BADINPUT).all()
+    bad_first = first.copy()
+    bad_first[80] = 3
+    _, st, _ = run_seg(cost[[0, 3]], rbound, last, bad_first, redge)
     assert (st == CFP_ST_BADINPUT).all()
 
 
