@@ -67,3 +67,20 @@ def test_config_full():
     say("config scan_n4096_k512")
     d = configs.make("scan_n4096_k512")
     assert_scan_parity(d["cost"], d["rtab"], d["redge"], "scan config")
+
+
+def test_repeat_is_bit_identical():
+    """The product tree, down-sweep and traceback give the same optimum, status
+    and plan on every call (a fresh workspace each time), and the first call
+    matches the oracle."""
+    need_gpu()
+    say("scan repeat")
+    d = configs.make("scan_n4096_k512")
+    cost = np.ascontiguousarray(d["cost"][:2, :300])
+    redge = np.ascontiguousarray(d["redge"][:300])
+    assert_scan_parity(cost, d["rtab"], redge, "scan repeat, first call")
+    a = run_scan(cost, d["rtab"], redge)
+    for _ in range(3):
+        b = run_scan(cost, d["rtab"], redge)
+        for x, y in zip(a, b):
+            np.testing.assert_array_equal(x, y)
