@@ -47,6 +47,7 @@ KERNEL_ROLE = {
     "chain_wide_n512_k256": "speculative pass only; forward_call_frac covers the whole forward call",
     "scan_n4096_k512:chain": "speculative pass only; forward_call_frac covers the whole forward call",
     "scan_n4096_k512": "the 12 min-plus matrix-product launches of the up-sweep",
+    "seg_gpt_n96_k81": "the forward pass in one launch (speculative, fix-up and final passes of four chunks per search)",
 }
 KERNELS = {
     # one launch of cfp_search_chain: forward pass and traceback
@@ -59,7 +60,7 @@ KERNELS = {
     # the scan workload through the chain search: speculative pass of the chunk-parallel form
     "scan_n4096_k512:chain": ("chain_cw_kernel<512,0>", ["chain_cw.hip", "chain_fwd_wide.hip"]),
     "scan_n4096_k512": ("scan_gemm_kernel", ["scan.hip"]),
-    "seg_gpt_n96_k81": ("seg_fwd_kernel<2, 4>", ["seg_fwd.hip"]),
+    "seg_gpt_n96_k81": ("seg_chunk_kernel<2, 4>", ["seg_fwd.hip"]),
 }
 COMMON_SOURCES = ["common.h", "cfp_internal.h", "../../include/cfp.h"]
 

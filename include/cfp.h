@@ -222,7 +222,10 @@ typedef struct {
 size_t cfp_segment_workspace_bytes(const cfp_segment_desc *d);
 
 /* Forward segment search; opt/status as for cfp_dp_chain.  CFP_ERR_UNSUPPORTED
- * when K > CFP_MAX_K or L or F exceeds 8. */
+ * when K > CFP_MAX_K, L or F exceeds 8, or 8 N K exceeds 2^31 - 1 (device row
+ * offsets are 32-bit).  Batches too small to occupy the device run each chain
+ * as chunks made exact by rank convergence; the workspace then also holds the
+ * speculative rows (B N K 4 bytes, counted by cfp_segment_workspace_bytes). */
 int cfp_dp_segments(const cfp_segment_desc *d, void *ws, size_t ws_bytes, int64_t *opt, int32_t *status,
                     void *stream);
 

@@ -54,6 +54,10 @@ WsLayout layout(int variant, int n, int k, int batch, int n_mem, int n_tables) {
     L.cw = off;
     off = align_up(off + cw_region_bytes(n, k, n_tables, batch));
   }
+  if (variant == CFP_V_SEG) {
+    L.seg = off;
+    off = align_up(off + seg_region_bytes(n, k, batch));
+  }
   if (variant == CFP_V_SCAN) {
     L.scan = off;
     L.scan_bytes = scan_region_bytes(n, k, batch);
@@ -500,6 +504,7 @@ int check_seg(const cfp_segment_desc *d) {
   if (!d) return CFP_ERR_ARG;
   if (d->k > CFP_MAX_K || d->n_last > 8 || d->n_first > 8) return CFP_ERR_UNSUPPORTED;
   if (!seg_desc_ok(d) || d->n_last < 1 || d->n_first < 1) return CFP_ERR_ARG;
+  if ((size_t)d->n_segments * d->k * 8 > (size_t)INT32_MAX) return CFP_ERR_UNSUPPORTED;  // 32-bit row offsets
   for (int i = 1; i < d->n_segments; ++i)
     if (d->redge[i] < 0 || d->redge[i] >= d->n_tables) return CFP_ERR_RANGE;
   return CFP_OK;
@@ -542,8 +547,8 @@ int cfp_dp_segments(const cfp_segment_desc *d, void *ws, size_t ws_bytes, int64_
   if (launch_validate_range(d->rbound, (size_t)d->n_tables * d->n_last * d->n_first, cfp_r_limit(CFP_V_SEG, d->k),
                             hdr, st) != hipSuccess)
     return CFP_ERR_HIP;
-  if (launch_seg_fwd(*d, (const int32_t *)(w + L.redge), w + L.table, (SearchResult *)(w + L.result), hdr, opt,
-                     status, st) != hipSuccess)
+  if (launch_seg_fwd(*d, (const int32_t *)(w + L.redge), w + L.table, w + L.seg, (SearchResult *)(w + L.result), hdr,
+                     opt, status, st) != hipSuccess)
     return CFP_ERR_HIP;
   return CFP_OK;
 }

@@ -59,6 +59,7 @@ struct WsLayout {
   size_t split = 0;    // chain variant, K > 64: exchange slots and flags of the split kernel
   size_t wave = 0;     // chain variant, 32 < K <= 64 on long chains: packed tables, chunk records, checkpoints
   size_t cw = 0;       // chain variant, 128 < K <= 256 on long chains: packed tables, chunk records, checkpoints
+  size_t seg = 0;      // segment variant, small batches: speculative rows, running sums, chunk records
   size_t scan = 0;     // scan variant: start of its private region
   size_t scan_bytes = 0;
   size_t total = 0;
@@ -73,8 +74,10 @@ hipError_t launch_validate_rtab(const int32_t *rtab, int e, int k, int32_t limit
                                 hipStream_t st);
 hipError_t launch_validate_range(const int32_t *a, size_t count, int32_t limit, WsHeader *hdr, hipStream_t st);
 bool seg_supported(int k, int n_last, int n_first);
-hipError_t launch_seg_fwd(const cfp_segment_desc &d, const int32_t *redge_dev, uint8_t *table, SearchResult *res,
-                          const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st);
+// Segment search: region of the chunk-parallel form (0 when one pass suffices).
+size_t seg_region_bytes(int n, int k, int batch);
+hipError_t launch_seg_fwd(const cfp_segment_desc &d, const int32_t *redge_dev, uint8_t *table, uint8_t *region,
+                          SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st);
 hipError_t launch_chain_fwd(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *table, int elem,
                             uint8_t *wide, SearchResult *res, const WsHeader *hdr, int64_t *opt,
                             int32_t *status, hipStream_t st);

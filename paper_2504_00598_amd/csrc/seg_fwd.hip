@@ -12,11 +12,11 @@
 //     M_l     = min_{t : last(t) = l} D[i-1][t],
 // O(K + L F) work per step instead of O(K^2).
 //
-// One wave per search, four searches per workgroup, no barrier: lane x holds
-// the states x, x+64, ...  A row lives in registers as exact-normalised values
-// Q[s] = min(D[i][s] - min_s D[i][s], cap).  With one wave per SIMD at the
-// usual batch sizes a step costs what its instructions take to issue, so it is
-// built from lane exchanges only (DPP, permlane swaps), with no LDS:
+// One wave runs one search, or one chunk of one: lane x holds the states x,
+// x+64, ...  A row lives in registers as exact-normalised values
+// Q[s] = min(D[i][s] - min_s D[i][s], cap).  With one wave per SIMD a step
+// costs what its instructions take to issue, so it is built from lane
+// exchanges only (DPP, permlane swaps), with no LDS:
 //   1. class minima: the packed words (Q << b) | t are reduced over the wave
 //      per class by a reduce-scatter (each exchange halves the classes a lane
 //      keeps, until a lane keeps one), then by plain exchanges; a minimum
@@ -34,6 +34,29 @@
 // entries come from rings of kSegAhead rows in registers, loaded that many
 // steps ahead (the edge indices twice as far), so the wait for a row's data
 // never covers the loads and argmin stores of the steps since.
+//
+// Parallelism over the chain.  A batch too small to give every SIMD a wave
+// cuts each chain into P chunks that run at once, made exact by rank
+// convergence (Maleki, Musuvathi and Mytkowicz, PPoPP 2014), as the chunked
+// chain searches do; with only L F boundary pairs between segments the rows
+// of a run become parallel to the true ones within a few steps.  One
+// workgroup per search, wave p for chunk p, the passes separated by barriers:
+//   1. speculative pass: chunk p starts at its first row from that row's
+//      costs alone, writes its argmin rows and every normalised row with the
+//      running sum of its row minima;
+//   2. fix-up pass, chunks p >= 1: start again from the last speculative row
+//      of chunk p-1 and recompute until the row equals chunk p's speculative
+//      row of the same step (from there on every speculative row is the one
+//      the true start gives), rewriting the argmins on the way;
+//   3. final pass, wave 0: sums the chunks' row minima.  When a
+//      chunk's fix-up met no speculative row, its end row is the true one but
+//      the next chunk's fix-up started from a wrong row: that chunk is rerun
+//      from the true row, at least as far as its fix-up went and then until
+//      its row meets the speculative one (or to its end, and the next chunk
+//      is rerun in turn).
+// The result is the sequential recurrence's bit for bit for every input.
+#include <algorithm>
+
 #include "cfp_internal.h"
 #include "common.h"
 
@@ -41,9 +64,12 @@ namespace cfp {
 
 namespace {
 
-constexpr int kSegWaves = 4;  // searches per workgroup
-constexpr int kSegMaxLF = 8;  // largest number of strategies of a boundary block
-constexpr int kSegAhead = 8;  // rows in flight per lane
+constexpr int kSegWaves = 4;     // waves (searches or chunks) per workgroup
+constexpr int kSegMaxLF = 8;     // largest number of strategies of a boundary block
+constexpr int kSegAhead = 8;     // rows in flight per lane
+constexpr int kSegMaxP = 8;      // chunks per search (waves of a workgroup)
+constexpr int kSegMinRows = 16;  // least rows per chunk
+constexpr int kSegSimds = 1024;  // SIMDs of the chip: waves at one per SIMD
 
 // DPP controls: quad_perm [1,0,3,2] and [2,3,0,1] (lane ^ 1, lane ^ 2),
 // row_ror:4 and :8, row_half_mirror, row_mirror, row_newbcast:n.
@@ -67,12 +93,6 @@ __device__ __forceinline__ uint32_t seg_cross_rows(uint32_t x) {
   return umin(r[0], r[1]);
 }
 
-// Raw buffer resource over [base, base + bytes): loads beyond it read 0 and
-// stores beyond it are dropped (32-bit data format, no swizzle).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
-}
-
 // Minimum over the 64 lanes of a wave; every lane gets it.
 __device__ __forceinline__ uint32_t seg_wave_min(uint32_t x) {
   x = min_dpp<kXor1>(x, x);
@@ -94,41 +114,78 @@ __device__ __forceinline__ uint32_t seg_wave_min_s(uint32_t x) {
   return umin(umin(r0, r1), umin(r2, r3));
 }
 
+// Raw buffer resource over [base, base + bytes): loads beyond it read 0 and
+// stores beyond it are dropped (32-bit data format, no swizzle).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+constexpr uint32_t kOob = 0x80000000u;  // a lane offset past every resource (its access is dropped)
+
+enum { kSegFull = 0, kSegSpec = 1, kSegFix = 2, kSegRepair = 3 };
+
+struct SegRec {
+  int64_t dfix;   // fix-up: sum of the row minima of its rows (to the meeting row or the chunk end)
+  int32_t conv;   // fix-up: meeting row, -1 if none
+  int32_t flags;  // speculative pass: bit 0 bad input, bit 1 a row with no available strategy
+};
+
+struct SegArgs {
+  const int32_t *cost;    // [B][N][K]
+  const int32_t *rbound;  // [E][L][F]
+  const uint8_t *last, *first;
+  const int32_t *redge;   // device copy, entry 0 a valid table
+  int N, K, B, L, F, bits;
+  uint8_t *table;         // argmin entries [B][N][K], u8 or u16 (K > 256)
+  // chunk-parallel form
+  int P, CL;              // chunks per search, rows per chunk
+  uint32_t *ckrow;        // speculative normalised rows [B][N][K]
+  int64_t *dck;           // speculative running sum of row minima from the chunk's first row [B][N]
+  SegRec *rec;            // [B][P]
+  uint32_t *endrow;       // fix-up end rows of chunks that met no speculative row [B][P][K]
+};
+
 }  // namespace
 
-// SPL states per lane (K <= 64 SPL); LM >= n_last, n_first is 4 or 8.  The
-// argmin entries are 16-bit exactly when K > 256, i.e. SPL = 8.
+// One run of the recurrence for search b over rows [r0, r1), in one wave.
+//   kSegFull, kSegSpec: row r0 from its costs alone (its row minimum counts);
+//     kSegSpec stores every normalised row and the running sum of minima.
+//   kSegFix, kSegRepair: qs is the normalised row r0 - 1; rows r0 .. are
+//     computed and compared with the speculative rows; the run stops at the
+//     first row i >= lim that equals it (stop = i), else at r1 - 1 (stop = -1).
+// Every computed row's argmins are stored (row r0 has none in kSegFull and
+// kSegSpec).  o is the sum of the computed rows' minima, rmax the largest of
+// them (kSat when a row has no available strategy); q ends as the last
+// computed row; bad flags a negative cost or a boundary map out of range.
 //
-// Class of a lane after the reduce-scatter (bits b0, b1, b2 of the lane):
-// LM = 4: 2 b0 + b1; LM = 8: 4 b0 + 2 b1 + b2.  Boundary pair (l, f) sits in
-// the lanes of class l in group f: LM = 4, groups of 4 lanes, f = (lane / 4) %
-// 4 (every row holds all pairs); LM = 8, groups of 8 lanes, f = lane / 8.
-template <int SPL, int LM>
-__global__ __launch_bounds__(kSegWaves * 64) void seg_fwd_kernel(
-    const int32_t *__restrict__ cost, const int32_t *__restrict__ rbound, const uint8_t *__restrict__ last,
-    const uint8_t *__restrict__ first, const int32_t *__restrict__ redge, int N, int K, int B, int L, int F,
-    int bits, uint8_t *__restrict__ table, SearchResult *__restrict__ res, const WsHeader *__restrict__ hdr,
-    int64_t *__restrict__ opt, int32_t *__restrict__ status) {
+// SPL states per lane (K <= 64 SPL); LM >= n_last, n_first is 4 or 8.  The
+// argmin entries are 16-bit exactly when K > 256, i.e. SPL = 8.  Class of a
+// lane after the reduce-scatter (bits b0, b1, b2 of the lane): LM = 4:
+// 2 b0 + b1; LM = 8: 4 b0 + 2 b1 + b2.  Boundary pair (l, f) sits in the lanes
+// of class l in group f: LM = 4, groups of 4 lanes, f = (lane / 4) % 4 (every
+// row holds all pairs); LM = 8, groups of 8 lanes, f = lane / 8.
+template <int SPL, int LM, int MODE>
+__device__ __forceinline__ void seg_run(const SegArgs &a, int b, int r0, int r1, int lim, const uint32_t (&qs)[SPL],
+                                        uint32_t (&q)[SPL], int64_t &o, uint32_t &rmax, int &stop, bool &bad) {
   static_assert(LM == 4 || LM == 8, "classes per boundary side");
   constexpr bool kWide = SPL == 8;
+  constexpr bool kFromCost = MODE == kSegFull || MODE == kSegSpec;
+  constexpr bool kCompare = MODE == kSegFix || MODE == kSegRepair;
   constexpr int H = LM / 2;  // classes a lane keeps after the first exchange
-  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-  const int b = blockIdx.x * kSegWaves + wid;
-  if (b >= B) return;  // the waves are independent: nothing below waits for another wave
-  const uint32_t CAP = (1u << (32 - bits)) - 1u, IMASK = (1u << bits) - 1u;
-  const int32_t *cb = cost + (size_t)b * N * K;
+  const int lane = threadIdx.x & 63;
+  const int N = a.N, K = a.K, L = a.L, F = a.F, bits = a.bits;
+  const uint32_t CAP = (1u << (32 - bits)) - 1u;
   const int b0 = lane & 1, b1 = (lane >> 1) & 1, b2 = (lane >> 2) & 1;
 
   int ls[SPL], fs[SPL];
   bool real[SPL];
-  uint32_t q[SPL];
-  bool bad = false;
+  bad = false;
 #pragma unroll
   for (int j = 0; j < SPL; ++j) {
     const int s = lane + 64 * j;
     real[j] = s < K;
-    ls[j] = real[j] ? last[s] : 0;
-    fs[j] = real[j] ? first[s] : 0;
+    ls[j] = real[j] ? a.last[s] : 0;
+    fs[j] = real[j] ? a.first[s] : 0;
     bad |= real[j] && (ls[j] >= L || fs[j] >= F);
     if (ls[j] >= L) ls[j] = 0;  // keep the selects in range; the search reports bad input
     if (fs[j] >= F) fs[j] = 0;
@@ -138,14 +195,22 @@ __global__ __launch_bounds__(kSegWaves * 64) void seg_fwd_kernel(
 
   // Memory goes through buffer resources: a scalar row offset plus a fixed
   // lane offset, so a step spends no vector instructions on addresses.  The
-  // host keeps N K 4 below 2^31.
+  // host keeps N K 8 below 2^31.
+  const size_t cells = (size_t)N * K;
   const uint32_t K4 = (uint32_t)K * 4u, last_row = (uint32_t)(N - 1) * K4;
-  const __amdgpu_buffer_rsrc_t crs = make_rsrc(cb, (uint32_t)N * K4);
-  const __amdgpu_buffer_rsrc_t rrs = make_rsrc(rbound, 0x7FFFFFFFu);  // offsets come from checked edges
-  const __amdgpu_buffer_rsrc_t ers = make_rsrc(redge, (uint32_t)N * 4u);
+  const __amdgpu_buffer_rsrc_t crs = make_rsrc(a.cost + (size_t)b * cells, (uint32_t)N * K4);
+  const __amdgpu_buffer_rsrc_t rrs = make_rsrc(a.rbound, 0x7FFFFFFFu);  // offsets come from checked edges
+  const __amdgpu_buffer_rsrc_t ers = make_rsrc(a.redge, (uint32_t)N * 4u);
+  // speculative rows (stored by kSegSpec, compared by kSegFix and kSegRepair) and running sums
+  const uint32_t *ckb = kFromCost && MODE != kSegSpec ? nullptr : a.ckrow + (size_t)b * cells;
+  const __amdgpu_buffer_rsrc_t krs = make_rsrc(ckb, ckb ? (uint32_t)N * K4 : 0u);
+  const int64_t *dkb = MODE == kSegSpec ? a.dck + (size_t)b * N : nullptr;
+  const __amdgpu_buffer_rsrc_t drs = make_rsrc(dkb, dkb ? (uint32_t)N * 8u : 0u);
 
-  // Ring of cost rows: row i >= 1 sits in slot (i - 1) % kSegAhead.
+  // Rings: row i sits in slot (i - f0) % kSegAhead, f0 the first computed row.
+  const int f0 = kFromCost ? r0 + 1 : r0;
   int32_t ring[kSegAhead][SPL];
+  uint32_t kring[kCompare ? kSegAhead : 1][SPL];
   uint32_t coff[SPL];  // byte offset of a lane's states within a row
 #pragma unroll
   for (int j = 0; j < SPL; ++j) coff[j] = (real[j] ? (uint32_t)(lane + 64 * j) : sl) * 4u;
@@ -153,8 +218,11 @@ __global__ __launch_bounds__(kSegWaves * 64) void seg_fwd_kernel(
 #pragma unroll
     for (int j = 0; j < SPL; ++j) dst[j] = __builtin_amdgcn_raw_buffer_load_b32(crs, (int)coff[j], (int)roff, 0);
   };
-  int32_t c0[SPL];
-  load_row(0, c0);
+  auto load_ck = [&](uint32_t roff, uint32_t(&dst)[SPL]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < SPL; ++j)
+      dst[j] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(krs, (int)coff[j], (int)roff, 0);
+  };
 
   // Boundary lanes and the ring of their entries r_{e(i)}[l][f]; the edge
   // index of a row is read kSegAhead steps before its entries, into a ring of
@@ -173,56 +241,92 @@ __global__ __launch_bounds__(kSegWaves * 64) void seg_fwd_kernel(
   auto row_off = [&](int i) __attribute__((always_inline)) { return min((uint32_t)i * K4, last_row); };
   auto edge_off = [&](int i) __attribute__((always_inline)) { return (uint32_t)min(i, N - 1) * 4u; };
   uint32_t rring[kSegAhead], ering[kSegAhead];
+  int32_t c0[SPL];
+  if constexpr (kFromCost) load_row(row_off(r0), c0);
 #pragma unroll
-  for (int u = 0; u < kSegAhead; ++u) {  // in the order the steps issue them
-    rring[u] = load_r(__builtin_amdgcn_readfirstlane(load_e(edge_off(1 + u))));
-    ering[u] = load_e(edge_off(1 + u + kSegAhead));
-    load_row(row_off(1 + u), ring[u]);
+  for (int u = 0; u < kSegAhead; ++u) {
+    rring[u] = load_r(__builtin_amdgcn_readfirstlane(load_e(edge_off(f0 + u))));
+    ering[u] = load_e(edge_off(f0 + u + kSegAhead));
+    load_row(row_off(f0 + u), ring[u]);
+    if constexpr (kCompare) load_ck(row_off(f0 + u), kring[u]);
   }
 
-  // Row 0.
-  uint32_t ym = kSat;
+  // Speculative rows and running sums: a lane without a state, and every lane
+  // in a step past the run's end, stores out of range (dropped).
+  uint32_t ckoff[SPL];
 #pragma unroll
-  for (int j = 0; j < SPL; ++j) {
-    const int32_t c = c0[j];
-    bad |= real[j] && c < 0;
-    const uint32_t y = !real[j] || c == CFP_COST_INF ? kSat : (uint32_t)c;
-    q[j] = y;
-    ym = umin(ym, y);
+  for (int j = 0; j < SPL; ++j) ckoff[j] = real[j] ? (uint32_t)(lane + 64 * j) * 4u : kOob;
+  const uint32_t doff = lane == 0 ? 0u : kOob;
+  auto store_spec = [&](int i, bool valid) __attribute__((always_inline)) {
+    if constexpr (MODE == kSegSpec) {
+      const uint32_t roff = valid ? (uint32_t)i * K4 : kOob;
+#pragma unroll
+      for (int j = 0; j < SPL; ++j) __builtin_amdgcn_raw_buffer_store_b32(q[j], krs, (int)(ckoff[j] + roff), 0, 0);
+      const uint32_t droff = valid ? (uint32_t)i * 8u : kOob;
+      typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+      const u32x2 ov = {(uint32_t)(uint64_t)o, (uint32_t)((uint64_t)o >> 32)};
+      __builtin_amdgcn_raw_buffer_store_b64(ov, drs, (int)(doff + droff), 0, 0);
+    }
+  };
+
+  // The start row.
+  if constexpr (kFromCost) {
+    uint32_t ym = kSat;
+#pragma unroll
+    for (int j = 0; j < SPL; ++j) {
+      const int32_t c = c0[j];
+      bad |= real[j] && c < 0;
+      const uint32_t y = !real[j] || c == CFP_COST_INF ? kSat : (uint32_t)c;
+      q[j] = y;
+      ym = umin(ym, y);
+    }
+    const uint32_t rmin = __builtin_amdgcn_readfirstlane(seg_wave_min(ym));
+    o = rmin;
+    rmax = rmin;
+#pragma unroll
+    for (int j = 0; j < SPL; ++j) q[j] = umin(q[j] - rmin, CAP);
+    store_spec(r0, true);
+  } else {
+#pragma unroll
+    for (int j = 0; j < SPL; ++j) q[j] = qs[j];
+    o = 0;
+    rmax = 0;
   }
-  uint32_t rmin = __builtin_amdgcn_readfirstlane(seg_wave_min(ym));
-  int64_t o = rmin;
-  uint32_t rmax = rmin;  // kSat once a row has no reachable state
-#pragma unroll
-  for (int j = 0; j < SPL; ++j) q[j] = umin(q[j] - rmin, CAP);
+  stop = -1;
+  bool done = false;
 
   uint32_t neg = 0;  // OR of the costs read: the sign bit flags a negative one
 
-  // Wait here for every load above (once per search): the waits in the loop
-  // then count only the loads the loop itself issued, several steps back
-  // (the compiler orders the loads above by kind, not by slot).
+  // Wait here for every load above (once per run): the waits in the loop then
+  // count only the loads the loop itself issued, several steps back (the
+  // compiler orders the loads above by kind, not by slot).
 #pragma unroll
   for (int u = 0; u < kSegAhead; ++u) {
     asm volatile("" ::"v"(rring[u]), "v"(ering[u]));
 #pragma unroll
     for (int j = 0; j < SPL; ++j) asm volatile("" ::"v"(ring[u][j]));
+    if constexpr (kCompare) {
+#pragma unroll
+      for (int j = 0; j < SPL; ++j) asm volatile("" ::"v"(kring[u][j]));
+    }
   }
 
   // Argmin cells of this search: a lane without a state stores out of the
-  // resource's range (dropped); in the steps past the last row every lane
-  // stores into row 0, which is never read back.  So every step issues the
-  // same loads and stores, with no branch between them.
+  // resource's range (dropped); in a step past the run's end every lane stores
+  // into row 0, which is never read back.  So every step issues the same loads
+  // and stores, with no branch between them.
   constexpr uint32_t kElem = kWide ? 2u : 1u;
-  const __amdgpu_buffer_rsrc_t trs = make_rsrc(table + (size_t)b * N * K * kElem, (uint32_t)N * K * kElem);
+  const __amdgpu_buffer_rsrc_t trs = make_rsrc(a.table + (size_t)b * cells * kElem, (uint32_t)N * K * kElem);
   uint32_t toff[SPL];
 #pragma unroll
-  for (int j = 0; j < SPL; ++j) toff[j] = real[j] ? (uint32_t)(lane + 64 * j) * kElem : 0x80000000u;
+  for (int j = 0; j < SPL; ++j) toff[j] = real[j] ? (uint32_t)(lane + 64 * j) * kElem : kOob;
 
-  // The step of row i, with its data in ring slot U = (i - 1) % kSegAhead.
-  // Steps with i >= N (the padding of the last group) change no state.
+  // The step of row i, with its data in ring slot U = (i - f0) % kSegAhead.
+  // A step past the run's end (the padding of the last group, or after the
+  // run has met the speculative row) changes no state.
   auto step = [&](int i, auto Uc) __attribute__((always_inline)) {
     constexpr int U = decltype(Uc)::value;
-    const bool valid = i < N;
+    const bool valid = i < r1 && !done;
     // 1. class minima of the previous row
     uint32_t pk[SPL];
 #pragma unroll
@@ -288,7 +392,7 @@ __global__ __launch_bounds__(kSegWaves * 64) void seg_fwd_kernel(
     // 3. the new row; the low bits of an argmin entry are the predecessor
     // (the bits above it are not read back)
     const uint32_t trow = valid ? (uint32_t)i * (uint32_t)K * kElem : 0u;
-    ym = kSat;
+    uint32_t ym = kSat;
     uint32_t yn[SPL];
 #pragma unroll
     for (int j = 0; j < SPL; ++j) {
@@ -316,9 +420,22 @@ __global__ __launch_bounds__(kSegWaves * 64) void seg_fwd_kernel(
 #pragma unroll
       for (int j = 0; j < SPL; ++j) q[j] = umin(yn[j] - rm, CAP);
     }
+    store_spec(i, valid);
+    if constexpr (kCompare) {
+      bool diff = false;
+#pragma unroll
+      for (int j = 0; j < SPL; ++j) diff |= real[j] && q[j] != kring[U][j];
+      if (valid && i >= lim && __ballot(diff) == 0) {  // uniform
+        stop = i;
+        done = true;
+      }
+      // the speculative row i + kSegAhead, into the registers just compared
+      __builtin_amdgcn_sched_barrier(0);
+      load_ck(row_off(i + kSegAhead), kring[U]);
+    }
   };
   // rows in groups of kSegAhead so that every ring slot is a constant
-  for (int i0 = 1; i0 < N; i0 += kSegAhead) {
+  for (int i0 = f0; i0 < r1 && !done; i0 += kSegAhead) {
     step(i0 + 0, std::integral_constant<int, 0>{});
     step(i0 + 1, std::integral_constant<int, 1>{});
     step(i0 + 2, std::integral_constant<int, 2>{});
@@ -329,55 +446,249 @@ __global__ __launch_bounds__(kSegWaves * 64) void seg_fwd_kernel(
     step(i0 + 7, std::integral_constant<int, 7>{});
   }
   static_assert(kSegAhead == 8, "the group above has kSegAhead steps");
+  bad = bad || (int32_t)neg < 0;
+}
 
+// Status and outputs of search b from its last normalised row (lane 0 writes).
+template <int SPL>
+__device__ __forceinline__ void seg_finish(const SegArgs &a, int b, const uint32_t (&q)[SPL], int64_t o, bool bad,
+                                           bool infeasible, SearchResult *__restrict__ res,
+                                           const WsHeader *__restrict__ hdr, int64_t *__restrict__ opt,
+                                           int32_t *__restrict__ status) {
+  const int lane = threadIdx.x & 63;
+  const uint32_t IMASK = (1u << a.bits) - 1u;
   // Lowest final state of least value (the least is 0 after normalisation).
   uint32_t pk = kSat;
 #pragma unroll
   for (int j = 0; j < SPL; ++j)
-    if (real[j]) pk = umin(pk, (q[j] << bits) | (uint32_t)(lane + 64 * j));
+    if (lane + 64 * j < a.K) pk = umin(pk, (q[j] << a.bits) | (uint32_t)(lane + 64 * j));
   const uint32_t fin = __builtin_amdgcn_readfirstlane(seg_wave_min(pk));
-  const bool infeasible = rmax == kSat;
-  bad = __any(bad || (int32_t)neg < 0);
+  bad = __any(bad);
   if (lane == 0) {
     int st = CFP_ST_OK;
     if (bad || hdr->rflag) st = CFP_ST_BADINPUT;
     else if (infeasible) st = CFP_ST_INFEASIBLE;
-    else if ((fin >> bits) != 0) st = CFP_ST_OVERFLOW;
+    else if ((fin >> a.bits) != 0) st = CFP_ST_OVERFLOW;
     status[b] = st;
-    opt[b] = st == CFP_ST_OK ? o + (int64_t)(fin >> bits) : INT64_MAX;
+    opt[b] = st == CFP_ST_OK ? o + (int64_t)(fin >> a.bits) : INT64_MAX;
     res[b].final_state = st == CFP_ST_OK ? (int32_t)(fin & IMASK) : -1;
     res[b].status = st;
     res[b].final_m = 0;
   }
 }
 
+// Whole searches, one wave each.
+template <int SPL, int LM>
+__global__ __launch_bounds__(kSegWaves * 64) void seg_fwd_kernel(SegArgs a, SearchResult *__restrict__ res,
+                                                                 const WsHeader *__restrict__ hdr,
+                                                                 int64_t *__restrict__ opt,
+                                                                 int32_t *__restrict__ status) {
+  const int b = blockIdx.x * kSegWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (b >= a.B) return;  // the waves are independent: nothing below waits for another wave
+  uint32_t q[SPL];
+  int64_t o;
+  uint32_t rmax;
+  int stop;
+  bool bad;
+  seg_run<SPL, LM, kSegFull>(a, b, 0, a.N, 0, q, q, o, rmax, stop, bad);
+  seg_finish<SPL>(a, b, q, o, bad, rmax == kSat, res, hdr, opt, status);
+}
+
+// The final pass of search b (see the top of the file): the chunks' sums of
+// row minima, the reruns a chunk whose predecessor met no speculative row
+// needs, and the outputs.
+template <int SPL, int LM>
+__device__ __forceinline__ void seg_final(const SegArgs &a, int b, SearchResult *__restrict__ res,
+                                          const WsHeader *__restrict__ hdr, int64_t *__restrict__ opt,
+                                          int32_t *__restrict__ status) {
+  const int lane = threadIdx.x & 63;
+  const int N = a.N, K = a.K, P = a.P, CL = a.CL;
+  const SegRec *rc = a.rec + (size_t)b * P;
+  const int64_t *dk = a.dck + (size_t)b * N;
+  int fl = 0;
+  for (int p = 0; p < P; ++p) fl |= rc[p].flags;
+  int64_t total = dk[min(CL, N) - 1];  // chunk 0 started at the true first row
+  bool end_true = true;                // the last speculative row of the previous chunk is the true one
+  uint32_t t[SPL];                     // otherwise the true end row of the previous chunk
+#pragma unroll
+  for (int j = 0; j < SPL; ++j) t[j] = 0;
+  for (int p = 1; p < P; ++p) {
+    const int r0 = p * CL, r1 = min(r0 + CL, N);
+    const int conv = rc[p].conv;
+    if (end_true) {  // the fix-up of chunk p started from the true row
+      total += rc[p].dfix;
+      if (conv >= 0) {
+        total += dk[r1 - 1] - dk[conv];
+      } else {
+        end_true = false;
+        const uint32_t *er = a.endrow + ((size_t)b * P + p) * K;
+#pragma unroll
+        for (int j = 0; j < SPL; ++j) t[j] = er[min(lane + 64 * j, K - 1)];
+      }
+    } else {  // rerun chunk p from the true row, at least as far as its fix-up went
+      uint32_t q[SPL];
+      int64_t o;
+      uint32_t rmax;
+      int stop;
+      bool bad;
+      seg_run<SPL, LM, kSegRepair>(a, b, r0, r1, conv >= 0 ? conv : r1 - 1, t, q, o, rmax, stop, bad);
+      total += o;
+      if (stop >= 0) {
+        total += dk[r1 - 1] - dk[stop];
+        end_true = true;
+      } else {
+#pragma unroll
+        for (int j = 0; j < SPL; ++j) t[j] = q[j];
+      }
+    }
+  }
+  uint32_t q[SPL];
+  if (end_true) {
+    const uint32_t *lr = a.ckrow + ((size_t)b * N + N - 1) * K;
+#pragma unroll
+    for (int j = 0; j < SPL; ++j) q[j] = lr[min(lane + 64 * j, K - 1)];
+  } else {
+#pragma unroll
+    for (int j = 0; j < SPL; ++j) q[j] = t[j];
+  }
+  seg_finish<SPL>(a, b, q, total, (fl & 1) != 0, (fl & 2) != 0, res, hdr, opt, status);
+}
+
+// The chunk-parallel search in one launch: one workgroup per search, wave p
+// for chunk p.  The passes are separated by workgroup barriers (the waves of
+// a workgroup share a compute unit, so a barrier also orders their global
+// stores and loads): every wave runs its chunk speculatively, waves 1..P-1
+// then fix up their chunks, and wave 0 runs the final pass.
+template <int SPL, int LM>
+__global__ __launch_bounds__(64 * kSegMaxP) void seg_chunk_kernel(SegArgs a, SearchResult *__restrict__ res,
+                                                                  const WsHeader *__restrict__ hdr,
+                                                                  int64_t *__restrict__ opt,
+                                                                  int32_t *__restrict__ status) {
+  const int b = blockIdx.x, p = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int P = a.P, lane = threadIdx.x & 63;
+  const int r0 = p * a.CL, r1 = min(r0 + a.CL, a.N);
+  {  // 1. speculative run of chunk p
+    uint32_t q[SPL];
+    int64_t o;
+    uint32_t rmax;
+    int stop;
+    bool bad;
+    seg_run<SPL, LM, kSegSpec>(a, b, r0, r1, 0, q, q, o, rmax, stop, bad);
+    bad = __any(bad);
+    if (lane == 0) a.rec[(size_t)b * P + p].flags = (bad ? 1 : 0) | (rmax == kSat ? 2 : 0);
+  }
+  __syncthreads();
+  if (p >= 1) {  // 2. fix-up of chunk p from the last speculative row of chunk p-1
+    const uint32_t *prev = a.ckrow + ((size_t)b * a.N + r0 - 1) * a.K;
+    uint32_t qs[SPL];
+#pragma unroll
+    for (int x = 0; x < SPL; ++x) qs[x] = prev[min(lane + 64 * x, a.K - 1)];
+    uint32_t q[SPL];
+    int64_t o;
+    uint32_t rmax;
+    int stop;
+    bool bad;
+    seg_run<SPL, LM, kSegFix>(a, b, r0, r1, r0, qs, q, o, rmax, stop, bad);
+    const size_t ri = (size_t)b * P + p;
+    if (stop < 0) {
+      uint32_t *er = a.endrow + ri * a.K;
+#pragma unroll
+      for (int x = 0; x < SPL; ++x)
+        if (lane + 64 * x < a.K) er[lane + 64 * x] = q[x];
+    }
+    if (lane == 0) {
+      a.rec[ri].conv = stop;
+      a.rec[ri].dfix = o;
+    }
+  }
+  __syncthreads();
+  if (p == 0) seg_final<SPL, LM>(a, b, res, hdr, opt, status);  // 3. final pass
+}
+
 bool seg_supported(int k, int n_last, int n_first) {
   return k >= 1 && k <= CFP_MAX_K && n_last >= 1 && n_last <= kSegMaxLF && n_first >= 1 && n_first <= kSegMaxLF;
 }
 
+namespace {
+
+// Chunks per search: enough waves for one per SIMD, chunks of at least
+// kSegMinRows rows; P = 1 means the one-pass kernel.
+struct SegPlan {
+  int P, CL;
+};
+
+SegPlan seg_plan(int n, int batch) {
+  int P = std::min(kSegMaxP, std::max(1, kSegSimds / std::max(1, batch)));
+  P = std::min(P, n / kSegMinRows);
+  if (P < 2) return SegPlan{1, n};
+  const int CL = (n + P - 1) / P;
+  return SegPlan{(n + CL - 1) / CL, CL};
+}
+
 template <int SPL, int LM>
-static void launch_seg_spl(const cfp_segment_desc &d, const int32_t *redge_dev, uint8_t *table, SearchResult *res,
-                           const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st) {
-  const int grid = (d.batch + kSegWaves - 1) / kSegWaves;
-  timed_launch(seg_fwd_kernel<SPL, LM>, dim3(grid), dim3(kSegWaves * 64), 0, st, d.cost, d.rbound, d.last,
-               d.first, redge_dev, d.n_segments, d.k, d.batch, d.n_last, d.n_first, index_bits(d.k), table, res,
-               hdr, opt, status);
+void launch_seg_spl(const SegArgs &a, SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
+                    hipStream_t st) {
+  const dim3 blk(kSegWaves * 64);
+  auto grid = [](long waves) { return dim3((unsigned)((waves + kSegWaves - 1) / kSegWaves)); };
+  if (a.P < 2) {
+    timed_launch(seg_fwd_kernel<SPL, LM>, grid(a.B), blk, 0, st, a, res, hdr, opt, status);
+    return;
+  }
+  timed_launch(seg_chunk_kernel<SPL, LM>, dim3(a.B), dim3(64 * a.P), 0, st, a, res, hdr, opt, status);
 }
 
 template <int LM>
-static void launch_seg_lm(const cfp_segment_desc &d, const int32_t *redge_dev, uint8_t *table, SearchResult *res,
-                          const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st) {
-  if (d.k <= 64) launch_seg_spl<1, LM>(d, redge_dev, table, res, hdr, opt, status, st);
-  else if (d.k <= 128) launch_seg_spl<2, LM>(d, redge_dev, table, res, hdr, opt, status, st);
-  else if (d.k <= 256) launch_seg_spl<4, LM>(d, redge_dev, table, res, hdr, opt, status, st);
-  else launch_seg_spl<8, LM>(d, redge_dev, table, res, hdr, opt, status, st);
+void launch_seg_lm(const SegArgs &a, SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
+                   hipStream_t st) {
+  if (a.K <= 64) launch_seg_spl<1, LM>(a, res, hdr, opt, status, st);
+  else if (a.K <= 128) launch_seg_spl<2, LM>(a, res, hdr, opt, status, st);
+  else if (a.K <= 256) launch_seg_spl<4, LM>(a, res, hdr, opt, status, st);
+  else launch_seg_spl<8, LM>(a, res, hdr, opt, status, st);
 }
 
-hipError_t launch_seg_fwd(const cfp_segment_desc &d, const int32_t *redge_dev, uint8_t *table, SearchResult *res,
-                          const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st) {
+}  // namespace
+
+size_t seg_region_bytes(int n, int k, int batch) {
+  const SegPlan c = seg_plan(n, batch);
+  if (c.P < 2) return 0;
+  size_t off = align_up((size_t)batch * n * k * 4);           // speculative rows
+  off += align_up((size_t)batch * n * 8);                     // running sums
+  off += align_up((size_t)batch * c.P * sizeof(SegRec));      // chunk records
+  off += align_up((size_t)batch * c.P * k * 4);               // fix-up end rows
+  return off;
+}
+
+hipError_t launch_seg_fwd(const cfp_segment_desc &d, const int32_t *redge_dev, uint8_t *table, uint8_t *region,
+                          SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st) {
+  SegArgs a{};
+  a.cost = d.cost;
+  a.rbound = d.rbound;
+  a.last = d.last;
+  a.first = d.first;
+  a.redge = redge_dev;
+  a.N = d.n_segments;
+  a.K = d.k;
+  a.B = d.batch;
+  a.L = d.n_last;
+  a.F = d.n_first;
+  a.bits = index_bits(d.k);
+  a.table = table;
+  const SegPlan c = seg_plan(d.n_segments, d.batch);
+  a.P = c.P;
+  a.CL = c.CL;
+  if (c.P >= 2) {
+    size_t off = 0;
+    a.ckrow = (uint32_t *)(region + off);
+    off += align_up((size_t)d.batch * d.n_segments * d.k * 4);
+    a.dck = (int64_t *)(region + off);
+    off += align_up((size_t)d.batch * d.n_segments * 8);
+    a.rec = (SegRec *)(region + off);
+    off += align_up((size_t)d.batch * c.P * sizeof(SegRec));
+    a.endrow = (uint32_t *)(region + off);
+  }
   timer_begin(st);
-  if (d.n_last <= 4 && d.n_first <= 4) launch_seg_lm<4>(d, redge_dev, table, res, hdr, opt, status, st);
-  else launch_seg_lm<8>(d, redge_dev, table, res, hdr, opt, status, st);
+  if (d.n_last <= 4 && d.n_first <= 4) launch_seg_lm<4>(a, res, hdr, opt, status, st);
+  else launch_seg_lm<8>(a, res, hdr, opt, status, st);
   timer_end(st);
   return hipGetLastError();
 }

@@ -130,3 +130,69 @@ def test_repeat_is_bit_identical():
         b = run_seg(d["cost"], d["rbound"], d["last"], d["first"], d["redge"])
         for x, y in zip(a, b):
             np.testing.assert_array_equal(x, y)
+
+
+# Batches that leave SIMDs idle run each chain as chunks (rank convergence): one
+# workgroup per search, P = min(8, 1024 // B, N // 16) chunks of ceil(N / P) rows.
+def seg_chunks(N, B):
+    P = min(8, max(1, 1024 // B), N // 16)
+    return P if P >= 2 else 1
+
+
+def test_chunked_shapes_across_kernel_forms():
+    """The chunked path at K = 512 (16-bit argmins, eight states per lane) and
+    at K = 216 with six boundary strategies (the eight-class form)."""
+    need_gpu()
+    for seed, (B, N, P, S) in enumerate([(3, 40, 9, 2), (4, 48, 3, 6), (2, 64, 4, 3)]):
+        say("seg chunked", B, N, P, S)
+        assert seg_chunks(N, B) >= 2
+        cost, rbound, last, first, redge = seg_case([70, seed], B, N, P, S, 3, 10_000, 10_000_000)
+        assert_seg_parity(cost, rbound, last, first, redge, f"chunked B={B} N={N} K={S ** P}")
+
+
+def _class_chains(seed, B, N, E_mix, pattern):
+    """Plans whose first and last block strategies coincide (first = last = s mod 3) and
+    boundary table 0 that never moves a search between classes (0 on the diagonal, the
+    largest entry off it): over rows using table 0 the three classes run as separate
+    chains, so a run started anywhere else never becomes parallel to the true one.  The
+    other tables mix the classes.  pattern[p] says whether chunk p's rows use table 0."""
+    from paper_2504_00598_amd import cfp_r_limit, CFP_V_SEG
+    rs = np.random.default_rng(seed)
+    K, L = 12, 3
+    last = (np.arange(K) % L).astype(np.uint8)
+    first = last.copy()
+    cost = rs.integers(0, 10**6, size=(B, N, K)).astype(np.int32)
+    rbound = rs.integers(0, 10**5, size=(1 + E_mix, L, L)).astype(np.int32)
+    rbound[0] = cfp_r_limit(CFP_V_SEG, K) - 1
+    rbound[0][np.arange(L), np.arange(L)] = 0
+    P = seg_chunks(N, B)
+    CL = -(-N // P)
+    redge = rs.integers(1, 1 + E_mix, size=N).astype(np.int32)
+    for p, iso in enumerate(pattern):
+        if iso:
+            redge[p * CL:min((p + 1) * CL, N)] = 0
+    return cost, rbound, last, first, redge, P
+
+
+def test_chunked_rows_that_never_meet():
+    """Every row's table keeps the classes apart: no fix-up meets its chunk's
+    speculative rows, and the final pass reruns every chunk after the first."""
+    need_gpu()
+    say("seg chunks never meet")
+    cost, rbound, last, first, redge, P = _class_chains(71, 4, 64, 2, [True] * 8)
+    assert P == 4
+    assert_seg_parity(cost, rbound, last, first, redge, "never meet")
+
+
+@pytest.mark.parametrize("pattern", [(False, True, False, False), (False, True, True, False),
+                                     (True, False, True, False), (False, False, False, True)])
+def test_chunked_rows_that_meet_in_some_chunks(pattern):
+    """A chunk of class-separating rows leaves its successor's fix-up started from a
+    wrong row: that chunk is rerun from the true row, at least as far as its fix-up
+    went, and where the rerun meets the speculative rows the chunks after it count
+    again; two such chunks in a row chain the reruns."""
+    need_gpu()
+    say("seg chunks meet in some", pattern)
+    cost, rbound, last, first, redge, P = _class_chains([72, *pattern], 4, 64, 2, pattern)
+    assert P == 4
+    assert_seg_parity(cost, rbound, last, first, redge, f"pattern {pattern}")
