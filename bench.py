@@ -79,7 +79,7 @@ TRAFFIC = {
     "chain_wide_n512_k256": {"fetch_kib": 44184.9, "write_kib": 16425.8, "sources": "c125e5f6d9988dd4"},
     # mean over the 12 matrix-product launches of one forward call
     "scan_n4096_k512": {"fetch_kib": 3033680.5, "write_kib": 1398442.5, "sources": "1c91451c813b5cea"},
-    "seg_gpt_n96_k81": {"fetch_kib": 3956.4, "write_kib": 1952.0, "sources": "c10bb791ae973515"},
+    "seg_gpt_n96_k81": {"fetch_kib": 6322.8, "write_kib": 10135.6, "sources": "8be3413f022d76a0"},
     # the memory workload run as a budget frontier (every chunk of every search active)
     "mem_llama_n288_k32:frontier": {"fetch_kib": 166315.1, "write_kib": 442223.0, "sources": "b1c04725b6a0843d"},
     # the scan workload through the chain search (speculative pass)
