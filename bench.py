@@ -60,7 +60,7 @@ KERNELS = {
     # the scan workload through the chain search: speculative pass of the chunk-parallel form
     "scan_n4096_k512:chain": ("chain_cw_kernel<512,0>", ["chain_cw.hip", "chain_fwd_wide.hip"]),
     "scan_n4096_k512": ("scan_gemm_kernel", ["scan.hip"]),
-    "seg_gpt_n96_k81": ("seg_chunk_kernel<2, 4>", ["seg_fwd.hip"]),
+    "seg_gpt_n96_k81": ("seg_chunk_kernel<2, 4, true>", ["seg_fwd.hip"]),
 }
 COMMON_SOURCES = ["common.h", "cfp_internal.h", "../../include/cfp.h"]
 
@@ -79,7 +79,7 @@ TRAFFIC = {
     "chain_wide_n512_k256": {"fetch_kib": 44184.9, "write_kib": 16425.8, "sources": "c125e5f6d9988dd4"},
     # mean over the 12 matrix-product launches of one forward call
     "scan_n4096_k512": {"fetch_kib": 3033680.5, "write_kib": 1398442.5, "sources": "1c91451c813b5cea"},
-    "seg_gpt_n96_k81": {"fetch_kib": 6322.8, "write_kib": 10135.6, "sources": "8be3413f022d76a0"},
+    "seg_gpt_n96_k81": {"fetch_kib": 6338.9, "write_kib": 10137.1, "sources": "1d03d894fb522632"},
     # the memory workload run as a budget frontier (every chunk of every search active)
     "mem_llama_n288_k32:frontier": {"fetch_kib": 166315.1, "write_kib": 442223.0, "sources": "b1c04725b6a0843d"},
     # the scan workload through the chain search (speculative pass)

@@ -542,11 +542,11 @@ int cfp_dp_segments(const cfp_segment_desc *d, void *ws, size_t ws_bytes, int64_
   hipStream_t st = (hipStream_t)stream;
   uint8_t *w = (uint8_t *)ws;
   const cfp_chain_desc c = as_chain(d);
-  if ((rc = upload_header(&c, CFP_V_SEG, 0, L, ws, st)) != CFP_OK) return rc;
+  // the search kernels check the range of rbound themselves and read the edge
+  // map from the workspace only when it is too long for the kernel arguments
+  if (!seg_edges_in_args(d->n_segments, d->n_tables) && (rc = upload_header(&c, CFP_V_SEG, 0, L, ws, st)) != CFP_OK)
+    return rc;
   WsHeader *hdr = (WsHeader *)w;
-  if (launch_validate_range(d->rbound, (size_t)d->n_tables * d->n_last * d->n_first, cfp_r_limit(CFP_V_SEG, d->k),
-                            hdr, st) != hipSuccess)
-    return CFP_ERR_HIP;
   if (launch_seg_fwd(*d, (const int32_t *)(w + L.redge), w + L.table, w + L.seg, (SearchResult *)(w + L.result), hdr,
                      opt, status, st) != hipSuccess)
     return CFP_ERR_HIP;

@@ -74,8 +74,11 @@ hipError_t launch_validate_rtab(const int32_t *rtab, int e, int k, int32_t limit
                                 hipStream_t st);
 hipError_t launch_validate_range(const int32_t *a, size_t count, int32_t limit, WsHeader *hdr, hipStream_t st);
 bool seg_supported(int k, int n_last, int n_first);
-// Segment search: region of the chunk-parallel form (0 when one pass suffices).
+// Segment search: region of the chunk-parallel form (0 when one pass suffices);
+// whether the edge map travels in the kernel arguments (then nothing of the
+// header is read and no upload is needed).
 size_t seg_region_bytes(int n, int k, int batch);
+bool seg_edges_in_args(int n, int n_tables);
 hipError_t launch_seg_fwd(const cfp_segment_desc &d, const int32_t *redge_dev, uint8_t *table, uint8_t *region,
                           SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st);
 hipError_t launch_chain_fwd(const cfp_chain_desc &d, const int32_t *redge_dev, uint8_t *table, int elem,

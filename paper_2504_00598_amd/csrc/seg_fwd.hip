@@ -70,6 +70,7 @@ constexpr int kSegAhead = 8;     // rows in flight per lane
 constexpr int kSegMaxP = 8;      // chunks per search (waves of a workgroup)
 constexpr int kSegMinRows = 16;  // least rows per chunk
 constexpr int kSegSimds = 1024;  // SIMDs of the chip: waves at one per SIMD
+constexpr int kSegArgN = 1536;   // longest edge map carried in the kernel arguments (16-bit entries)
 
 // DPP controls: quad_perm [1,0,3,2] and [2,3,0,1] (lane ^ 1, lane ^ 2),
 // row_ror:4 and :8, row_half_mirror, row_mirror, row_newbcast:n.
@@ -135,7 +136,7 @@ struct SegArgs {
   const int32_t *rbound;  // [E][L][F]
   const uint8_t *last, *first;
   const int32_t *redge;   // device copy, entry 0 a valid table
-  int N, K, B, L, F, bits;
+  int N, K, B, E, L, F, bits;
   uint8_t *table;         // argmin entries [B][N][K], u8 or u16 (K > 256)
   // chunk-parallel form
   int P, CL;              // chunks per search, rows per chunk
@@ -143,7 +144,12 @@ struct SegArgs {
   int64_t *dck;           // speculative running sum of row minima from the chunk's first row [B][N]
   SegRec *rec;            // [B][P]
   uint32_t *endrow;       // fix-up end rows of chunks that met no speculative row [B][P][K]
+  // the edge map itself when N <= kSegArgN and E <= 65536 (no upload before the
+  // launch): entry i in the 16-bit half i % 2 of word i / 2, so that a scalar
+  // load reads it
+  uint32_t earg[kSegArgN / 2];
 };
+static_assert(sizeof(SegArgs) + 64 <= 4096, "the arguments of a launch fit one 4 KiB block");
 
 }  // namespace
 
@@ -164,7 +170,7 @@ struct SegArgs {
 // 2 b0 + b1; LM = 8: 4 b0 + 2 b1 + b2.  Boundary pair (l, f) sits in the lanes
 // of class l in group f: LM = 4, groups of 4 lanes, f = (lane / 4) % 4 (every
 // row holds all pairs); LM = 8, groups of 8 lanes, f = lane / 8.
-template <int SPL, int LM, int MODE>
+template <int SPL, int LM, int MODE, bool EA>
 __device__ __forceinline__ void seg_run(const SegArgs &a, int b, int r0, int r1, int lim, const uint32_t (&qs)[SPL],
                                         uint32_t (&q)[SPL], int64_t &o, uint32_t &rmax, int &stop, bool &bad) {
   static_assert(LM == 4 || LM == 8, "classes per boundary side");
@@ -240,13 +246,21 @@ __device__ __forceinline__ void seg_run(const SegArgs &a, int b, int r0, int r1,
   };
   auto row_off = [&](int i) __attribute__((always_inline)) { return min((uint32_t)i * K4, last_row); };
   auto edge_off = [&](int i) __attribute__((always_inline)) { return (uint32_t)min(i, N - 1) * 4u; };
+  // table index of row i's boundary (EA: from the kernel arguments)
+  auto edge_at = [&](int i) __attribute__((always_inline)) -> uint32_t {
+    if constexpr (EA) {
+      const int x = min(i, N - 1);
+      return (a.earg[x >> 1] >> (16 * (x & 1))) & 0xFFFFu;
+    }
+    else return load_e(edge_off(i));
+  };
   uint32_t rring[kSegAhead], ering[kSegAhead];
   int32_t c0[SPL];
   if constexpr (kFromCost) load_row(row_off(r0), c0);
 #pragma unroll
   for (int u = 0; u < kSegAhead; ++u) {
-    rring[u] = load_r(__builtin_amdgcn_readfirstlane(load_e(edge_off(f0 + u))));
-    ering[u] = load_e(edge_off(f0 + u + kSegAhead));
+    rring[u] = load_r(__builtin_amdgcn_readfirstlane(edge_at(f0 + u)));
+    ering[u] = edge_at(f0 + u + kSegAhead);
     load_row(row_off(f0 + u), ring[u]);
     if constexpr (kCompare) load_ck(row_off(f0 + u), kring[u]);
   }
@@ -411,7 +425,7 @@ __device__ __forceinline__ void seg_run(const SegArgs &a, int b, int r0, int r1,
     // below their last reads, so each ring slot stays in its registers)
     __builtin_amdgcn_sched_barrier(0);
     rring[U] = load_r(__builtin_amdgcn_readfirstlane(ering[U]));
-    ering[U] = load_e(edge_off(i + 2 * kSegAhead));
+    ering[U] = edge_at(i + 2 * kSegAhead);
     load_row(row_off(i + kSegAhead), ring[U]);
     const uint32_t rm = seg_wave_min_s(ym);
     if (valid) {  // uniform; no memory operation below
@@ -450,13 +464,17 @@ __device__ __forceinline__ void seg_run(const SegArgs &a, int b, int r0, int r1,
 }
 
 // Status and outputs of search b from its last normalised row (lane 0 writes).
+// Every boundary entry of every table must lie in [0, cap) (cfp_r_limit): the
+// E L F entries are checked here, once per search.
 template <int SPL>
 __device__ __forceinline__ void seg_finish(const SegArgs &a, int b, const uint32_t (&q)[SPL], int64_t o, bool bad,
                                            bool infeasible, SearchResult *__restrict__ res,
                                            const WsHeader *__restrict__ hdr, int64_t *__restrict__ opt,
                                            int32_t *__restrict__ status) {
   const int lane = threadIdx.x & 63;
-  const uint32_t IMASK = (1u << a.bits) - 1u;
+  const uint32_t IMASK = (1u << a.bits) - 1u, CAP = (1u << (32 - a.bits)) - 1u;
+  const int nr = a.E * a.L * a.F;
+  for (int x = lane; x < nr; x += 64) bad |= (uint32_t)a.rbound[x] >= CAP;
   // Lowest final state of least value (the least is 0 after normalisation).
   uint32_t pk = kSat;
 #pragma unroll
@@ -466,7 +484,7 @@ __device__ __forceinline__ void seg_finish(const SegArgs &a, int b, const uint32
   bad = __any(bad);
   if (lane == 0) {
     int st = CFP_ST_OK;
-    if (bad || hdr->rflag) st = CFP_ST_BADINPUT;
+    if (bad) st = CFP_ST_BADINPUT;
     else if (infeasible) st = CFP_ST_INFEASIBLE;
     else if ((fin >> a.bits) != 0) st = CFP_ST_OVERFLOW;
     status[b] = st;
@@ -478,7 +496,7 @@ __device__ __forceinline__ void seg_finish(const SegArgs &a, int b, const uint32
 }
 
 // Whole searches, one wave each.
-template <int SPL, int LM>
+template <int SPL, int LM, bool EA>
 __global__ __launch_bounds__(kSegWaves * 64) void seg_fwd_kernel(SegArgs a, SearchResult *__restrict__ res,
                                                                  const WsHeader *__restrict__ hdr,
                                                                  int64_t *__restrict__ opt,
@@ -490,14 +508,14 @@ __global__ __launch_bounds__(kSegWaves * 64) void seg_fwd_kernel(SegArgs a, Sear
   uint32_t rmax;
   int stop;
   bool bad;
-  seg_run<SPL, LM, kSegFull>(a, b, 0, a.N, 0, q, q, o, rmax, stop, bad);
+  seg_run<SPL, LM, kSegFull, EA>(a, b, 0, a.N, 0, q, q, o, rmax, stop, bad);
   seg_finish<SPL>(a, b, q, o, bad, rmax == kSat, res, hdr, opt, status);
 }
 
 // The final pass of search b (see the top of the file): the chunks' sums of
 // row minima, the reruns a chunk whose predecessor met no speculative row
 // needs, and the outputs.
-template <int SPL, int LM>
+template <int SPL, int LM, bool EA>
 __device__ __forceinline__ void seg_final(const SegArgs &a, int b, SearchResult *__restrict__ res,
                                           const WsHeader *__restrict__ hdr, int64_t *__restrict__ opt,
                                           int32_t *__restrict__ status) {
@@ -531,7 +549,7 @@ __device__ __forceinline__ void seg_final(const SegArgs &a, int b, SearchResult 
       uint32_t rmax;
       int stop;
       bool bad;
-      seg_run<SPL, LM, kSegRepair>(a, b, r0, r1, conv >= 0 ? conv : r1 - 1, t, q, o, rmax, stop, bad);
+      seg_run<SPL, LM, kSegRepair, EA>(a, b, r0, r1, conv >= 0 ? conv : r1 - 1, t, q, o, rmax, stop, bad);
       total += o;
       if (stop >= 0) {
         total += dk[r1 - 1] - dk[stop];
@@ -559,7 +577,7 @@ __device__ __forceinline__ void seg_final(const SegArgs &a, int b, SearchResult 
 // a workgroup share a compute unit, so a barrier also orders their global
 // stores and loads): every wave runs its chunk speculatively, waves 1..P-1
 // then fix up their chunks, and wave 0 runs the final pass.
-template <int SPL, int LM>
+template <int SPL, int LM, bool EA>
 __global__ __launch_bounds__(64 * kSegMaxP) void seg_chunk_kernel(SegArgs a, SearchResult *__restrict__ res,
                                                                   const WsHeader *__restrict__ hdr,
                                                                   int64_t *__restrict__ opt,
@@ -573,7 +591,7 @@ __global__ __launch_bounds__(64 * kSegMaxP) void seg_chunk_kernel(SegArgs a, Sea
     uint32_t rmax;
     int stop;
     bool bad;
-    seg_run<SPL, LM, kSegSpec>(a, b, r0, r1, 0, q, q, o, rmax, stop, bad);
+    seg_run<SPL, LM, kSegSpec, EA>(a, b, r0, r1, 0, q, q, o, rmax, stop, bad);
     bad = __any(bad);
     if (lane == 0) a.rec[(size_t)b * P + p].flags = (bad ? 1 : 0) | (rmax == kSat ? 2 : 0);
   }
@@ -588,7 +606,7 @@ __global__ __launch_bounds__(64 * kSegMaxP) void seg_chunk_kernel(SegArgs a, Sea
     uint32_t rmax;
     int stop;
     bool bad;
-    seg_run<SPL, LM, kSegFix>(a, b, r0, r1, r0, qs, q, o, rmax, stop, bad);
+    seg_run<SPL, LM, kSegFix, EA>(a, b, r0, r1, r0, qs, q, o, rmax, stop, bad);
     const size_t ri = (size_t)b * P + p;
     if (stop < 0) {
       uint32_t *er = a.endrow + ri * a.K;
@@ -602,7 +620,7 @@ __global__ __launch_bounds__(64 * kSegMaxP) void seg_chunk_kernel(SegArgs a, Sea
     }
   }
   __syncthreads();
-  if (p == 0) seg_final<SPL, LM>(a, b, res, hdr, opt, status);  // 3. final pass
+  if (p == 0) seg_final<SPL, LM, EA>(a, b, res, hdr, opt, status);  // 3. final pass
 }
 
 bool seg_supported(int k, int n_last, int n_first) {
@@ -625,25 +643,32 @@ SegPlan seg_plan(int n, int batch) {
   return SegPlan{(n + CL - 1) / CL, CL};
 }
 
-template <int SPL, int LM>
-void launch_seg_spl(const SegArgs &a, SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
-                    hipStream_t st) {
+template <int SPL, int LM, bool EA>
+void launch_seg_ea(const SegArgs &a, SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
+                   hipStream_t st) {
   const dim3 blk(kSegWaves * 64);
   auto grid = [](long waves) { return dim3((unsigned)((waves + kSegWaves - 1) / kSegWaves)); };
   if (a.P < 2) {
-    timed_launch(seg_fwd_kernel<SPL, LM>, grid(a.B), blk, 0, st, a, res, hdr, opt, status);
+    timed_launch(seg_fwd_kernel<SPL, LM, EA>, grid(a.B), blk, 0, st, a, res, hdr, opt, status);
     return;
   }
-  timed_launch(seg_chunk_kernel<SPL, LM>, dim3(a.B), dim3(64 * a.P), 0, st, a, res, hdr, opt, status);
+  timed_launch(seg_chunk_kernel<SPL, LM, EA>, dim3(a.B), dim3(64 * a.P), 0, st, a, res, hdr, opt, status);
+}
+
+template <int SPL, int LM>
+void launch_seg_spl(const SegArgs &a, bool ea, SearchResult *res, const WsHeader *hdr, int64_t *opt,
+                    int32_t *status, hipStream_t st) {
+  if (ea) launch_seg_ea<SPL, LM, true>(a, res, hdr, opt, status, st);
+  else launch_seg_ea<SPL, LM, false>(a, res, hdr, opt, status, st);
 }
 
 template <int LM>
-void launch_seg_lm(const SegArgs &a, SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status,
-                   hipStream_t st) {
-  if (a.K <= 64) launch_seg_spl<1, LM>(a, res, hdr, opt, status, st);
-  else if (a.K <= 128) launch_seg_spl<2, LM>(a, res, hdr, opt, status, st);
-  else if (a.K <= 256) launch_seg_spl<4, LM>(a, res, hdr, opt, status, st);
-  else launch_seg_spl<8, LM>(a, res, hdr, opt, status, st);
+void launch_seg_lm(const SegArgs &a, bool ea, SearchResult *res, const WsHeader *hdr, int64_t *opt,
+                   int32_t *status, hipStream_t st) {
+  if (a.K <= 64) launch_seg_spl<1, LM>(a, ea, res, hdr, opt, status, st);
+  else if (a.K <= 128) launch_seg_spl<2, LM>(a, ea, res, hdr, opt, status, st);
+  else if (a.K <= 256) launch_seg_spl<4, LM>(a, ea, res, hdr, opt, status, st);
+  else launch_seg_spl<8, LM>(a, ea, res, hdr, opt, status, st);
 }
 
 }  // namespace
@@ -658,9 +683,14 @@ size_t seg_region_bytes(int n, int k, int batch) {
   return off;
 }
 
+bool seg_edges_in_args(int n, int n_tables) { return n <= kSegArgN && n_tables <= 65536; }
+
 hipError_t launch_seg_fwd(const cfp_segment_desc &d, const int32_t *redge_dev, uint8_t *table, uint8_t *region,
                           SearchResult *res, const WsHeader *hdr, int64_t *opt, int32_t *status, hipStream_t st) {
   SegArgs a{};
+  const bool ea = seg_edges_in_args(d.n_segments, d.n_tables);
+  if (ea)  // entry 0 is never read as a boundary; keep it a valid table
+    for (int i = 1; i < d.n_segments; ++i) a.earg[i >> 1] |= (uint32_t)d.redge[i] << (16 * (i & 1));
   a.cost = d.cost;
   a.rbound = d.rbound;
   a.last = d.last;
@@ -669,6 +699,7 @@ hipError_t launch_seg_fwd(const cfp_segment_desc &d, const int32_t *redge_dev, u
   a.N = d.n_segments;
   a.K = d.k;
   a.B = d.batch;
+  a.E = d.n_tables;
   a.L = d.n_last;
   a.F = d.n_first;
   a.bits = index_bits(d.k);
@@ -687,8 +718,8 @@ hipError_t launch_seg_fwd(const cfp_segment_desc &d, const int32_t *redge_dev, u
     a.endrow = (uint32_t *)(region + off);
   }
   timer_begin(st);
-  if (d.n_last <= 4 && d.n_first <= 4) launch_seg_lm<4>(a, res, hdr, opt, status, st);
-  else launch_seg_lm<8>(a, res, hdr, opt, status, st);
+  if (d.n_last <= 4 && d.n_first <= 4) launch_seg_lm<4>(a, ea, res, hdr, opt, status, st);
+  else launch_seg_lm<8>(a, ea, res, hdr, opt, status, st);
   timer_end(st);
   return hipGetLastError();
 }

@@ -196,3 +196,14 @@ def test_chunked_rows_that_meet_in_some_chunks(pattern):
     cost, rbound, last, first, redge, P = _class_chains([72, *pattern], 4, 64, 2, pattern)
     assert P == 4
     assert_seg_parity(cost, rbound, last, first, redge, f"pattern {pattern}")
+
+
+@pytest.mark.parametrize("B,N,P,S", [(3, 1600, 2, 3), (520, 1600, 2, 2), (520, 50, 2, 3)])
+def test_edge_map_in_arguments_and_in_workspace(B, N, P, S):
+    """Chains of up to 1536 segments carry their edge map in the kernel
+    arguments; longer ones read the device copy uploaded with the header.  Both,
+    chunked (small batch) and one wave per search (B >= 512)."""
+    need_gpu()
+    say("seg edge map", B, N, P, S)
+    cost, rbound, last, first, redge = seg_case([73, B, N], B, N, P, S, 5, 10_000, 10_000_000)
+    assert_seg_parity(cost, rbound, last, first, redge, f"B={B} N={N} K={S ** P}")
