@@ -376,7 +376,10 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
     for (int h = 0; h < CH; ++h) {
       const uint32_t cv = cq[cur][h];
       cq[cur][h] = (uint32_t)cbase[h][(size_t)min(i + 2, r1) * K];
-      if (MODE == kCSpec) cor[h] |= cv;
+      if (MODE == kCSpec) {
+        cor[h] |= cv;
+        asm volatile("" : "+v"(cor[h]));  // kept in its step (not sunk behind the argmin stores)
+      }
       x[h] = (sin && cv != (uint32_t)CFP_COST_INF) ? (m[h] >> BITS) + cv : kCX;
       if (sin && hv[h] && i >= r0) tbase[h][(size_t)i * K] = (Arg)(m[h] & (KP - 1));
     }

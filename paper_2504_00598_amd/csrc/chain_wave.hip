@@ -449,7 +449,12 @@ __device__ __forceinline__ void wave_run(const WaveArgs &a, int bw, int nvalid, 
       if (MODE == kWFix && !live) continue;
       const uint32_t cv = cs[(J / 4) % 3][u][g];
       const bool avail = lane < K && cv != (uint32_t)CFP_COST_INF;
-      if (MODE == kWSpec) ch.cor[g] |= cv;
+      if (MODE == kWSpec) {
+        ch.cor[g] |= cv;
+        // kept in its row: sunk to the end of a block, the OR waits for the
+        // latest cost loads behind the block's argmin stores
+        asm volatile("" : "+v"(ch.cor[g]));
+      }
       const uint32_t x = avail ? (acc[g] >> kWBits) + cv : kWX;
       const uint32_t d = wave_min64_s(x);
       if (MODE == kWSpec && d == kWX) ch.flags[g] |= 2;
