@@ -174,18 +174,31 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
   };
   int hc[CH];  // chain of pair h
   bool hv[CH];
+  // A chain's rows start at a wave-uniform address (scalar registers); the
+  // thread's state adds one 32-bit byte offset, so no 64-bit address is held
+  // per chain in vector registers.
   const int32_t *cbase[CH];
   Arg *tbase[CH];
   uint32_t *ckb[CH];
 #pragma unroll
   for (int h = 0; h < CH; ++h) {
     hc[h] = TPS * h + sub;
-    const int b = pick(bs, h);
+    const int b = __builtin_amdgcn_readfirstlane(pick(bs, h));
     hv[h] = pick(valid, h);
-    cbase[h] = a.cost + (size_t)b * N * K + min(ms, K - 1);
-    tbase[h] = (Arg *)a.table + (size_t)b * N * K + ms;
-    ckb[h] = a.ckrow + (size_t)b * a.nq * KP + ms;
+    cbase[h] = a.cost + (size_t)b * N * K;
+    tbase[h] = (Arg *)a.table + (size_t)b * N * K;
+    ckb[h] = a.ckrow + (size_t)b * a.nq * KP;
   }
+  const uint32_t coff = (uint32_t)min(ms, K - 1) * 4u, toffb = (uint32_t)ms * (uint32_t)sizeof(Arg),
+                 koff = (uint32_t)ms * 4u;
+  auto cost_at = [&](int h, size_t row, uint32_t off) __attribute__((always_inline)) {
+    return *(const uint32_t *)((const char *)(cbase[h] + row * K) + off);
+  };
+  auto ck_at = [&](int h, size_t q) __attribute__((always_inline)) -> uint32_t & {
+    uint32_t off = koff;
+    asm volatile("" : "+v"(off));  // (no base + offset pair hoisted out of the loop, where it would spill)
+    return *(uint32_t *)((char *)(ckb[h] + q * KP) + off);
+  };
   // redge is read-only for the kernel's lifetime: read through the constant
   // address space, so a row's table index is one scalar load.
   const __attribute__((address_space(4))) int32_t *redge_c =
@@ -235,7 +248,7 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
     uint32_t x[CH], d[kCG];
 #pragma unroll
     for (int h = 0; h < CH; ++h) {
-      const uint32_t cv = (uint32_t)cbase[h][(size_t)rs * K];
+      const uint32_t cv = cost_at(h, (size_t)rs, coff);
       cor[h] = cv;
       x[h] = (sin && cv != (uint32_t)CFP_COST_INF) ? cv : kCX;
     }
@@ -253,7 +266,7 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
     if (i0 > r1) {  // a run of one row (rs = r0): the start row is its checkpoint
 #pragma unroll
       for (int h = 0; h < CH; ++h)
-        if (hv[h]) ckb[h][(size_t)(r0 / 4) * KP] = ch.x[h];
+        if (hv[h]) ck_at(h, (size_t)(r0 / 4)) = ch.x[h];
 #pragma unroll
       for (int c = 0; c < kCG; ++c)
         if (tid == c && valid[c]) a.dck[(size_t)bs[c] * a.nq + r0 / 4] = (int64_t)ch.dsum[c];
@@ -283,10 +296,10 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
   uint32_t cq[2][CH], ckv[CH];
 #pragma unroll
   for (int h = 0; h < CH; ++h) {
-    cq[0][h] = (uint32_t)cbase[h][(size_t)i0 * K];
-    cq[1][h] = (uint32_t)cbase[h][(size_t)min(i0 + 1, r1) * K];
+    cq[0][h] = cost_at(h, (size_t)i0, coff);
+    cq[1][h] = cost_at(h, (size_t)min(i0 + 1, r1), coff);
     ckv[h] = 0;
-    if (CHECK) ckv[h] = ckb[h][(size_t)(i0 >> 2) * KP];
+    if (CHECK) ckv[h] = ck_at(h, (size_t)(i0 >> 2));
   }
   __syncthreads();
 
@@ -375,13 +388,23 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
 #pragma unroll
     for (int h = 0; h < CH; ++h) {
       const uint32_t cv = cq[cur][h];
-      cq[cur][h] = (uint32_t)cbase[h][(size_t)min(i + 2, r1) * K];
       if (MODE == kCSpec) {
         cor[h] |= cv;
         asm volatile("" : "+v"(cor[h]));  // kept in its step (not sunk behind the argmin stores)
       }
       x[h] = (sin && cv != (uint32_t)CFP_COST_INF) ? (m[h] >> BITS) + cv : kCX;
-      if (sin && hv[h] && i >= r0) tbase[h][(size_t)i * K] = (Arg)(m[h] & (KP - 1));
+      if (sin && hv[h] && i >= r0)
+        *(Arg *)((char *)(tbase[h] + (size_t)i * K) + toffb) = (Arg)(m[h] & (KP - 1));
+    }
+    // The costs of row i + 2, into the registers just read.  The lane offset
+    // passes through an empty asm that also takes x[h], so the load cannot be
+    // issued before the last read of the old cost: the set keeps its registers
+    // and no register copy at the end of the loop waits for a load.
+#pragma unroll
+    for (int h = 0; h < CH; ++h) {
+      uint32_t off = coff;
+      asm volatile("" : "+v"(off) : "v"(x[h]));
+      cq[cur][h] = cost_at(h, (size_t)min(i + 2, r1), off);
     }
     uint32_t d[kCG];
     row_min(x, d);
@@ -401,7 +424,7 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
       if (MODE == kCSpec && i >= r0) {
 #pragma unroll
         for (int h = 0; h < CH; ++h)
-          if (hv[h]) ckb[h][(size_t)q * KP] = ch.x[h];
+          if (hv[h]) ck_at(h, (size_t)q) = ch.x[h];
 #pragma unroll
         for (int c = 0; c < kCG; ++c)
           if (tid == c && valid[c]) a.dck[(size_t)bs[c] * a.nq + q] = (int64_t)ch.dsum[c];
@@ -414,7 +437,7 @@ __device__ __forceinline__ void cw_run(const CwArgs &a, const int *bs, const boo
         }
         if (i < r1) {
 #pragma unroll
-          for (int h = 0; h < CH; ++h) ckv[h] = ckb[h][(size_t)(q + 1) * KP];
+          for (int h = 0; h < CH; ++h) ckv[h] = ck_at(h, (size_t)(q + 1));
         }
       }
     }
