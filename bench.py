@@ -73,17 +73,17 @@ COMMON_SOURCES = ["common.h", "cfp_internal.h", "../../include/cfp.h"]
 # changed and the figure is withheld.
 FETCH_SCALE, WRITE_SCALE = 524288.0 / 262166.9, 524288.0 / 524288.0
 TRAFFIC = {
-    "chain_gpt_n24_k16": {"fetch_kib": 12.7, "write_kib": 0.2, "sources": "08c51b7710b5e094"},
-    "chain_gpt_n1152_k64": {"fetch_kib": 37975.4, "write_kib": 37515.1, "sources": "b3609396e310cc0b"},
-    "mem_llama_n288_k32": {"fetch_kib": 127696.6, "write_kib": 338789.8, "sources": "b1c04725b6a0843d"},
-    "chain_wide_n512_k256": {"fetch_kib": 44184.9, "write_kib": 16425.8, "sources": "c125e5f6d9988dd4"},
+    "chain_gpt_n24_k16": {"fetch_kib": 12.7, "write_kib": 0.2, "sources": "52818aaa4e4934d4"},
+    "chain_gpt_n1152_k64": {"fetch_kib": 37976.1, "write_kib": 37516.8, "sources": "7611dbd3b031e2fb"},
+    "mem_llama_n288_k32": {"fetch_kib": 127247.8, "write_kib": 338789.8, "sources": "800a6f06f2b6bf9f"},
+    "chain_wide_n512_k256": {"fetch_kib": 45013.6, "write_kib": 16423.8, "sources": "5894d8e2dd5893bd"},
     # mean over the 12 matrix-product launches of one forward call
-    "scan_n4096_k512": {"fetch_kib": 3033680.5, "write_kib": 1398442.5, "sources": "1c91451c813b5cea"},
+    "scan_n4096_k512": {"fetch_kib": 3034309.5, "write_kib": 1398442.5, "sources": "2746a9b212acf5ef"},
     "seg_gpt_n96_k81": {"fetch_kib": 6338.9, "write_kib": 10137.1, "sources": "1d03d894fb522632"},
     # the memory workload run as a budget frontier (every chunk of every search active)
-    "mem_llama_n288_k32:frontier": {"fetch_kib": 166315.1, "write_kib": 442223.0, "sources": "b1c04725b6a0843d"},
+    "mem_llama_n288_k32:frontier": {"fetch_kib": 166120.7, "write_kib": 442222.8, "sources": "800a6f06f2b6bf9f"},
     # the scan workload through the chain search (speculative pass)
-    "scan_n4096_k512:chain": {"fetch_kib": 801691.1, "write_kib": 25992.0, "sources": "c125e5f6d9988dd4"},
+    "scan_n4096_k512:chain": {"fetch_kib": 790709.3, "write_kib": 24456.0, "sources": "5894d8e2dd5893bd"},
 }
 
 
