@@ -45,7 +45,8 @@ KERNEL_ROLE = {
     "chain_gpt_n24_k16": "the whole search (forward pass and traceback) in one launch",
     "chain_gpt_n1152_k64": "speculative pass only; forward_call_frac covers the whole forward call",
     "chain_wide_n512_k256": "speculative pass only; forward_call_frac covers the whole forward call",
-    "scan_n4096_k512:chain": "speculative pass only; forward_call_frac covers the whole forward call",
+    "scan_n4096_k512:chain": "speculative pass only (four workgroups per chunk, rows exchanged every step); "
+                             "forward_call_frac covers the whole forward call",
     "scan_n4096_k512": "the 12 min-plus matrix-product launches of the up-sweep",
     "seg_gpt_n96_k81": "the forward pass in one launch (speculative, fix-up and final passes of four chunks per search)",
 }
@@ -58,7 +59,7 @@ KERNELS = {
     # speculative pass of the chunk-parallel search
     "chain_wide_n512_k256": ("chain_cw_kernel<256,0>", ["chain_cw.hip", "chain_fwd_wide.hip"]),
     # the scan workload through the chain search: speculative pass of the chunk-parallel form
-    "scan_n4096_k512:chain": ("chain_cw_kernel<512,0>", ["chain_cw.hip", "chain_fwd_wide.hip"]),
+    "scan_n4096_k512:chain": ("chain_cx_kernel<0>", ["chain_cw.hip", "chain_fwd_wide.hip"]),
     "scan_n4096_k512": ("scan_gemm_kernel", ["scan.hip"]),
     "seg_gpt_n96_k81": ("seg_chunk_kernel<2, 4, true>", ["seg_fwd.hip"]),
 }
@@ -83,7 +84,7 @@ TRAFFIC = {
     # the memory workload run as a budget frontier (every chunk of every search active)
     "mem_llama_n288_k32:frontier": {"fetch_kib": 166120.7, "write_kib": 442222.8, "sources": "800a6f06f2b6bf9f"},
     # the scan workload through the chain search (speculative pass)
-    "scan_n4096_k512:chain": {"fetch_kib": 790709.3, "write_kib": 24456.0, "sources": "5894d8e2dd5893bd"},
+    "scan_n4096_k512:chain": {"fetch_kib": 277909.2, "write_kib": 89988.7, "sources": "ffbf0c8c71534897"},
 }
 
 
@@ -445,8 +446,10 @@ def measure(name: str, steps: int, warmup: int, cpu_s: float, frontier: bool = F
         b.record(r.stream)
     torch.cuda.synchronize()
     kern_ms, kern_launches = L.cfp_timer_stop()
-    fwd_ms = float(np.mean([a.elapsed_time(m) for a, m, _ in ev]))
-    tb_ms = float(np.mean([m.elapsed_time(b) for _, m, b in ev]))
+    # medians: an interval that opens while the GPU has caught up with the host
+    # also holds any host stall before the next launch (milliseconds, now and then)
+    fwd_ms = float(np.median([a.elapsed_time(m) for a, m, _ in ev]))
+    tb_ms = float(np.median([m.elapsed_time(b) for _, m, b in ev]))
     ms_per_step = wall * 1e3 / steps
 
     cells = cells_of(cfg, data)

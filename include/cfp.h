@@ -46,11 +46,13 @@
  *  - No global mutable state apart from the opt-in benchmarking timer and
  *    the static workspace of cfp_search_chain_noalloc (both declared
  *    below): calls on different streams with different workspaces may
- *    run concurrently.  Two paths wait on the device for other workgroups of
+ *    run concurrently.  Three paths wait on the device for other workgroups of
  *    the same launch and need them resident at the same time: the memory
- *    variant (cfp_dp_chain_mem, cfp_mem_frontier) and the split chain kernel
+ *    variant (cfp_dp_chain_mem, cfp_mem_frontier), the split chain kernel
  *    that cfp_dp_chain uses for K > 64 when the chunk-parallel kernels do not
- *    apply.  Their waits are bounded; if another long kernel keeps their
+ *    apply, and the chunk-parallel chain search for 256 < K <= 512 with at
+ *    most 8 searches (four workgroups per chunk exchange every row).  Their
+ *    waits are bounded; if another long kernel keeps their
  *    workgroups from being dispatched (a shared GPU, concurrent calls), a
  *    wait may expire and the search ends with CFP_ST_TIMEOUT, never with a
  *    wrong answer.
@@ -84,8 +86,9 @@ enum {
   CFP_ST_OK = 0,
   CFP_ST_INFEASIBLE = 1, /* no plan (all strategies unavailable at a block, or budget too small) */
   CFP_ST_OVERFLOW = 2,   /* reserved: device arithmetic left its exact range (not reachable with valid inputs) */
-  CFP_ST_TIMEOUT = 3,    /* a bounded device wait expired (memory variant, or the K > 64 split chain
-                            kernel, while other work held the GPU; see above) */
+  CFP_ST_TIMEOUT = 3,    /* a bounded device wait expired (memory variant, K > 64 split chain kernel,
+                            or 256 < K <= 512 chunk-parallel teams, while other work held the GPU;
+                            see above) */
   CFP_ST_BADINPUT = 4    /* a device array value is outside its documented range */
 };
 

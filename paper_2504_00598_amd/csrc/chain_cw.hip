@@ -90,7 +90,8 @@ struct CwShape {
 
 struct CwRec {
   int64_t dfix;   // fix-up pass: offset sum at the meeting checkpoint, or at the chunk end
-  int32_t flags;  // speculative pass: bit 0 a negative cost, bit 1 a row with no available strategy
+  int32_t flags;  // bit 0 a negative cost, bit 1 a row with no available strategy (speculative
+                  // pass); bit 2 a wait between the workgroups of a team expired
   int32_t conv;   // fix-up pass: quad of the meeting checkpoint, -1 if none
 };
 
@@ -104,6 +105,8 @@ struct CwArgs {
   int64_t *dck;            // speculative offset sum at every checkpoint [B][nq]
   uint32_t *ckrow;         // speculative row at every checkpoint [B][nq][KP]
   uint32_t *endrow;        // fix-up end row of chunks that met no checkpoint [B][P][KP]
+  uint64_t *xb;            // state-split teams: exchanged rows [team][slot][chain][KP]
+  int32_t *xflag;          // state-split teams: a member gave up waiting [team]
 };
 
 template <int KP>
@@ -516,6 +519,363 @@ __global__ __launch_bounds__(kCThreads, 1) void chain_cw_kernel(CwArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// State-split teams (KP = 512 with few searches).  Four chains fill one
+// workgroup, so a batch of a few searches leaves most compute units idle while
+// each workgroup streams the whole 1 MiB table of every step.  Here a team of
+// kXS workgroups carries the four chains of one chunk: part z computes the
+// states z W .. z W + W - 1 (W = KP / kXS) of all four chains and so streams
+// only those W columns of the table (a quarter).  After each row the parts
+// exchange their new values x[s] (before normalisation) as 64-bit words
+// (tag << 32) | x through device memory, every part gathers the whole row, and
+// all parts normalise it the same way, exactly as one workgroup would.  A
+// word's tag is its row (with the top bit set in the fix-up pass), and each
+// team has two slots used in turn: a part publishes row i + 2 only after it
+// has gathered row i + 1, which every part publishes only after gathering row
+// i, so a slot is never rewritten before every part has read it.  Every
+// decision that ends a run (the fix-up's meeting test) is taken by each part
+// on the whole row, so the parts of a team always run the same rows.  All the
+// workgroups of a launch must be resident at once (at most one per compute
+// unit); a wait that expires marks the team, and the search ends with
+// CFP_ST_TIMEOUT.
+
+constexpr int kXS = 4;                      // workgroups per team
+constexpr int kXW = 512 / kXS;              // states per part
+constexpr int kXSpin = 1 << 20;             // polls of one word before a part gives up
+constexpr uint32_t kXFixTag = 0x80000000u;  // tag bit of the fix-up pass
+constexpr int kXMaxGroups = 2;              // teams are used for at most 2 x 4 searches
+constexpr int kXQW = kXW + kXW / 8;         // padded LDS words of one part's states
+
+struct CxSmem {
+  uint32_t part[kCG][kCWaves][kXW];      // partial minima [chain][predecessor group][state of the part]
+  uint32_t q[2][kCG][CwShape<512>::QS];  // whole rows [buffer][chain][state, padded]
+  uint32_t wm[kCWaves];                  // wave minima of the new row (waves 2c and 2c+1 hold chain c)
+  int32_t wd[kCWaves];                   // fix-up: the wave found a state off the checkpoint
+  int32_t abort;                         // a wait expired, or another part of the team gave up
+};
+
+// A thread's view after the products: chain c = tid / W... of the four chains
+// (two waves each), state sl = tid % W of every part.
+struct CxChains {
+  uint32_t q[kXS];      // the chain's normalised, shifted values at states sl + z W, z = 0 .. kXS - 1
+  uint64_t dsum[kCG];   // offset sums since the start row (uniform)
+  int conv[kCG];        // fix-up: quad of the meeting checkpoint, -1 before
+  uint64_t dconv[kCG];  // fix-up: dsum at that checkpoint
+  uint32_t flags[kCG];  // speculative: bit 1 a row with no available strategy
+  uint32_t neg;         // speculative: OR of the thread's costs (bit 31: a negative cost)
+  bool aborted;
+};
+
+// Runs rows [r0, r1] of the team's chains in part z.  Speculative: the start
+// row r0 comes from its costs alone; argmins from row r0 + 1 and checkpoints
+// are written.  Fix-up: the start row (row r0 - 1) is start[c]; stops at the
+// first quad end where every real chain has met its checkpoint.
+// Element idx (wave-uniform) of a four-element array, by selects rather than a
+// dynamic index (which would move the array to scratch memory).
+template <typename T>
+__device__ __forceinline__ T sel4(const T (&v)[4], int idx) {
+  return idx == 0 ? v[0] : idx == 1 ? v[1] : idx == 2 ? v[2] : v[3];
+}
+
+template <int MODE>
+__device__ __forceinline__ void cx_run(const CwArgs &a, int z, int team, int grp, int r0, int r1, CxSmem &sm,
+                                       CxChains &ch) {
+  constexpr int KP = 512;
+  using S = CwShape<KP>;
+  constexpr int BITS = S::BITS;
+  constexpr uint32_t CAP = S::CAP;
+  constexpr int PG = S::PG;  // predecessors per wave
+  constexpr uint32_t PASS = MODE == kCFix ? kXFixTag : 0u;
+  const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int c = wid >> 1;          // the thread's chain after the products (uniform in the wave)
+  const int sl = tid & (kXW - 1);  // the thread's state within each part
+  const int N = a.N, K = a.K;
+  const int b = min(kCG * grp + c, a.B - 1);  // chains past the batch repeat the last search and write nothing
+  const bool hv = kCG * grp + c < a.B;
+  const int s = z * kXW + sl;      // the thread's own state (computed by this part)
+  const bool sin = s < K;
+  const int qsl = qpad(sl);        // LDS index of state zz W + sl: zz kXQW + qsl
+  const int32_t *cbase = a.cost + (size_t)b * N * K;
+  uint16_t *tbase = (uint16_t *)a.table + (size_t)b * N * K;
+  uint32_t *ckb = a.ckrow + (size_t)b * a.nq * KP;
+  uint64_t *xbt = a.xb + (size_t)team * 2 * kCG * KP;
+  const uint32_t coff = (uint32_t)min(s, K - 1) * 4u;
+  auto cost_at = [&](size_t row, uint32_t off) __attribute__((always_inline)) {
+    return *(const uint32_t *)((const char *)(cbase + row * K) + off);
+  };
+  const __attribute__((address_space(4))) int32_t *redge_c =
+      (const __attribute__((address_space(4))) int32_t *)a.redge;
+
+  // The step's table words of the wave's predecessors t = PG wid + j, states
+  // z W + 2 lane and z W + 2 lane + 1: one 8-byte load per predecessor, the
+  // whole step held in registers and loaded one step ahead.
+  const uint32_t toff = (uint32_t)(PG * wid * KP + z * kXW + 2 * lane) * 4u;
+  uint2 tb[PG];
+  auto tload = [&](int j, int row, uint32_t dep) __attribute__((always_inline)) {
+    const char *tab = (const char *)(a.rpk + (size_t)redge_c[row] * KP * KP);
+    // The lane offset is formed by an asm add that also takes a value computed
+    // from the register's last read: the load is issued after that read, and
+    // no offset is hoisted out of the loop (64 of them would not fit).  One
+    // 32-bit offset from the scalar base.
+    uint32_t off;
+    asm volatile("v_add_u32 %0, %1, %2" : "=v"(off) : "n"(j * KP * 4), "v"(toff), "v"(dep));
+    tb[j] = *(const uint2 *)(tab + off);
+  };
+
+  // Publishes the part's value x of row i and gathers the other parts' values
+  // of the same chain and state sl; returns the row's values in xv.
+  auto exchange = [&](int i, uint32_t x, uint32_t (&xv)[kXS]) __attribute__((always_inline)) {
+    const uint32_t tag = (uint32_t)i | PASS;
+    char *slot = (char *)(xbt + (size_t)((i & 1) * kCG + c) * KP);  // uniform
+    auto word = [&](int zz) __attribute__((always_inline)) {
+      uint32_t off = (uint32_t)sl * 8u;
+      asm volatile("" : "+v"(off));
+      return (uint64_t *)(slot + off + (uint32_t)(zz * kXW * 8));
+    };
+    __hip_atomic_store(word(z), ((uint64_t)tag << 32) | x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    bool ok[kXS];
+#pragma unroll
+    for (int zz = 0; zz < kXS; ++zz) {
+      ok[zz] = zz == z || ch.aborted;
+      xv[zz] = zz == z ? x : kCX;
+    }
+    int spins = 0;
+    while (true) {
+      // every word polled at once (the own word too: one round trip per poll)
+      uint64_t w[kXS];
+#pragma unroll
+      for (int zz = 0; zz < kXS; ++zz) w[zz] = __hip_atomic_load(word(zz), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      bool all = true;
+#pragma unroll
+      for (int zz = 0; zz < kXS; ++zz) {
+        if (!ok[zz] && (uint32_t)(w[zz] >> 32) == tag) {
+          xv[zz] = (uint32_t)w[zz];
+          ok[zz] = true;
+        }
+        all = all && ok[zz];
+      }
+      if (all) break;
+      ++spins;
+      // another part gave up (checked every 256 polls), or this wait expired
+      if (spins > kXSpin ||
+          ((spins & 255) == 0 && __hip_atomic_load(&a.xflag[team], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))) {
+        sm.abort = 1;
+        __hip_atomic_store(&a.xflag[team], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+  };
+
+  // Row minima of the four chains from the gathered values, the offsets, and
+  // the normalised row into LDS buffer NXT.  Ends with every thread past a barrier.
+  auto finish_row = [&](const uint32_t (&xv)[kXS], int nxt, uint32_t (&d)[kCG]) __attribute__((always_inline)) {
+    uint32_t m = umin(umin(xv[0], xv[1]), umin(xv[2], xv[3]));
+    m = cw_wave_min(m);
+    if (lane == 0) sm.wm[wid] = m;
+    __syncthreads();
+#pragma unroll
+    for (int cc = 0; cc < kCG; ++cc) d[cc] = __builtin_amdgcn_readfirstlane(umin(sm.wm[2 * cc], sm.wm[2 * cc + 1]));
+    ch.aborted = sm.abort != 0;
+    const uint32_t dc = sel4(d, c);
+#pragma unroll
+    for (int zz = 0; zz < kXS; ++zz) {
+      ch.q[zz] = umin(xv[zz] - dc, CAP) << BITS;
+      sm.q[nxt][c][zz * kXQW + qsl] = ch.q[zz];
+    }
+#pragma unroll
+    for (int cc = 0; cc < kCG; ++cc) ch.dsum[cc] += d[cc];
+  };
+
+#pragma unroll
+  for (int cc = 0; cc < kCG; ++cc) {
+    ch.flags[cc] = 0;
+    ch.conv[cc] = -1;
+    ch.dconv[cc] = 0;
+    ch.dsum[cc] = 0;
+  }
+  ch.neg = 0;
+  ch.aborted = false;
+  if (tid == 0) sm.abort = 0;
+  __syncthreads();
+  int i0;
+  if (MODE == kCSpec) {
+    // start row r0 from its costs alone
+    const uint32_t cv = cost_at((size_t)r0, coff);
+    ch.neg = cv;
+    uint32_t xv[kXS], d[kCG];
+    exchange(r0, (sin && cv != (uint32_t)CFP_COST_INF) ? cv : kCX, xv);
+    finish_row(xv, 0, d);
+#pragma unroll
+    for (int cc = 0; cc < kCG; ++cc)
+      if (d[cc] == kCX) ch.flags[cc] |= 2;
+    if (r0 == r1) {  // a run of one row: the start row is its checkpoint
+      if (hv) ckb[(size_t)(r0 / 4) * KP + s] = sel4(ch.q, z);
+      if (z == 0 && sl == 0 && (wid & 1) == 0 && hv) a.dck[(size_t)b * a.nq + r0 / 4] = (int64_t)sel4(ch.dsum, c);
+    }
+    i0 = r0 + 1;
+  } else {
+    // the start row: chunk p - 1's last checkpoint (row r0 - 1, a quad end)
+    const uint32_t *start = ckb + (size_t)(r0 / 4 - 1) * KP;
+#pragma unroll
+    for (int zz = 0; zz < kXS; ++zz) {
+      ch.q[zz] = start[zz * kXW + sl];
+      sm.q[0][c][zz * kXQW + qsl] = ch.q[zz];
+    }
+    i0 = r0;
+  }
+  __syncthreads();
+  if (i0 > r1 || ch.aborted) return;
+
+#pragma unroll
+  for (int j = 0; j < PG; ++j) tload(j, i0, 0);
+  // the own state's costs of the next two rows: step i uses set (i - i0) mod 2
+  uint32_t cq[2], ckv[kXS];
+  cq[0] = cost_at((size_t)i0, coff);
+  cq[1] = cost_at((size_t)min(i0 + 1, r1), coff);
+#pragma unroll
+  for (int zz = 0; zz < kXS; ++zz) ckv[zz] = MODE == kCFix ? ckb[(size_t)(i0 >> 2) * KP + zz * kXW + sl] : 0u;
+
+  // One row i with the previous row in LDS buffer CUR; returns true when the
+  // run is over (fix-up: every chain met; any mode: the team gave up).
+  auto step = [&](int i, auto Pc) __attribute__((always_inline)) -> bool {
+    constexpr int cur = decltype(Pc)::value, nxt = cur ^ 1;
+    const int inext = min(i + 1, r1);
+    uint32_t acc[kCG][2];
+#pragma unroll
+    for (int cc = 0; cc < kCG; ++cc) acc[cc][0] = acc[cc][1] = kSat;
+#pragma unroll
+    for (int j4 = 0; j4 < PG / 4; ++j4) {
+      u32x4 v[kCG];  // predecessors PG wid + 4 j4 .. + 3 of every chain (LDS broadcast reads)
+#pragma unroll
+      for (int cc = 0; cc < kCG; ++cc) v[cc] = *(const u32x4 *)&sm.q[cur][cc][qpad(PG * wid + 4 * j4)];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const uint2 w0 = tb[4 * j4 + 2 * h], w1 = tb[4 * j4 + 2 * h + 1];
+#pragma unroll
+        for (int cc = 0; cc < kCG; ++cc) {
+          const uint32_t va = h ? v[cc].z : v[cc].x, vb = h ? v[cc].w : v[cc].y;
+          acc[cc][0] = umin(umin(acc[cc][0], sat_add(va, w0.x)), sat_add(vb, w1.x));
+          acc[cc][1] = umin(umin(acc[cc][1], sat_add(va, w0.y)), sat_add(vb, w1.y));
+        }
+      }
+      // the four registers just read take the next row's words
+#pragma unroll
+      for (int u = 0; u < 4; ++u) tload(4 * j4 + u, inext, acc[u][u & 1]);
+    }
+    // minima over the eight predecessor groups through LDS
+#pragma unroll
+    for (int cc = 0; cc < kCG; ++cc) *(uint2 *)&sm.part[cc][wid][2 * lane] = make_uint2(acc[cc][0], acc[cc][1]);
+    __syncthreads();
+    uint32_t mv = sm.part[c][0][sl];
+#pragma unroll
+    for (int g = 1; g < kCWaves; ++g) mv = umin(mv, sm.part[c][g][sl]);
+    const uint32_t cv = cq[cur];
+    if (MODE == kCSpec) {
+      ch.neg |= cv;
+      asm volatile("" : "+v"(ch.neg));
+    }
+    const uint32_t x = (sin && cv != (uint32_t)CFP_COST_INF) ? (mv >> BITS) + cv : kCX;
+    if (sin && hv) *(uint16_t *)((char *)(tbase + (size_t)i * K) + (uint32_t)s * 2u) = (uint16_t)(mv & (KP - 1));
+    {
+      uint32_t off = coff;
+      asm volatile("" : "+v"(off) : "v"(x));
+      cq[cur] = cost_at((size_t)min(i + 2, r1), off);
+    }
+    uint32_t xv[kXS], d[kCG];
+    exchange(i, x, xv);
+    finish_row(xv, nxt, d);
+    if (MODE == kCSpec) {
+#pragma unroll
+      for (int cc = 0; cc < kCG; ++cc)
+        if (d[cc] == kCX) ch.flags[cc] |= 2;
+    }
+    const bool qend = (i & 3) == 3 || i == r1;
+    if (qend) {
+      const int q = i >> 2;
+      if (MODE == kCSpec) {
+        if (hv) ckb[(size_t)q * KP + s] = sel4(ch.q, z);
+        if (z == 0 && sl == 0 && (wid & 1) == 0 && hv) a.dck[(size_t)b * a.nq + q] = (int64_t)sel4(ch.dsum, c);
+      } else {
+        bool off = false;
+#pragma unroll
+        for (int zz = 0; zz < kXS; ++zz) off = off || ch.q[zz] != ckv[zz];
+        const uint64_t bal = __ballot(off);
+        if (lane == 0) sm.wd[wid] = bal != 0;
+        if (i < r1) {
+#pragma unroll
+          for (int zz = 0; zz < kXS; ++zz) ckv[zz] = ckb[(size_t)(q + 1) * KP + zz * kXW + sl];
+        }
+      }
+    }
+    __syncthreads();
+    if (MODE == kCFix && qend) {
+      const int q = i >> 2;
+      bool all = true;
+#pragma unroll
+      for (int cc = 0; cc < kCG; ++cc) {
+        const bool same = !sm.wd[2 * cc] && !sm.wd[2 * cc + 1];
+        if (ch.conv[cc] < 0 && same) {
+          ch.conv[cc] = q;
+          ch.dconv[cc] = ch.dsum[cc];
+        }
+        all = all && (ch.conv[cc] >= 0 || kCG * grp + cc >= a.B);
+      }
+      if (all) return true;
+    }
+    return ch.aborted;
+  };
+  for (int i = i0; i <= r1; i += 2) {
+    if (step(i, std::integral_constant<int, 0>{})) break;
+    if (i + 1 > r1 || step(i + 1, std::integral_constant<int, 1>{})) break;
+  }
+}
+
+// Clears the exchange slots and abort flags of every team and the flags of
+// every chunk record before a call's passes.
+__global__ void chain_cx_init_kernel(uint64_t *xb, size_t nxb, int32_t *xflag, int teams, CwRec *rec, int nrec) {
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t x = (size_t)blockIdx.x * blockDim.x + threadIdx.x; x < nxb; x += stride) xb[x] = ~0ull;
+  for (size_t x = (size_t)blockIdx.x * blockDim.x + threadIdx.x; x < (size_t)teams; x += stride) xflag[x] = 0;
+  for (size_t x = (size_t)blockIdx.x * blockDim.x + threadIdx.x; x < (size_t)nrec; x += stride) rec[x].flags = 0;
+}
+
+// Speculative (MODE kCSpec, grid (kXS, ceil(B/kCG), P)) and fix-up (kCFix,
+// grid (kXS, ceil(B/kCG), P-1)) passes of the state-split teams; part z is
+// blockIdx.x, so consecutive workgroups form a team.
+template <int MODE>
+__global__ __launch_bounds__(kCThreads, 1) void chain_cx_kernel(CwArgs a) {
+  __shared__ __align__(16) CxSmem sm;
+  const int z = blockIdx.x, grp = blockIdx.y;
+  const int p = MODE == kCFix ? blockIdx.z + 1 : blockIdx.z;
+  const int team = grp * a.P + p;
+  const int r0 = p * a.CL, r1 = min(r0 + a.CL, a.N) - 1;
+  CxChains ch;
+  cx_run<MODE>(a, z, team, grp, r0, r1, sm, ch);
+  const int tid = threadIdx.x, wid = __builtin_amdgcn_readfirstlane(tid >> 6), c = wid >> 1, sl = tid & (kXW - 1);
+  // flags of the run, one word per chain, ORed over the parts
+  int32_t fl[kCG];
+#pragma unroll
+  for (int cc = 0; cc < kCG; ++cc) {
+    fl[cc] = (MODE == kCSpec ? (int32_t)ch.flags[cc] : 0) | (ch.aborted ? 4 : 0);
+    if (MODE == kCSpec && __syncthreads_or(c == cc && (ch.neg >> 31))) fl[cc] |= 1;
+  }
+#pragma unroll
+  for (int cc = 0; cc < kCG; ++cc)
+    if (tid == cc && kCG * grp + cc < a.B && fl[cc]) atomicOr(&a.rec[(size_t)(kCG * grp + cc) * a.P + p].flags, fl[cc]);
+  if (MODE == kCFix) {
+    const int s = z * kXW + sl, bc = kCG * grp + c;
+    if (bc < a.B && sel4(ch.conv, c) < 0) a.endrow[((size_t)bc * a.P + p) * 512 + s] = sel4(ch.q, z);
+#pragma unroll
+    for (int cc = 0; cc < kCG; ++cc) {
+      if (z != 0 || tid != cc || kCG * grp + cc >= a.B) continue;
+      CwRec &r = a.rec[(size_t)(kCG * grp + cc) * a.P + p];
+      r.conv = ch.conv[cc];
+      r.dfix = (int64_t)(ch.conv[cc] >= 0 ? ch.dconv[cc] : ch.dsum[cc]);
+    }
+  }
+}
+
 // Final pass, one workgroup per search: the chunk offsets, the reruns after
 // chunks whose fix-up met no checkpoint, and the lowest optimal final state.
 template <int KP>
@@ -610,7 +970,8 @@ __global__ __launch_bounds__(kCThreads, 1) void chain_cw_final_kernel(CwArgs a, 
     for (int w = 1; w < kCWaves; ++w) fin = umin(fin, s_fin[w]);
     const int fl = s_flags;
     int st = CFP_ST_OK;
-    if ((fl & 1) || hdr->rflag) st = CFP_ST_BADINPUT;
+    if (fl & 4) st = CFP_ST_TIMEOUT;
+    else if ((fl & 1) || hdr->rflag) st = CFP_ST_BADINPUT;
     else if (fl & 2) st = CFP_ST_INFEASIBLE;
     else if ((fin >> S::BITS) != 0) st = CFP_ST_OVERFLOW;
     status[b] = st;
@@ -623,16 +984,35 @@ __global__ __launch_bounds__(kCThreads, 1) void chain_cw_final_kernel(CwArgs a, 
 
 struct CwPlan {
   int KP, P, CL, nq;
+  int S;  // workgroups per chunk and group of four searches: 1, or kXS for state-split teams
 };
 
+// Compute units of the current device (256 if the query fails, as on a host
+// without one, so that workspace sizes do not depend on it there).
+int cw_device_cus() {
+  static int cus = -1;
+  if (cus < 0) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cus = n;
+  }
+  return cus;
+}
+
 CwPlan cw_plan(int n, int k, int batch) {
-  CwPlan c{0, 0, 0, 0};
+  CwPlan c{0, 0, 0, 0, 1};
   if (k <= 128 || k > 512) return c;
   const int kp = k <= 256 ? 256 : 512;
   const int minrows = kp == 256 ? CwShape<256>::MINROWS : CwShape<512>::MINROWS;
   if (n < 2 * minrows) return c;
   const int groups = (batch + kCG - 1) / kCG;
-  int P = std::max(2, (256 + groups - 1) / groups);  // about one workgroup per compute unit
+  // K > 256 with at most two groups of four searches: state-split teams, every
+  // workgroup resident on its own compute unit.
+  const int cus = cw_device_cus();
+  const bool team = kp == 512 && groups <= kXMaxGroups && cus / (kXS * groups) >= 2;
+  int P = team ? cus / (kXS * groups) : std::max(2, (256 + groups - 1) / groups);  // about one workgroup per CU
   P = std::min(P, std::min(kCMaxChunks, n / minrows));
   int CL = ((n + P - 1) / P + 3) & ~3;
   P = (n + CL - 1) / CL;
@@ -641,6 +1021,7 @@ CwPlan cw_plan(int n, int k, int batch) {
   c.P = P;
   c.CL = CL;
   c.nq = (n + 3) / 4;
+  c.S = team ? kXS : 1;
   return c;
 }
 
@@ -652,6 +1033,18 @@ void launch_cw_kp(const CwArgs &a, int groups, const WsHeader *hdr, SearchResult
   timer_end(st);
   hipLaunchKernelGGL((chain_cw_kernel<KP, kCFix>), dim3(groups, a.P - 1), dim3(kCThreads), 0, st, a);
   hipLaunchKernelGGL(chain_cw_final_kernel<KP>, dim3(a.B), dim3(kCThreads), 0, st, a, hdr, res, opt, status);
+}
+
+void launch_cx(const CwArgs &a, int groups, const WsHeader *hdr, SearchResult *res, int64_t *opt, int32_t *status,
+               hipStream_t st) {
+  const int teams = groups * a.P;
+  hipLaunchKernelGGL(chain_cx_init_kernel, dim3(64), dim3(256), 0, st, a.xb, (size_t)teams * 2 * kCG * 512, a.xflag,
+                     teams, a.rec, a.B * a.P);
+  timer_begin(st);
+  timed_launch(chain_cx_kernel<kCSpec>, dim3(kXS, groups, a.P), dim3(kCThreads), 0, st, a);
+  timer_end(st);
+  hipLaunchKernelGGL(chain_cx_kernel<kCFix>, dim3(kXS, groups, a.P - 1), dim3(kCThreads), 0, st, a);
+  hipLaunchKernelGGL(chain_cw_final_kernel<512>, dim3(a.B), dim3(kCThreads), 0, st, a, hdr, res, opt, status);
 }
 
 }  // namespace
@@ -667,6 +1060,11 @@ size_t cw_region_bytes(int n, int k, int n_tables, int batch) {
   off += align_up((size_t)batch * c.nq * 8);
   off += align_up((size_t)batch * c.nq * kp * 4);
   off += align_up((size_t)batch * c.P * kp * 4);
+  if (c.S > 1) {
+    const size_t teams = (size_t)((batch + kCG - 1) / kCG) * c.P;
+    off += align_up(teams * 2 * kCG * kp * 8);
+    off += align_up(teams * 4);
+  }
   return off;
 }
 
@@ -695,10 +1093,19 @@ hipError_t launch_chain_cw(const cfp_chain_desc &d, const int32_t *redge_dev, ui
   a.ckrow = (uint32_t *)(region + off);
   off += align_up((size_t)d.batch * c.nq * kp * 4);
   a.endrow = (uint32_t *)(region + off);
+  off += align_up((size_t)d.batch * c.P * kp * 4);
+  const int groups = (d.batch + kCG - 1) / kCG;
+  a.xb = nullptr;
+  a.xflag = nullptr;
+  if (c.S > 1) {
+    a.xb = (uint64_t *)(region + off);
+    off += align_up((size_t)groups * c.P * 2 * kCG * kp * 8);
+    a.xflag = (int32_t *)(region + off);
+  }
   launch_pack_rtab(d.rtab, d.n_tables, d.k, (int)kp, kp == 256 ? CwShape<256>::BITS : CwShape<512>::BITS, rpk, st,
                    cfp_r_limit(CFP_V_CHAIN, d.k), const_cast<WsHeader *>(hdr));
-  const int groups = (d.batch + kCG - 1) / kCG;
-  if (kp == 256) launch_cw_kp<256>(a, groups, hdr, res, opt, status, st);
+  if (c.S > 1) launch_cx(a, groups, hdr, res, opt, status, st);
+  else if (kp == 256) launch_cw_kp<256>(a, groups, hdr, res, opt, status, st);
   else launch_cw_kp<512>(a, groups, hdr, res, opt, status, st);
   return hipGetLastError();
 }

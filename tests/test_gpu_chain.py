@@ -429,11 +429,14 @@ def test_range_flag_ignores_stale_workspace_bytes():
 # 256 < K <= 512 on chains of at least 128 blocks runs chunk-parallel with chunks of at
 # least 64 rows (runs take tens of rows to become parallel at this width).  The final
 # pass reruns, whole, each chunk that follows one whose fix-up met no checkpoint.
+# Batches of at most 8 searches run in state-split teams (four workgroups per chunk,
+# rows exchanged every step); larger batches carry four searches per workgroup.
 
 @pytest.mark.parametrize("N,K,B", [(128, 512, 1), (300, 400, 5), (1000, 512, 3), (640, 300, 8), (129, 257, 2),
-                                   (4096, 512, 1)])
+                                   (4096, 512, 1), (700, 512, 12), (300, 300, 9), (1200, 511, 7)])
 def test_chunked_k512_shapes(N, K, B):
-    """Two chunks of 64 rows, ragged K and batches, ragged last chunks, 64 chunks."""
+    """Two chunks of 64 rows, ragged K and batches, ragged last chunks, 64 chunks;
+    teams of one and two groups of searches, and four searches per workgroup."""
     need_gpu()
     from paper_2504_00598_amd import cfp_r_limit
     rhi = min(1_000_000, cfp_r_limit(0, K))
