@@ -77,14 +77,14 @@ TRAFFIC = {
     "chain_gpt_n24_k16": {"fetch_kib": 12.7, "write_kib": 0.2, "sources": "52818aaa4e4934d4"},
     "chain_gpt_n1152_k64": {"fetch_kib": 37976.1, "write_kib": 37516.8, "sources": "7611dbd3b031e2fb"},
     "mem_llama_n288_k32": {"fetch_kib": 127247.8, "write_kib": 338789.8, "sources": "800a6f06f2b6bf9f"},
-    "chain_wide_n512_k256": {"fetch_kib": 45494.0, "write_kib": 16414.9, "sources": "ffbf0c8c71534897"},
+    "chain_wide_n512_k256": {"fetch_kib": 45109.3, "write_kib": 16423.7, "sources": "fabd52fde0631d42"},
     # mean over the 12 matrix-product launches of one forward call
     "scan_n4096_k512": {"fetch_kib": 3034309.5, "write_kib": 1398442.5, "sources": "2746a9b212acf5ef"},
     "seg_gpt_n96_k81": {"fetch_kib": 6338.9, "write_kib": 10137.1, "sources": "1d03d894fb522632"},
     # the memory workload run as a budget frontier (every chunk of every search active)
     "mem_llama_n288_k32:frontier": {"fetch_kib": 166120.7, "write_kib": 442222.8, "sources": "800a6f06f2b6bf9f"},
     # the scan workload through the chain search (speculative pass)
-    "scan_n4096_k512:chain": {"fetch_kib": 277909.2, "write_kib": 89988.7, "sources": "ffbf0c8c71534897"},
+    "scan_n4096_k512:chain": {"fetch_kib": 290919.0, "write_kib": 89986.2, "sources": "fabd52fde0631d42"},
 }
 
 

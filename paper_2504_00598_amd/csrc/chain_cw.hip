@@ -541,7 +541,7 @@ __global__ __launch_bounds__(kCThreads, 1) void chain_cw_kernel(CwArgs a) {
 
 constexpr int kXS = 4;                      // workgroups per team
 constexpr int kXW = 512 / kXS;              // states per part
-constexpr int kXSpin = 1 << 20;             // polls of one word before a part gives up
+constexpr int kXSpin = 1 << 20;             // poll rounds before a part gives up
 constexpr uint32_t kXFixTag = 0x80000000u;  // tag bit of the fix-up pass
 constexpr int kXMaxGroups = 2;              // teams are used for at most 2 x 4 searches
 constexpr int kXQW = kXW + kXW / 8;         // padded LDS words of one part's states
@@ -640,11 +640,10 @@ __device__ __forceinline__ void cx_run(const CwArgs &a, int z, int team, int grp
       xv[zz] = zz == z ? x : kCX;
     }
     int spins = 0;
-    while (true) {
-      // every word polled at once (the own word too: one round trip per poll)
-      uint64_t w[kXS];
-#pragma unroll
-      for (int zz = 0; zz < kXS; ++zz) w[zz] = __hip_atomic_load(word(zz), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // Every word is polled at once (the own word too), and twice, a few hundred
+    // cycles apart: a word that lands just after the first poll left is seen
+    // by the second rather than a whole round trip later.
+    auto take = [&](const uint64_t (&w)[kXS]) __attribute__((always_inline)) {
       bool all = true;
 #pragma unroll
       for (int zz = 0; zz < kXS; ++zz) {
@@ -654,7 +653,16 @@ __device__ __forceinline__ void cx_run(const CwArgs &a, int z, int team, int grp
         }
         all = all && ok[zz];
       }
-      if (all) break;
+      return all;
+    };
+    while (true) {
+      uint64_t w[kXS], w2[kXS];
+#pragma unroll
+      for (int zz = 0; zz < kXS; ++zz) w[zz] = __hip_atomic_load(word(zz), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __builtin_amdgcn_s_sleep(4);
+#pragma unroll
+      for (int zz = 0; zz < kXS; ++zz) w2[zz] = __hip_atomic_load(word(zz), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (take(w) || take(w2)) break;
       ++spins;
       // another part gave up (checked every 256 polls), or this wait expired
       if (spins > kXSpin ||
