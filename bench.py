@@ -423,7 +423,7 @@ def measure(name: str, steps: int, warmup: int, cpu_s: float, frontier: bool = F
 
     # Timed region: K whole steps (forward + traceback) with nothing else on the
     # stream; an event record costs several microseconds of GPU time, so the
-    # per-phase split and the kernel timer come from a second, instrumented pass.
+    # per-phase split and the kernel timer come from further, instrumented passes.
     t0 = time.perf_counter()
     for _ in range(steps):
         r.forward()
@@ -431,12 +431,26 @@ def measure(name: str, steps: int, warmup: int, cpu_s: float, frontier: bool = F
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
+    # The library brackets each launch of the dominant kernel with HIP events
+    # attached to its dispatch, on the stream it is launched on.  The timer is
+    # armed for one step at a time (128 events; cfp_timer_stop waits for them):
+    # armed once for all the steps, with thousands of fresh events, some timed
+    # launches showed millisecond stalls that neither the kernel trace nor a
+    # per-step timer ever shows.
+    L = r.L
+    kern_ms, kern_launches = 0.0, 0
+    for _ in range(steps):
+        L.cfp_timer_start(64)
+        r.forward()
+        r.traceback()
+        ms, n = L.cfp_timer_stop()
+        kern_ms += ms
+        kern_launches += n
+    # The forward call and the traceback by stream events, the timer off.
+    # Medians: an interval that opens while the GPU has caught up with the host
+    # also holds any host stall before the next launch (milliseconds, now and then).
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
            torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-    # the library brackets each launch of the dominant kernel with HIP events
-    # on the stream it is launched on
-    L = r.L
-    L.cfp_timer_start(steps * 64)
     torch.cuda.synchronize()
     for a, m, b in ev:
         a.record(r.stream)
@@ -445,9 +459,6 @@ def measure(name: str, steps: int, warmup: int, cpu_s: float, frontier: bool = F
         r.traceback()
         b.record(r.stream)
     torch.cuda.synchronize()
-    kern_ms, kern_launches = L.cfp_timer_stop()
-    # medians: an interval that opens while the GPU has caught up with the host
-    # also holds any host stall before the next launch (milliseconds, now and then)
     fwd_ms = float(np.median([a.elapsed_time(m) for a, m, _ in ev]))
     tb_ms = float(np.median([m.elapsed_time(b) for _, m, b in ev]))
     ms_per_step = wall * 1e3 / steps
