@@ -479,6 +479,38 @@ def test_chunked_k512_some_chunks_meet(seed):
     assert_chain_parity(cost, rtab, redge, f"K>256 partial seed={seed}")
 
 
+def test_teams_ignore_stale_exchange_words():
+    """Batches of at most 8 searches with 256 < K <= 512 run in state-split
+    teams that exchange rows as step-tagged words in the workspace.  A
+    workspace of zeros (words whose tags name row 0), of all-ones, or left by
+    a call on other inputs must still give the oracle's answers."""
+    need_gpu()
+    import torch
+    from paper_2504_00598_amd import _lib as L, search
+    say("teams with stale exchange words")
+    rs = np.random.default_rng(64)
+    B, N, K = 3, 500, 400
+    runs = []
+    for _ in range(2):
+        cost = rs.integers(10_000, 1_000_000, size=(B, N, K)).astype(np.int32)
+        rtab = rs.integers(10_000, 1_000_000, size=(12, K, K)).astype(np.int32)
+        rtab[:, np.arange(K), np.arange(K)] = 0
+        redge = rs.integers(0, 12, size=N).astype(np.int32)
+        o_opt, o_plan, o_st = O.chain(cost, rtab, redge, nthreads=oracle_threads())
+        runs.append((dev(cost), dev(rtab), redge, o_opt, o_plan, o_st))
+    nbytes = L.cfp_workspace_bytes(L.Desc(runs[0][0], runs[0][1], runs[0][2]), L.CFP_V_CHAIN)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    for fill in (0, 0xFF, 0x01):
+        ws.fill_(fill)
+        for j in (0, 1, 0):
+            c, r, e, o_opt, o_plan, o_st = runs[j]
+            res = search.dp_chain(c, r, e, ws=ws)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(res.status.cpu().numpy(), o_st, err_msg=f"status, fill {fill} input {j}")
+            np.testing.assert_array_equal(res.opt.cpu().numpy(), o_opt, err_msg=f"opt, fill {fill} input {j}")
+            np.testing.assert_array_equal(res.plan.cpu().numpy(), o_plan, err_msg=f"plan, fill {fill} input {j}")
+
+
 def test_chunked_k512_ties_and_statuses():
     """Tie-heavy values, unavailable strategies, an infeasible search and a negative cost."""
     need_gpu()
