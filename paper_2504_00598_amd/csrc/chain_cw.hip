@@ -34,7 +34,9 @@
 //
 // The table stream is what bounds a step: KP^2 words per workgroup and step
 // from the cache hierarchy (the step time does not change with the number of
-// workgroups), hence four chains per workgroup.  Chunks are at least 16 rows
+// workgroups), hence four chains per workgroup.  At KP = 512 a batch of at
+// most eight searches would leave most compute units idle; there teams of
+// four workgroups split the states of each chunk (state-split teams, below).  Chunks are at least 16 rows
 // long at KP = 256 and 64 at KP = 512, where runs take longer to become
 // parallel (tens of rows on random costs).
 //
