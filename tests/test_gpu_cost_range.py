@@ -57,8 +57,9 @@ CHAIN_CASES = [
     (300, 48, 20, 12, False, "chunk-parallel K<=64"),
     (200, 256, 9, 12, True, "chunk-parallel K<=256"),
     (100, 200, 3, 5, False, "chunk-parallel K<=256, ragged K"),
-    (200, 512, 4, 12, True, "chunk-parallel K<=512"),
-    (130, 300, 3, 7, False, "chunk-parallel K<=512, ragged K"),
+    (200, 512, 4, 12, True, "chunk-parallel K<=512, state-split teams"),
+    (130, 300, 3, 7, False, "chunk-parallel K<=512, ragged K, state-split teams"),
+    (200, 400, 12, 12, False, "chunk-parallel K<=512, four searches per workgroup"),
     (100, 100, 4, 12, False, "split, tables in registers"),
     (30, 512, 2, 12, False, "split K=512"),
     (60, 100, 8, 17, False, "split, streamed tables"),
