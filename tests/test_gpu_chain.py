@@ -447,6 +447,18 @@ def test_chunked_k512_shapes(N, K, B):
     assert_chain_parity(cost, rtab, redge, f"chunked K>256 N={N} K={K} B={B}")
 
 
+@pytest.mark.parametrize("N,K,B", [(1089, 512, 1), (1090, 400, 5), (1091, 512, 3)])
+def test_chunked_k512_short_last_chunk(N, K, B):
+    """17 chunks of 68 rows and a last chunk of 1, 2 or 3 rows (a run of one
+    row is its own checkpoint), in state-split teams of one and two groups."""
+    need_gpu()
+    from paper_2504_00598_amd import cfp_r_limit
+    rhi = min(1_000_000, cfp_r_limit(0, K))
+    cost, rtab, redge = rand_case([52, N, K, B], B, N, K, 12, 10_000, 1_000_000, rlo=10_000, rhi=rhi)
+    say("chunked K>256, short last chunk", N, K, B)
+    assert_chain_parity(cost, rtab, redge, f"short last chunk N={N} K={K} B={B}")
+
+
 @pytest.mark.parametrize("K,B", [(512, 2), (300, 5)])
 def test_chunked_k512_rows_never_meet(K, B):
     """No chunk meets its checkpoints: every chunk after the first is rerun in turn."""
